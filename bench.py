@@ -1,0 +1,252 @@
+"""Benchmark: fused CIS loss forward+backward on one MI355X.
+
+Workload (default): the MoE-rollout batch, T = 16384 packed tokens, V = 151936, bf16 logits,
+c = 1 (lambda = e - 1), kappa = 5e-3 (see workloads/synth.py). Inputs are generated on the GPU
+before the timed region; a step is one call of the fused loss (every row: log-softmax, CIS
+weight, loss term, gradient) through the C ABI with preallocated outputs.
+
+Prints one JSON line. `roofline` refers to the fused row kernel: algorithmic bytes per launch
+(read the logits once, write the gradient once, plus the per-token inputs and outputs) divided by
+the average call time measured with HIP events on the stream the kernels run on (the call also
+contains the tiny loss-reduction kernel, so this slightly understates the row kernel's rate).
+`cpu_baseline` times the float64 CPU oracle on a bounded sample of the same rows, on the host's
+cores.
+
+    python bench.py [--steps K] [--warmup W] [--c C] [--mode bwd|fwd] [--no-cpu-baseline]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "tokens/sec and achieved HBM GB/s, CIS loss fwd+bwd, V=151936, 1 MI355X"
+PER_TOKEN_SCALAR_BYTES = 30   # ids 8 + mask 1 + l_infer 4 + A 4 in; l_train 4 + w 4 + trunc 1 + term 4 out
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("paper_2609_32444_amd/csrc/cis_kernels.hip", "paper_2609_32444_amd/csrc/cis_api.cpp",
+              "paper_2609_32444_amd/csrc/cis_internal.h"):
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(T_valid: int, T_invalid: int, V: int, esize: int, bwd: bool) -> int:
+    per_valid = esize * V * (2 if bwd else 1) + PER_TOKEN_SCALAR_BYTES
+    per_invalid = (esize * V if bwd else 0) + 9
+    return T_valid * per_valid + T_invalid * per_invalid
+
+
+def hbm_traffic(mode: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter passes, if they were taken on the
+    current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+        e = rec[mode][workload]
+        if e.get("source_hash") != kernel_source_hash():
+            return None
+        return int(e["bytes_per_launch"])
+    except Exception:
+        return None
+
+
+def copy_ceiling_gbs(nbytes: int, torch) -> float:
+    """Device-to-device copy of nbytes (read + write) as a measured bandwidth ceiling."""
+    n = nbytes // 2
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 5
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    return 2 * n / (ms * 1e-3) / 1e9
+
+
+def cpu_baseline(b, V: int, target_s: float = 15.0):
+    """The oracle as it stands (float64, with the gradient) on a sample of rows, in a process
+    pool over the host cores; sized to roughly target_s of CPU time."""
+    import multiprocessing as mp
+
+    import numpy as np
+
+    from oracle import cis as O
+
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    cores = max(1, min(cores, 16))
+    # probe one row to size the sample
+    rows_all = np.nonzero(b.mask.cpu().numpy())[0]
+    rng = np.random.default_rng(0)
+    probe = rows_all[:2]
+    import torch
+    zp = O.Bf16Matrix(b.logits[torch.as_tensor(probe, device=b.logits.device)].contiguous()
+                      .view(torch.int16).cpu().numpy().view(np.uint16))
+    t0 = time.perf_counter()
+    O.cis_loss(zp, b.ids[probe].cpu().numpy(), b.logp_infer[probe].cpu().double().numpy(),
+               b.adv[probe].cpu().double().numpy(), None, b.lam, b.kappa, b.scale)
+    per_row = (time.perf_counter() - t0) / len(probe)
+    n = int(min(len(rows_all), max(cores * 4, target_s / max(per_row, 1e-6))))
+    n = max(cores, (n // cores) * cores)
+    rows = np.sort(rng.choice(rows_all, size=n, replace=False))
+    bits = b.logits[torch.as_tensor(rows, device=b.logits.device)].contiguous() \
+        .view(torch.int16).cpu().numpy().view(np.uint16)
+    ids = b.ids.cpu().numpy()[rows]
+    linf = b.logp_infer.cpu().double().numpy()[rows]
+    adv = b.adv.cpu().double().numpy()[rows]
+    global _BASE
+    _BASE = (bits, ids, linf, adv, float(np.float32(b.lam)), float(np.float32(b.kappa)),
+             float(np.float32(b.scale)))
+    blocks = np.array_split(np.arange(n), cores)
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(cores) as pool:
+        pool.map(_baseline_worker, blocks)
+    dt = time.perf_counter() - t0
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": n / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n} random valid rows of the same batch, float64 oracle with gradient, "
+                      f"{cores} worker processes, {dt:.1f} s wall ({per_row * n:.0f} s CPU est.)",
+            "cpu_model": model}
+
+
+_BASE = None
+
+
+def _baseline_worker(idx):
+    from oracle import cis as O
+    bits, ids, linf, adv, lam, kappa, scale = _BASE
+    O.cis_loss(O.Bf16Matrix(bits[idx]), ids[idx], linf[idx], adv[idx], None, lam, kappa, scale,
+               with_grad=True)
+    return len(idx)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--c", type=float, default=1.0)
+    ap.add_argument("--mode", choices=("bwd", "fwd"), default="bwd")
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-copy-ceiling", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the CIS loss is measured on one MI355X "
+              "(multi-GPU sharding is a design note only)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_32444_amd as cis
+    from workloads import make_batch
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    b = make_batch(args.config, device="cuda", c=args.c)
+    torch.cuda.synchronize()
+    bwd = args.mode == "bwd"
+    call = cis.LossCall(b.logits, b.ids, b.logp_infer, b.adv, b.mask, lam=b.lam, kappa=b.kappa,
+                        scale=b.scale, bwd=bwd)
+    for _ in range(args.warmup):
+        call.run()
+    torch.cuda.synchronize()
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    t_all0 = torch.cuda.Event(enable_timing=True)
+    t_all1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_all0.record()
+    for i in range(args.steps):
+        starts[i].record()
+        call.run()
+        ends[i].record()
+    t_all1.record()
+    torch.cuda.synchronize()
+    total_ms = t_all0.elapsed_time(t_all1)
+    per_call = sorted(s.elapsed_time(e) for s, e in zip(starts, ends))
+    avg_call_ms = sum(per_call) / len(per_call)
+    ms_per_step = total_ms / args.steps
+
+    stats = cis.read_stats(call.workspace)
+    n_valid = stats["n_valid"]
+    T, V = b.T, b.V
+    esize = b.logits.element_size()
+    alg = algorithmic_bytes(n_valid, T - n_valid, V, esize, bwd)
+    achieved_gbs = alg / (avg_call_ms * 1e-3) / 1e9
+    tokens_per_s = n_valid / (ms_per_step * 1e-3)
+
+    workload = f"{b.meta['name']} T={T} V={V} {'bf16' if esize == 2 else 'fp32'} c={args.c:g} " \
+               f"kappa={b.kappa:g} {'fused fwd+bwd' if bwd else 'forward only'}"
+    traffic = hbm_traffic(args.mode, f"cfg{args.config}")
+    line = {
+        "metric": METRIC if bwd else METRIC.replace("fwd+bwd", "fwd"),
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if esize == 2 else "f32",
+        "data": "synthetic",
+        "config": {"workload": workload, "T": T, "V": V, "valid_tokens": n_valid,
+                   "lambda": b.lam, "kappa": b.kappa, "seed": b.meta["seed"]},
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved_gbs,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved_gbs / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": alg,
+            "avg_call_ms": avg_call_ms,
+            "min_call_ms": per_call[0],
+            "kernel_source": kernel_source_hash(),
+        },
+    }
+    if not args.no_copy_ceiling:
+        line["roofline"]["copy_ceiling_gbs"] = copy_ceiling_gbs(min(alg, 8 << 30), torch)
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(b, V)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,160 @@
+/*
+ * cis.h — C ABI of the MI355X (gfx950) calibrated-importance-sampling (CIS) token loss.
+ *
+ * Operation (Yu et al., "Rethinking Training-Inference Mismatch in LLM Reinforcement
+ * Learning", arXiv 2609.32444):
+ *
+ *   For every token row t with training logits z_t[0..V), sampled id y_t, the inference
+ *   engine's recorded log-probability l_infer_t (raw, from the sampling step), advantage A_t
+ *   and mask m_t:
+ *
+ *     l_train_t = log softmax(z_t)[y_t]                      (Sec. 3.1: p_t = softmax(z)_y)
+ *     k_t       = exp(l_train_t - l_infer_t)                 (Sec. 2.1, Eq. (1): k = p/q)
+ *     phi_t     = max(1 - p_t, kappa)                        (Sec. 3.3, Algorithm 1)
+ *     w_t       = min{k_t, 1 + lambda * phi_t}               (Eq. (4), Algorithm 1)
+ *     term_t    = scale * w_t * A_t * l_train_t
+ *     dL/dz_t   = scale * w_t * A_t * (onehot(y_t) - softmax(z_t))
+ *
+ *   w_t is a stop-gradient constant (Algorithm 1; App. C.1 "Operators"), evaluated from the
+ *   difference of the two log-probabilities (the right-hand form of Eq. (4)). lambda is the
+ *   paper's threshold: the displacement factor e^eps is truncated at 1 + lambda (Sec. 3.3), so
+ *   a bound c on the log-odds displacement itself corresponds to lambda = e^c - 1. kappa is
+ *   the numerical floor of Algorithm 1 (5e-3 in the paper). The loss is the REINFORCE form at
+ *   update ratio 1, whose gradient is the policy-gradient payload weighted by w_t.
+ *
+ *   A row is valid when m_t != 0 and 0 <= y_t < V. Invalid rows are not read: l_train, w,
+ *   trunc and term are 0 and their gradient row is 0. 1 - p_t is evaluated from the
+ *   complement mass sum_{j != y} e^{z_j - max} / sum_j e^{z_j - max}, which keeps its relative
+ *   accuracy as p_t -> 1. A token is "truncated" when k_t > 1 + lambda*phi_t (strict).
+ *   term_t is 0 when scale*w_t*A_t is 0.
+ *
+ * Conventions shared by every entry point:
+ *   - All array pointers are DEVICE pointers owned by the caller; the library never frees or
+ *     retains them and never allocates device memory.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null stream). The return
+ *     value reports argument and launch errors only; it never synchronises. On a nonzero
+ *     return nothing has been launched and no output has been written.
+ *   - Data errors (ids out of range on unmasked rows, non-finite rows) are not return codes:
+ *     they are counted in the cis_stats_t at the start of the workspace (below).
+ *   - Results are deterministic: repeated calls on the same inputs give identical bits.
+ */
+#ifndef CIS_H
+#define CIS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of the logits and of the gradient. */
+typedef enum { CIS_BF16 = 0, CIS_F32 = 1 } cis_dtype_t;
+
+/* Status codes. */
+enum {
+  CIS_OK = 0,
+  CIS_ERR_NULL = -1,      /* a required pointer is NULL                                       */
+  CIS_ERR_SHAPE = -2,     /* T < 0, V outside [1, 2^28], ld < V or ld_g < V                  */
+  CIS_ERR_DTYPE = -3,     /* dtype is not a cis_dtype_t                                       */
+  CIS_ERR_PARAM = -4,     /* lambda < 0 or not finite, kappa outside [0,1], scale not finite  */
+  CIS_ERR_ALIGN = -5,     /* logits/dlogits base or row stride in bytes not a multiple of 16; */
+                          /* workspace not 256-byte aligned                                   */
+  CIS_ERR_LAUNCH = -6,    /* the HIP runtime rejected a kernel launch                         */
+  CIS_ERR_WORKSPACE = -7, /* workspace smaller than cis_workspace_bytes(T)                    */
+  CIS_ERR_ALIAS = -8,     /* dlogits == logits with ld_g != ld, or a partial overlap          */
+  CIS_ERR_DEVICE = -9     /* the current device is not a gfx950 GPU, or no device            */
+};
+
+/* Per-call statistics, written at byte offset 0 of the workspace by cis_loss_fwd/_bwd once
+ * every row is done (read it after synchronising the stream). */
+typedef struct cis_stats {
+  double  loss;         /* sum_t term_t, accumulated in double in a fixed order             */
+  int64_t n_valid;      /* rows with mask != 0 and 0 <= id < V                              */
+  int64_t n_bad_id;     /* rows with mask != 0 and id outside [0, V)                        */
+  int64_t n_nonfinite;  /* valid rows whose log-sum-exp is not finite or whose w is NaN     */
+  int64_t n_trunc;      /* valid rows whose weight was truncated (k > 1 + lambda*phi)      */
+  int64_t reserved[3];
+} cis_stats_t;
+
+/* Bytes of device workspace cis_loss_fwd/_bwd need for T rows (T >= 0). The workspace holds
+ * the cis_stats_t, the per-row loss terms and per-row status flags; its previous contents
+ * do not matter. Returns 0 for T < 0. */
+size_t cis_workspace_bytes(int64_t T);
+
+/* Static, human-readable text for a status code. */
+const char* cis_status_string(int status);
+
+/*
+ * cis_weights — Algorithm 1 (Sec. 3.3) as one elementwise pass over recorded log-probabilities.
+ *
+ *   logp_train [T] float  training-side log-probability of each sampled token (<= 0)
+ *   logp_infer [T] float  inference-side log-probability recorded at sampling
+ *   mask       [T] uint8  nonzero = token counts; NULL = every token counts
+ *   lambda, kappa         threshold and floor (lambda >= 0 finite, 0 <= kappa <= 1)
+ *   w_out      [T] float  weight min{k, 1 + lambda*max(1-p, kappa)}; 0 on masked tokens
+ *   trunc_out  [T] uint8  1 where the cap was applied; NULL = not written
+ *
+ * Here p = exp(logp_train) and 1 - p is evaluated as -expm1(logp_train).
+ * Errors: CIS_ERR_NULL (T > 0 and a required pointer is NULL), CIS_ERR_SHAPE (T < 0),
+ * CIS_ERR_PARAM, CIS_ERR_LAUNCH, CIS_ERR_DEVICE.
+ */
+int cis_weights(const float* logp_train, const float* logp_infer, const uint8_t* mask,
+                int64_t T, float lambda, float kappa,
+                float* w_out, uint8_t* trunc_out, hipStream_t stream);
+
+/*
+ * cis_loss_fwd — the forward pass: training log-softmax at the sampled ids, CIS weights and
+ * loss, reading each valid logits row once.
+ *
+ *   logits     [T, ld] device, dtype elements, row-major; columns [V, ld) are never used.
+ *              Base address and ld*sizeof(dtype) must be multiples of 16 bytes.
+ *   dtype      CIS_BF16 or CIS_F32
+ *   T, V, ld   rows, vocabulary size (1 <= V <= 2^28), row stride in elements (ld >= V);
+ *              the buffer spans T*ld elements (the last row's padding included)
+ *   ids        [T] int64   sampled token id of each row
+ *   logp_infer [T] float   inference log-probability of the sampled id
+ *   adv        [T] float   advantage of each row (per-response factors already folded in)
+ *   mask       [T] uint8   nonzero = the row counts; NULL = every row counts
+ *   lambda, kappa, scale   threshold, floor, and the loss normalisation (e.g. -1/N_valid)
+ *   logp_train_out, w_out [T] float, trunc_out [T] uint8, loss_terms_out [T] float:
+ *              optional per-row outputs (NULL = not written)
+ *   loss_out   [1] float   optional; sum_t term_t rounded to float
+ *   workspace  device, 256-byte aligned, >= cis_workspace_bytes(T) bytes; receives cis_stats_t
+ * Errors: CIS_ERR_NULL, CIS_ERR_SHAPE, CIS_ERR_DTYPE, CIS_ERR_PARAM, CIS_ERR_ALIGN,
+ *         CIS_ERR_WORKSPACE, CIS_ERR_LAUNCH, CIS_ERR_DEVICE.
+ */
+int cis_loss_fwd(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
+                 const int64_t* ids, const float* logp_infer, const float* adv,
+                 const uint8_t* mask, float lambda, float kappa, float scale,
+                 float* logp_train_out, float* w_out, uint8_t* trunc_out,
+                 float* loss_terms_out, float* loss_out,
+                 void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * cis_loss_bwd — the fused forward and backward pass: everything cis_loss_fwd produces, plus
+ * the gradient of sum_t term_t with respect to the logits, written in the logits dtype with
+ * round-to-nearest-even.
+ *
+ *   dlogits    [T, ld_g] device, same dtype as logits; base and ld_g*sizeof(dtype) multiples
+ *              of 16 bytes. Columns [V, ld_g) are not written. Every row is written (zeros
+ *              for invalid rows). May be the logits buffer itself (in place) when ld_g == ld;
+ *              any other overlap is rejected with CIS_ERR_ALIAS.
+ *   other arguments as for cis_loss_fwd.
+ * Gradient values whose magnitude is below 2^-126 may be flushed to zero.
+ */
+int cis_loss_bwd(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
+                 const int64_t* ids, const float* logp_infer, const float* adv,
+                 const uint8_t* mask, float lambda, float kappa, float scale,
+                 void* dlogits, int64_t ld_g,
+                 float* logp_train_out, float* w_out, uint8_t* trunc_out,
+                 float* loss_terms_out, float* loss_out,
+                 void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CIS_H */

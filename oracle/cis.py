@@ -58,6 +58,7 @@ __all__ = [
     "bf16_bits_to_float64",
     "round_float64_to_bf16_bits",
     "bf16_neighbors",
+    "Bf16Matrix",
     "row_log_softmax",
     "cis_weight",
     "cis_weights",
@@ -121,6 +122,21 @@ def round_float64_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     nan = np.isnan(x)
     bits[nan] = np.where(np.signbit(x[nan]), 0xFFC0, 0x7FC0).astype(np.uint16)
     return bits
+
+
+class Bf16Matrix:
+    """Read-only [T, V] matrix of bfloat16 bit patterns whose rows read as float64.
+
+    Lets the oracle walk a large bfloat16 logits matrix one row at a time without holding a
+    float64 copy of all of it.
+    """
+
+    def __init__(self, bits: np.ndarray):
+        self.bits = np.asarray(bits, dtype=np.uint16)
+        self.shape = self.bits.shape
+
+    def __getitem__(self, t) -> np.ndarray:
+        return bf16_bits_to_float64(self.bits[t])
 
 
 def bf16_neighbors(x: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
@@ -263,11 +279,10 @@ def cis_loss(logits: np.ndarray, ids: np.ndarray, logp_infer: np.ndarray, adv: n
              with_grad: bool = True, rows: np.ndarray | None = None) -> CisResult:
     """CIS-weighted token loss over logits [T, V] (float64), and optionally dL/dlogits.
 
-    ``rows`` restricts the work to a subset of row indices (the other rows are left as zeros
-    and marked with flags 0); the returned arrays keep the full [T] / [T, V] shape only when
-    ``rows`` is None, otherwise they are indexed like ``rows``.
+    ``logits`` is any [T, V] matrix whose rows convert to float64 (a numpy array, or a
+    Bf16Matrix of bfloat16 bit patterns). ``rows`` restricts the work to a subset of row
+    indices; the returned arrays are indexed like ``rows`` (all rows when it is None).
     """
-    logits = np.asarray(logits)
     T, V = logits.shape
     sel = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
     n = sel.shape[0]

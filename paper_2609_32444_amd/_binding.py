@@ -1,0 +1,270 @@
+"""ctypes binding of libcis.so: argument checks and marshalling only."""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import struct
+from typing import Optional
+
+import torch
+
+CIS_BF16 = 0
+CIS_F32 = 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB: Optional[ctypes.CDLL] = None
+
+_vp = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_f32 = ctypes.c_float
+_int = ctypes.c_int
+_size = ctypes.c_size_t
+
+
+class CisError(RuntimeError):
+    """A libcis call returned a nonzero status."""
+
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn}: {status_string(status)} (status {status})")
+        self.status = status
+
+
+def library_path() -> str:
+    return os.path.join(_HERE, "libcis.so")
+
+
+def load_library() -> ctypes.CDLL:
+    """Loads libcis.so from the package directory (built by paper_2609_32444_amd.build)."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = library_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2609_32444_amd.build`")
+    lib = ctypes.CDLL(path)
+    lib.cis_workspace_bytes.argtypes = [_i64]
+    lib.cis_workspace_bytes.restype = _size
+    lib.cis_status_string.argtypes = [_int]
+    lib.cis_status_string.restype = ctypes.c_char_p
+    lib.cis_weights.argtypes = [_vp, _vp, _vp, _i64, _f32, _f32, _vp, _vp, _vp]
+    lib.cis_weights.restype = _int
+    lib.cis_loss_fwd.argtypes = [_vp, _int, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _f32, _f32, _f32,
+                                 _vp, _vp, _vp, _vp, _vp, _vp, _size, _vp]
+    lib.cis_loss_fwd.restype = _int
+    lib.cis_loss_bwd.argtypes = [_vp, _int, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _f32, _f32, _f32,
+                                 _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _size, _vp]
+    lib.cis_loss_bwd.restype = _int
+    _LIB = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().cis_status_string(int(status)).decode()
+
+
+def workspace_bytes(T: int) -> int:
+    return int(load_library().cis_workspace_bytes(int(T)))
+
+
+def lambda_from_logodds(c: float) -> float:
+    """Threshold lambda for a bound c on the log-odds displacement: e^eps <= 1 + lambda = e^c."""
+    return math.expm1(c)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(dev: torch.device) -> int:
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+def _check_vec(name: str, t: Optional[torch.Tensor], T: int, dtype, dev, optional=False):
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if t.device != dev:
+        raise ValueError(f"{name} must be on {dev}, got {t.device}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != 1 or t.shape[0] != T or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous [{T}] tensor, got {tuple(t.shape)}")
+    return t
+
+
+def _mask_u8(mask: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
+    if mask is None:
+        return None
+    if mask.dtype == torch.bool:
+        return mask.view(torch.uint8)
+    return mask
+
+
+def _logits_args(logits: torch.Tensor, V: Optional[int]):
+    if not logits.is_cuda:
+        raise ValueError("logits must be a device tensor")
+    if logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be [T, >=V] with unit column stride")
+    if logits.dtype == torch.bfloat16:
+        dtype = CIS_BF16
+    elif logits.dtype == torch.float32:
+        dtype = CIS_F32
+    else:
+        raise ValueError(f"logits dtype must be bfloat16 or float32, got {logits.dtype}")
+    T = logits.shape[0]
+    V = logits.shape[1] if V is None else int(V)
+    ld = logits.stride(0) if T > 1 else max(logits.shape[1], V)
+    return dtype, T, V, ld
+
+
+def _outputs(T: int, dev, want):
+    out = {}
+    if "logp_train" in want:
+        out["logp_train"] = torch.empty(T, dtype=torch.float32, device=dev)
+    if "w" in want:
+        out["w"] = torch.empty(T, dtype=torch.float32, device=dev)
+    if "trunc" in want:
+        out["trunc"] = torch.empty(T, dtype=torch.uint8, device=dev)
+    if "terms" in want:
+        out["terms"] = torch.empty(T, dtype=torch.float32, device=dev)
+    out["loss"] = torch.empty(1, dtype=torch.float32, device=dev)
+    return out
+
+
+_ALL = ("logp_train", "w", "trunc", "terms")
+
+
+def _loss(bwd: bool, logits, ids, logp_infer, adv, mask, lam, kappa, scale, V, dlogits, want,
+          workspace):
+    dtype, T, V, ld = _logits_args(logits, V)
+    dev = logits.device
+    _check_vec("ids", ids, T, torch.int64, dev)
+    _check_vec("logp_infer", logp_infer, T, torch.float32, dev)
+    _check_vec("adv", adv, T, torch.float32, dev)
+    mask = _check_vec("mask", _mask_u8(mask), T, torch.uint8, dev, optional=True)
+    out = _outputs(T, dev, want)
+    nws = workspace_bytes(T)
+    if workspace is None:
+        workspace = torch.empty(nws, dtype=torch.uint8, device=dev)
+    elif workspace.device != dev or workspace.numel() * workspace.element_size() < nws:
+        raise ValueError(f"workspace must hold {nws} bytes on {dev}")
+    lib = load_library()
+    with torch.cuda.device(dev):
+        common = (_ptr(logits), dtype, T, V, ld, _ptr(ids), _ptr(logp_infer), _ptr(adv),
+                  _ptr(mask), float(lam), float(kappa), float(scale))
+        tail = (_ptr(out.get("logp_train")), _ptr(out.get("w")), _ptr(out.get("trunc")),
+                _ptr(out.get("terms")), _ptr(out["loss"]), _ptr(workspace),
+                workspace.numel() * workspace.element_size(), _stream(dev))
+        if bwd:
+            if dlogits is None:
+                dlogits = torch.empty((T, V), dtype=logits.dtype, device=dev)
+            if dlogits.dtype != logits.dtype or dlogits.dim() != 2 or dlogits.stride(1) != 1 \
+                    or dlogits.shape[0] != T or dlogits.shape[1] < V or dlogits.device != dev:
+                raise ValueError("dlogits must be a [T, >=V] tensor like logits")
+            ldg = dlogits.stride(0) if T > 1 else max(dlogits.shape[1], V)
+            rc = lib.cis_loss_bwd(*common, _ptr(dlogits), ldg, *tail)
+            fn = "cis_loss_bwd"
+        else:
+            rc = lib.cis_loss_fwd(*common, *tail)
+            fn = "cis_loss_fwd"
+    if rc != 0:
+        raise CisError(fn, rc)
+    out["workspace"] = workspace
+    if bwd:
+        out["dlogits"] = dlogits
+    return out
+
+
+def loss_fwd(logits, ids, logp_infer, adv, mask=None, *, lam, kappa=5e-3, scale=1.0, V=None,
+             want=_ALL, workspace=None):
+    """Forward pass of the CIS token loss; returns a dict of device tensors.
+
+    Keys: the requested per-row outputs ("logp_train", "w", "trunc", "terms"), "loss" ([1]
+    float32, the sum of the terms) and "workspace" (holding the cis_stats_t; see read_stats).
+    """
+    return _loss(False, logits, ids, logp_infer, adv, mask, lam, kappa, scale, V, None, want,
+                 workspace)
+
+
+def loss_bwd(logits, ids, logp_infer, adv, mask=None, *, lam, kappa=5e-3, scale=1.0, V=None,
+             dlogits=None, want=_ALL, workspace=None):
+    """Fused forward and backward pass; like loss_fwd plus "dlogits" (d loss / d logits)."""
+    return _loss(True, logits, ids, logp_infer, adv, mask, lam, kappa, scale, V, dlogits, want,
+                 workspace)
+
+
+class LossCall:
+    """One loss call with every output, the gradient and the workspace allocated up front;
+    run() only launches (what a training step or a benchmark repeats)."""
+
+    def __init__(self, logits, ids, logp_infer, adv, mask=None, *, lam, kappa=5e-3, scale=1.0,
+                 bwd=True, V=None, want=_ALL):
+        dtype, T, V, ld = _logits_args(logits, V)
+        dev = logits.device
+        _check_vec("ids", ids, T, torch.int64, dev)
+        _check_vec("logp_infer", logp_infer, T, torch.float32, dev)
+        _check_vec("adv", adv, T, torch.float32, dev)
+        mask = _check_vec("mask", _mask_u8(mask), T, torch.uint8, dev, optional=True)
+        self.dev, self.bwd, self.T, self.V = dev, bwd, T, V
+        self.out = _outputs(T, dev, want)
+        self.workspace = torch.empty(workspace_bytes(T), dtype=torch.uint8, device=dev)
+        self._keep = (logits, ids, logp_infer, adv, mask)
+        common = (_ptr(logits), dtype, T, V, ld, _ptr(ids), _ptr(logp_infer), _ptr(adv),
+                  _ptr(mask), float(lam), float(kappa), float(scale))
+        tail = (_ptr(self.out.get("logp_train")), _ptr(self.out.get("w")),
+                _ptr(self.out.get("trunc")), _ptr(self.out.get("terms")), _ptr(self.out["loss"]),
+                _ptr(self.workspace), self.workspace.numel())
+        lib = load_library()
+        if bwd:
+            self.dlogits = torch.empty((T, V), dtype=logits.dtype, device=dev)
+            self._fn, self._name = lib.cis_loss_bwd, "cis_loss_bwd"
+            self._args = common + (_ptr(self.dlogits), self.dlogits.stride(0) if T > 1 else V) + tail
+            self.out["dlogits"] = self.dlogits
+        else:
+            self._fn, self._name = lib.cis_loss_fwd, "cis_loss_fwd"
+            self._args = common + tail
+        self.out["workspace"] = self.workspace
+
+    def run(self, stream: Optional[int] = None) -> dict:
+        with torch.cuda.device(self.dev):
+            s = _stream(self.dev) if stream is None else stream
+            rc = self._fn(*self._args, s)
+        if rc != 0:
+            raise CisError(self._name, rc)
+        return self.out
+
+
+def weights(logp_train, logp_infer, mask=None, *, lam, kappa=5e-3, w_out=None, trunc_out=None):
+    """Algorithm 1 on recorded log-probabilities: returns (w, trunc) device tensors."""
+    dev = logp_train.device
+    T = logp_train.shape[0]
+    _check_vec("logp_train", logp_train, T, torch.float32, dev)
+    _check_vec("logp_infer", logp_infer, T, torch.float32, dev)
+    mask = _check_vec("mask", _mask_u8(mask), T, torch.uint8, dev, optional=True)
+    if w_out is None:
+        w_out = torch.empty(T, dtype=torch.float32, device=dev)
+    if trunc_out is None:
+        trunc_out = torch.empty(T, dtype=torch.uint8, device=dev)
+    _check_vec("w_out", w_out, T, torch.float32, dev)
+    _check_vec("trunc_out", trunc_out, T, torch.uint8, dev)
+    with torch.cuda.device(dev):
+        rc = load_library().cis_weights(_ptr(logp_train), _ptr(logp_infer), _ptr(mask), T,
+                                        float(lam), float(kappa), _ptr(w_out), _ptr(trunc_out),
+                                        _stream(dev))
+    if rc != 0:
+        raise CisError("cis_weights", rc)
+    return w_out, trunc_out
+
+
+_STATS = struct.Struct("<d7q")
+
+
+def read_stats(workspace: torch.Tensor) -> dict:
+    """Copies the cis_stats_t at the start of a workspace to the host (synchronises)."""
+    raw = bytes(workspace[:_STATS.size].cpu().numpy().tobytes())
+    loss, n_valid, n_bad_id, n_nonfinite, n_trunc, _, _, _ = _STATS.unpack(raw)
+    return {"loss": loss, "n_valid": n_valid, "n_bad_id": n_bad_id, "n_nonfinite": n_nonfinite,
+            "n_trunc": n_trunc}

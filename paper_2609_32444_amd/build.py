@@ -1,0 +1,53 @@
+"""Builds libcis.so (the HIP kernels and the C ABI) in-tree for gfx950 with hipcc.
+
+    python -m paper_2609_32444_amd.build      # or: from paper_2609_32444_amd.build import build
+"""
+
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+LIB_PATH = os.path.join(HERE, "libcis.so")
+SOURCES = [os.path.join(HERE, "csrc", "cis_kernels.hip"), os.path.join(HERE, "csrc", "cis_api.cpp")]
+HEADERS = [os.path.join(ROOT, "include", "cis.h"), os.path.join(HERE, "csrc", "cis_internal.h")]
+
+# -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in device code (the compiler's host pass warns
+# that it does not know the feature; that warning is expected).
+HIPCC_FLAGS = [
+    "-x", "hip", "--offload-arch=gfx950", "-O3", "-std=c++20", "-fPIC", "-shared",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-I", os.path.join(ROOT, "include"),
+]
+
+
+def hipcc() -> str:
+    for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
+        if cand and os.path.exists(cand):
+            return cand
+    raise RuntimeError("hipcc not found (set HIPCC or install ROCm)")
+
+
+def build(verbose: bool = False) -> str:
+    """Compiles libcis.so; always recompiles. Returns the library path."""
+    tmp = LIB_PATH + ".tmp"
+    cmd = [hipcc(), *HIPCC_FLAGS, *SOURCES, "-o", tmp]
+    proc = subprocess.run(cmd, capture_output=True, text=True)
+    if proc.returncode != 0:
+        sys.stderr.write(proc.stdout + proc.stderr)
+        raise RuntimeError(f"hipcc failed with status {proc.returncode}")
+    if verbose:
+        noise = "'-packed-fp32-ops' is not a recognized feature"
+        out = "\n".join(l for l in (proc.stdout + proc.stderr).splitlines() if noise not in l)
+        if out.strip():
+            print(out)
+    os.replace(tmp, LIB_PATH)
+    return LIB_PATH
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

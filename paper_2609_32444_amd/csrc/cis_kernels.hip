@@ -1,0 +1,595 @@
+// HIP kernels (gfx950) of the CIS token loss: the fused row kernel (training log-softmax,
+// CIS weight, loss term and gradient), the deterministic loss/statistics reduction, and the
+// elementwise weight kernel of Algorithm 1.
+//
+// Row kernel design (one persistent workgroup per row at a time):
+//   * Each thread owns the 16-byte vectors v = tid, tid + BLOCK, ... of the row. The first
+//     NV of them stay in VGPRs from the load to the gradient store, so a row that fits in
+//     NV*BLOCK vectors is read from HBM exactly once; vectors beyond that are re-read.
+//   * Sweep 1: per-lane max, then per-lane sum of exp(z - max) excluding the sampled id
+//     (its element is set to -inf in registers), combined across the wave with shuffles and
+//     across waves through LDS in a fixed order (deterministic).
+//   * Epilogue: l_train, 1 - p (complement mass), the CIS weight of Algorithm 1 and the
+//     loss term, all computed redundantly by every thread from the same LDS values.
+//   * Sweep 2 (backward): g_j = -coef * exp(z_j - lse), evaluated as one FMA and one v_exp_f32
+//     with |coef| folded into the exponent, rounded to bf16 with the hardware RNE convert; the
+//     sampled element gets coef * (1 - p).
+#include <hip/hip_runtime.h>
+#include <float.h>
+#include <math.h>
+#include <stdint.h>
+
+#include <utility>
+
+#include "cis_internal.h"
+
+namespace cis {
+
+// Calls f(std::integral_constant<int, 0>) ... f(std::integral_constant<int, N-1>). Every access
+// to the register-resident row goes through a compile-time index, so the row array is
+// promoted to VGPRs (a runtime index anywhere would move it to scratch memory).
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.44269504088896340736f;
+constexpr double kLog2eD = 1.44269504088896340736;
+// Lowest reference point for a lane's running max. Keeping every max >= -2^127 keeps
+// max*log2(e) finite, so exp(z - max) can be evaluated with a single FMA even for lanes that
+// only hold -inf (padding) entries. A row whose largest logit is outside [-2^127, 2^127] is
+// reported as non-finite.
+constexpr float kMinRef = -0x1p127f;
+constexpr float kMaxRef = 0x1p127f;
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ------------------------------------------------------------------------------------------
+// Element formats: a 16-byte vector holds 8 bf16 or 4 fp32 logits.
+// ------------------------------------------------------------------------------------------
+struct Bf16 {
+  static constexpr int kPerVec = 8;
+  static constexpr int kBytes = 2;
+  static constexpr uint32_t kNegInf2 = 0xFF80FF80u;
+
+  __device__ static __forceinline__ void unpack(const u32x4 v, float (&f)[8]) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      f[2 * k] = __uint_as_float(v[k] << 16);
+      f[2 * k + 1] = __uint_as_float(v[k] & 0xFFFF0000u);
+    }
+  }
+  template <bool NEG>
+  __device__ static __forceinline__ u32x4 pack(const float (&f)[8]) {
+    u32x4 out;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      bf16x2 p = {(__bf16)(NEG ? -f[2 * k] : f[2 * k]),
+                  (__bf16)(NEG ? -f[2 * k + 1] : f[2 * k + 1])};
+      out[k] = __builtin_bit_cast(uint32_t, p);
+    }
+    return out;
+  }
+  __device__ static __forceinline__ u32x4 neg_inf_vec() {
+    return u32x4{kNegInf2, kNegInf2, kNegInf2, kNegInf2};
+  }
+  __device__ static __forceinline__ uint32_t bits_of(float x) {
+    bf16x2 p = {(__bf16)x, (__bf16)0.0f};
+    return __builtin_bit_cast(uint32_t, p) & 0xFFFFu;
+  }
+  // value of element e (runtime index)
+  __device__ static __forceinline__ float get(const u32x4 v, int e) {
+    const uint32_t d = v[e >> 1];
+    return __uint_as_float((e & 1) ? (d & 0xFFFF0000u) : (d << 16));
+  }
+  // replace element e with the 16-bit pattern `bits`
+  __device__ static __forceinline__ u32x4 set(u32x4 v, int e, uint32_t bits) {
+    const int k = e >> 1;
+    const uint32_t d = v[k];
+    const uint32_t nd = (e & 1) ? ((d & 0x0000FFFFu) | (bits << 16)) : ((d & 0xFFFF0000u) | bits);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (j == k) v[j] = nd;
+    return v;
+  }
+  // elements with index >= n become -inf
+  __device__ static __forceinline__ u32x4 mask_tail(u32x4 v, int n) {
+#pragma unroll 1
+    for (int e = n; e < 8; ++e) v = set(v, e, 0xFF80u);
+    return v;
+  }
+  __device__ static __forceinline__ void store_elem(void* row, int idx, uint32_t bits) {
+    reinterpret_cast<uint16_t*>(row)[idx] = (uint16_t)bits;
+  }
+  __device__ static __forceinline__ uint32_t elem_bits(const u32x4 v, int e) {
+    const uint32_t d = v[e >> 1];
+    return (e & 1) ? (d >> 16) : (d & 0xFFFFu);
+  }
+};
+
+struct F32 {
+  static constexpr int kPerVec = 4;
+  static constexpr int kBytes = 4;
+
+  __device__ static __forceinline__ void unpack(const u32x4 v, float (&f)[4]) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) f[k] = __uint_as_float(v[k]);
+  }
+  template <bool NEG>
+  __device__ static __forceinline__ u32x4 pack(const float (&f)[4]) {
+    u32x4 out;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) out[k] = __float_as_uint(NEG ? -f[k] : f[k]);
+    return out;
+  }
+  __device__ static __forceinline__ u32x4 neg_inf_vec() {
+    return u32x4{0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u};
+  }
+  __device__ static __forceinline__ uint32_t bits_of(float x) { return __float_as_uint(x); }
+  __device__ static __forceinline__ float get(const u32x4 v, int e) { return __uint_as_float(v[e]); }
+  __device__ static __forceinline__ u32x4 set(u32x4 v, int e, uint32_t bits) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (j == e) v[j] = bits;
+    return v;
+  }
+  __device__ static __forceinline__ u32x4 mask_tail(u32x4 v, int n) {
+#pragma unroll 1
+    for (int e = n; e < 4; ++e) v = set(v, e, 0xFF800000u);
+    return v;
+  }
+  __device__ static __forceinline__ void store_elem(void* row, int idx, uint32_t bits) {
+    reinterpret_cast<uint32_t*>(row)[idx] = bits;
+  }
+  __device__ static __forceinline__ uint32_t elem_bits(const u32x4 v, int e) { return v[e]; }
+};
+
+__device__ __forceinline__ u32x4 ld16(const u32x4* p) { return __builtin_nontemporal_load(p); }
+
+// Buffer addressing for the row sweeps: the row base lives in a scalar resource descriptor, the
+// per-thread offset tid*16 in one VGPR, and the per-slot offset i*BLOCK*16 in an SGPR, so the
+// register-resident slots need no per-slot address registers. Accesses whose VGPR offset is at
+// or beyond num_records are dropped (stores) or return zero (loads).
+constexpr int kRsrcWord3 = 0x00020000;  // gfx9 raw buffer: 32-bit data format
+constexpr int kAuxNT = 2;                // non-temporal: streamed once
+constexpr uint32_t kOutOfRange = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, kRsrcWord3);
+}
+__device__ __forceinline__ u32x4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kAuxNT);
+}
+__device__ __forceinline__ void bstore(u32x4 v, __amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                       uint32_t soff) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, kAuxNT);
+}
+
+// (m, s) pairs represent s * exp(m): combine two of them.
+__device__ __forceinline__ void lse_combine(float& m, float& s, float m2, float s2) {
+  const float mn = fmaxf(m, m2);
+  s = s * fast_exp2((m - mn) * kLog2e) + s2 * fast_exp2((m2 - mn) * kLog2e);
+  m = mn;
+}
+
+__device__ __forceinline__ void wave_lse_reduce(float& m, float& s) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float m2 = __shfl_xor(m, off, 64);
+    const float s2 = __shfl_xor(s, off, 64);
+    lse_combine(m, s, m2, s2);
+  }
+}
+
+// Optimisation barrier: the register-resident row is "redefined" here, so the compiler cannot
+// keep unpacked fp32 copies of it alive from one sweep to the next (it re-unpacks instead,
+// which costs one VALU op per element but keeps the row at 16 bytes per vector in VGPRs).
+template <int I, int NV>
+__device__ __forceinline__ void opaque_one(u32x4 (&r)[NV]) {
+  asm volatile("" : "+v"(r[I]));
+}
+template <int NV>
+__device__ __forceinline__ void opaque(u32x4 (&r)[NV]) {
+  static_for<NV>([&](auto I) { opaque_one<I>(r); });
+}
+
+// Row geometry shared by the sweeps. Vector v = i*BLOCK + tid of the row is "slot i" of thread
+// tid; slot L = (nvec-1)/BLOCK holds the last vector. When L <= NV, slots 0..L-1 (all complete)
+// live in r[0..L-1] and slot L (possibly partial, possibly ending in padding) in one extra
+// register vector rp; otherwise r holds slots 0..NV-1 and slots NV..L are streamed twice.
+struct RowGeom {
+  int nvec, tail;
+  int L;             // slot of the last vector
+  int nres;          // complete slots held in r[]
+  bool has_rp;       // slot L is held in rp
+  bool ragged;       // the last vector ends in padding (V % elements-per-vector != 0)
+  bool last_mine;    // this thread holds the last vector
+  bool rp_mine;      // this thread holds a vector of slot L
+};
+
+// Writes elements [0, n) of gradient vector v one by one (the partial last vector).
+template <class E>
+__device__ __forceinline__ void store_partial(void* grow, int v, u32x4 val, int n) {
+  for (int e = 0; e < n; ++e) E::store_elem(grow, v * E::kPerVec + e, E::elem_bits(val, e));
+}
+
+// Writes a zero gradient row. The write descriptor covers complete vectors only.
+template <class E, int BLOCK>
+__device__ __forceinline__ void zero_row(__amdgpu_buffer_rsrc_t ws, void* grow, const RowGeom& g,
+                                         int tid) {
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  for (int v = tid; v < g.nvec; v += BLOCK) bstore(z, ws, (uint32_t)v * 16u, 0u);
+  if (g.ragged && g.last_mine) store_partial<E>(grow, g.nvec - 1, z, g.tail);
+}
+
+// Gradient of one 16-byte vector of logits: sign * exp2(z*log2e - b2), rounded.
+template <class E, bool NEG>
+__device__ __forceinline__ u32x4 grad_vec(u32x4 zv, float b2) {
+  float f[E::kPerVec];
+  E::unpack(zv, f);
+#pragma unroll
+  for (int e = 0; e < E::kPerVec; ++e) f[e] = fast_exp2(__builtin_fmaf(f[e], kLog2e, -b2));
+  return E::template pack<NEG>(f);
+}
+
+// Sweep 2 of one row. Every vector is stored through the write descriptor (which drops the
+// partial last vector and out-of-range lanes); the partial last vector is then written element
+// by element, and finally the sampled element is overwritten with coef*(1-p) by the thread that
+// stored its vector (same-thread program order).
+template <class E, int BLOCK, int NV, bool NEG>
+__device__ __forceinline__ void grad_sweep(const u32x4 (&r)[NV], u32x4 rp,
+                                           __amdgpu_buffer_rsrc_t rs, __amdgpu_buffer_rsrc_t ws,
+                                           void* grow, const RowGeom& g, uint32_t voff, float b2,
+                                           int y, bool y_mine, uint32_t gy_bits) {
+  static_for<NV>([&](auto I) {
+    constexpr int i = I;
+    if (i < g.nres)
+      bstore(grad_vec<E, NEG>(r[i], b2), ws, voff + (uint32_t)(i * BLOCK * 16), 0u);
+  });
+  if (g.has_rp) {
+    bstore(grad_vec<E, NEG>(rp, b2), ws,
+           g.rp_mine ? voff + (uint32_t)(g.L * BLOCK * 16) : kOutOfRange, 0u);
+  } else {
+    for (uint32_t o = voff + (uint32_t)(NV * BLOCK * 16); o < (uint32_t)g.nvec * 16u;
+         o += (uint32_t)(BLOCK * 16))
+      bstore(grad_vec<E, NEG>(bload(rs, o, 0u), b2), ws, o, 0u);
+  }
+  if (g.ragged && g.last_mine)
+    store_partial<E>(grow, g.nvec - 1,
+                     grad_vec<E, NEG>(bload(rs, (uint32_t)(g.nvec - 1) * 16u, 0u), b2), g.tail);
+  if (y_mine) E::store_elem(grow, y, gy_bits);
+}
+
+// Exp-sum of one vector relative to mb = max*log2e, optionally leaving out element `skip`.
+template <class E>
+__device__ __forceinline__ void accum_vec(const float (&f)[E::kPerVec], float mb, float (&acc)[4]) {
+#pragma unroll
+  for (int e = 0; e < E::kPerVec; ++e) acc[e & 3] += fast_exp2(__builtin_fmaf(f[e], kLog2e, -mb));
+}
+template <class E>
+__device__ __forceinline__ void accum_vec_skip(const float (&f)[E::kPerVec], float mb,
+                                               float (&acc)[4], bool mine, int skip,
+                                               float& z_skip) {
+  // Not speculatable: keeps the caller's uniform branch a branch instead of per-slot selects.
+  asm volatile("");
+#pragma unroll
+  for (int e = 0; e < E::kPerVec; ++e) {
+    const bool hit = mine && e == skip;
+    z_skip = hit ? f[e] : z_skip;
+    acc[e & 3] += hit ? 0.f : fast_exp2(__builtin_fmaf(f[e], kLog2e, -mb));
+  }
+}
+
+template <class E, int BLOCK, int NV, bool BWD>
+__global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
+  constexpr int EPV = E::kPerVec;
+  constexpr int NW = BLOCK / 64;
+  __shared__ float sh_m[2][NW];
+  __shared__ float sh_s[2][NW];
+  __shared__ float sh_zy[2];
+
+  const int V = a.V;
+  int buf = 0;
+
+  for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) {
+    // The row geometry is loop-invariant, but letting the compiler hoist everything derived
+    // from it (one mask or address per slot) out of the row loop exhausts the register file;
+    // re-deriving it from opaque copies each row costs a few scalar instructions.
+    int tid = threadIdx.x;
+    int nvec_r = a.nvec;
+    asm volatile("" : "+v"(tid));
+    asm volatile("" : "+s"(nvec_r));
+    const int wid = __builtin_amdgcn_readfirstlane(tid) >> 6;
+    RowGeom g;
+    g.nvec = nvec_r;
+    g.tail = V - (g.nvec - 1) * EPV;  // valid elements in the last vector, 1..EPV
+    g.L = (g.nvec - 1) / BLOCK;
+    g.has_rp = g.L <= NV;
+    g.nres = g.has_rp ? g.L : NV;
+    g.ragged = g.tail != EPV;
+    g.last_mine = ((g.nvec - 1) % BLOCK) == tid;
+    g.rp_mine = g.L * BLOCK + tid < g.nvec;
+    uint32_t voff = (uint32_t)tid * 16u;
+
+    const int64_t y64 = a.ids[row];
+    const bool on = a.mask ? (a.mask[row] != 0) : true;
+    const bool in_range = (y64 >= 0) && (y64 < (int64_t)V);
+    void* grow = BWD ? (void*)((char*)a.dlogits + row * a.grow_bytes) : nullptr;
+    // write descriptor: complete vectors only
+    const __amdgpu_buffer_rsrc_t ws =
+        make_rsrc(grow, BWD ? (uint32_t)(g.nvec - (g.ragged ? 1 : 0)) * 16u : 0u);
+
+    if (!(on && in_range)) {
+      if (BWD) zero_row<E, BLOCK>(ws, grow, g, tid);
+      if (tid == 0) {
+        if (a.logp_train_out) a.logp_train_out[row] = 0.f;
+        if (a.w_out) a.w_out[row] = 0.f;
+        if (a.trunc_out) a.trunc_out[row] = 0;
+        if (a.terms_user) a.terms_user[row] = 0.f;
+        a.terms_ws[row] = 0.f;
+        a.flags_ws[row] = on ? kFlagBadId : 0;
+      }
+      continue;
+    }
+
+    const int y = (int)y64;
+    const int vy = y / EPV, ey = y % EPV;
+    const int slot_y = vy / BLOCK;
+    const bool y_mine = (vy % BLOCK) == tid;
+    const void* rowp = (const char*)a.logits + row * a.row_bytes;
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(rowp, (uint32_t)g.nvec * 16u);
+
+    // ---- load the resident part of the row ----------------------------------------------
+    u32x4 r[NV];
+    static_for<NV>([&](auto I) {
+      constexpr int i = I;
+      if (i < g.nres) r[i] = bload(rs, voff + (uint32_t)(i * BLOCK * 16), 0u);
+    });
+    u32x4 rp = E::neg_inf_vec();
+    if (g.has_rp) rp = bload(rs, g.rp_mine ? voff + (uint32_t)(g.L * BLOCK * 16) : kOutOfRange, 0u);
+    // Entries of rp that are not logits of this row become -inf: lanes past the last vector
+    // and the padding after V in a ragged last vector (after every load is in flight).
+    if (g.has_rp) {
+      rp = g.rp_mine ? rp : E::neg_inf_vec();
+      if (g.ragged && g.last_mine) rp = E::mask_tail(rp, g.tail);
+    }
+
+    // ---- sweep 1: max, then the exp-sum excluding the sampled id --------------------------
+    float m = kMinRef;
+    static_for<NV>([&](auto I) {
+      constexpr int i = I;
+      if (i < g.nres) {
+        float f[EPV];
+        E::unpack(r[i], f);
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
+      }
+    });
+    if (g.has_rp) {
+      float f[EPV];
+      E::unpack(rp, f);
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
+    } else {
+      // streamed slots NV..L: running max only (their exp-sum is taken below)
+      for (uint32_t o = voff + (uint32_t)(NV * BLOCK * 16); o < (uint32_t)g.nvec * 16u;
+           o += (uint32_t)(BLOCK * 16)) {
+        float f[EPV];
+        E::unpack(bload(rs, o, 0u), f);
+        const int j0 = (int)(o >> 4) * EPV;
+#pragma unroll
+        for (int e = 0; e < EPV; ++e)
+          if (j0 + e < V) m = fmaxf(m, f[e]);
+      }
+    }
+    opaque(r);
+    float s = 0.f;
+    float zy_mine = 0.f;
+    {
+      const float mb = m * kLog2e;
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+      static_for<NV>([&](auto I) {
+        constexpr int i = I;
+        if (i < g.nres) {
+          float f[EPV];
+          E::unpack(r[i], f);
+          if (i == slot_y)
+            accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
+          else
+            accum_vec<E>(f, mb, acc);
+        }
+      });
+      if (g.has_rp) {
+        float f[EPV];
+        E::unpack(rp, f);
+        if (slot_y == g.L)
+          accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
+        else
+          accum_vec<E>(f, mb, acc);
+      } else {
+        for (uint32_t o = voff + (uint32_t)(NV * BLOCK * 16); o < (uint32_t)g.nvec * 16u;
+             o += (uint32_t)(BLOCK * 16)) {
+          float f[EPV];
+          E::unpack(bload(rs, o, 0u), f);
+          const int j0 = (int)(o >> 4) * EPV;
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) {
+            const int j = j0 + e;
+            if (j == y) zy_mine = f[e];
+            if (j < V && j != y) acc[e & 3] += fast_exp2(__builtin_fmaf(f[e], kLog2e, -mb));
+          }
+        }
+      }
+      s = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    }
+    opaque(r);
+    asm volatile("" : "+v"(voff));
+
+    // ---- block reduction (fixed order) -------------------------------------------------
+    wave_lse_reduce(m, s);
+    if ((tid & 63) == 0) {
+      sh_m[buf][wid] = m;
+      sh_s[buf][wid] = s;
+    }
+    if (y_mine) sh_zy[buf] = zy_mine;
+    __syncthreads();
+    float M = sh_m[buf][0], sr = sh_s[buf][0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) lse_combine(M, sr, sh_m[buf][w], sh_s[buf][w]);
+    const float zy = sh_zy[buf];
+    buf ^= 1;
+
+    // ---- epilogue: l_train, 1 - p, CIS weight (Algorithm 1), loss term ------------------
+    // M: max over the row (sampled element included); sr: sum_{j != y} exp(z_j - M).
+    const float s_rest = sr;
+    const float e_y = expf(zy - M);
+    const float ssum = e_y + s_rest;
+    const float lse = M + logf(ssum);
+    const float ltr = (e_y >= s_rest) ? -log1pf(s_rest / e_y) : (zy - M) - logf(ssum);
+    const float one_m_p = s_rest / ssum;
+    const float delta = ltr - a.logp_infer[row];
+    const float lam_phi = a.lam * fmaxf(one_m_p, a.kappa);
+    const bool trunc = delta > log1pf(lam_phi);
+    const float w = trunc ? 1.0f + lam_phi : expf(delta);
+    const float coef = a.scale * w * a.adv[row];
+    const float term = (coef == 0.f) ? 0.f : coef * ltr;
+    const bool nonfinite = !(isfinite(lse) && M > kMinRef && M < kMaxRef) || isnan(w);
+
+    if (tid == 0) {
+      if (a.logp_train_out) a.logp_train_out[row] = ltr;
+      if (a.w_out) a.w_out[row] = w;
+      if (a.trunc_out) a.trunc_out[row] = trunc ? 1 : 0;
+      if (a.terms_user) a.terms_user[row] = term;
+      a.terms_ws[row] = term;
+      a.flags_ws[row] = kFlagValid | (trunc ? kFlagTrunc : 0) | (nonfinite ? kFlagNonFinite : 0);
+    }
+
+    // ---- sweep 2: gradient ----------------------------------------------------------------
+    if (BWD) {
+      if (coef == 0.f) {
+        zero_row<E, BLOCK>(ws, grow, g, tid);
+      } else {
+        // g_j = -coef * exp(z_j - lse) = -sign(coef) * exp2(z_j*log2e - b2) with
+        // b2 = (lse - ln|coef|) * log2e, formed in double and rounded once.
+        const double lse_d = (double)M + log((double)ssum);
+        const float b2 = (float)((lse_d - log(fabs((double)coef))) * kLog2eD);
+        const uint32_t gy_bits = E::bits_of(coef * one_m_p);
+        if (coef > 0.f)
+          grad_sweep<E, BLOCK, NV, true>(r, rp, rs, ws, grow, g, voff, b2, y, y_mine, gy_bits);
+        else
+          grad_sweep<E, BLOCK, NV, false>(r, rp, rs, ws, grow, g, voff, b2, y, y_mine, gy_bits);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Loss and statistics: one workgroup, fixed summation order (independent of the row grid).
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kFinalizeBlock) void cis_finalize_kernel(const FinalizeArgs a) {
+  constexpr int NW = kFinalizeBlock / 64;
+  __shared__ double sh_loss[NW];
+  __shared__ long long sh_cnt[4][NW];
+  const int tid = threadIdx.x;
+  double acc = 0.0;
+  long long nv = 0, nb = 0, nf = 0, nt = 0;
+  for (int64_t t = tid; t < a.T; t += kFinalizeBlock) {
+    acc += (double)a.terms_ws[t];
+    const uint8_t f = a.flags_ws[t];
+    nv += (f & kFlagValid) ? 1 : 0;
+    nb += (f & kFlagBadId) ? 1 : 0;
+    nf += (f & kFlagNonFinite) ? 1 : 0;
+    nt += (f & kFlagTrunc) ? 1 : 0;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    acc += __shfl_down(acc, off, 64);
+    nv += __shfl_down(nv, off, 64);
+    nb += __shfl_down(nb, off, 64);
+    nf += __shfl_down(nf, off, 64);
+    nt += __shfl_down(nt, off, 64);
+  }
+  const int wid = tid >> 6;
+  if ((tid & 63) == 0) {
+    sh_loss[wid] = acc;
+    sh_cnt[0][wid] = nv;
+    sh_cnt[1][wid] = nb;
+    sh_cnt[2][wid] = nf;
+    sh_cnt[3][wid] = nt;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double L = 0.0;
+    long long c[4] = {0, 0, 0, 0};
+    for (int w = 0; w < NW; ++w) {
+      L += sh_loss[w];
+      for (int k = 0; k < 4; ++k) c[k] += sh_cnt[k][w];
+    }
+    a.stats->loss = L;
+    a.stats->n_valid = c[0];
+    a.stats->n_bad_id = c[1];
+    a.stats->n_nonfinite = c[2];
+    a.stats->n_trunc = c[3];
+    a.stats->reserved[0] = 0;
+    a.stats->reserved[1] = 0;
+    a.stats->reserved[2] = 0;
+    if (a.loss_out) *a.loss_out = (float)L;
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Algorithm 1 as an elementwise pass over recorded log-probabilities.
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kWeightsBlock) void cis_weights_kernel(const WeightsArgs a) {
+  for (int64_t t = (int64_t)blockIdx.x * kWeightsBlock + threadIdx.x; t < a.T;
+       t += (int64_t)gridDim.x * kWeightsBlock) {
+    float w = 0.f;
+    bool trunc = false;
+    if (!a.mask || a.mask[t]) {
+      const float lt = a.logp_train[t];
+      const float delta = lt - a.logp_infer[t];
+      const float lam_phi = a.lam * fmaxf(-expm1f(lt), a.kappa);
+      trunc = delta > log1pf(lam_phi);
+      w = trunc ? 1.0f + lam_phi : expf(delta);
+    }
+    a.w_out[t] = w;
+    if (a.trunc_out) a.trunc_out[t] = trunc ? 1 : 0;
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Variant tables
+// ------------------------------------------------------------------------------------------
+#define CIS_V(E, B, N, BWD) RowVariant{B, N, (const void*)&cis_row_kernel<E, B, N, BWD>}
+#define CIS_TABLE(E, BWD)                                                                   \
+  {CIS_V(E, 256, 1, BWD),   CIS_V(E, 256, 3, BWD),                                          \
+   CIS_V(E, 256, 7, BWD),   CIS_V(E, 256, 11, BWD),  CIS_V(E, 256, 15, BWD),                \
+   CIS_V(E, 1024, 7, BWD),  CIS_V(E, 1024, 11, BWD), CIS_V(E, 1024, 15, BWD),               \
+   CIS_V(E, 1024, 18, BWD)}
+
+static const RowVariant kBf16Bwd[] = CIS_TABLE(Bf16, true);
+static const RowVariant kBf16Fwd[] = CIS_TABLE(Bf16, false);
+static const RowVariant kF32Bwd[] = CIS_TABLE(F32, true);
+static const RowVariant kF32Fwd[] = CIS_TABLE(F32, false);
+#undef CIS_TABLE
+#undef CIS_V
+
+const RowVariant& select_row_variant(int dtype, bool bwd, int32_t nvec) {
+  const RowVariant* t = dtype == CIS_BF16 ? (bwd ? kBf16Bwd : kBf16Fwd) : (bwd ? kF32Bwd : kF32Fwd);
+  constexpr int n = sizeof(kBf16Bwd) / sizeof(kBf16Bwd[0]);
+  for (int i = 0; i < n; ++i)
+    if ((int64_t)t[i].block * (t[i].nv + 1) >= nvec) return t[i];
+  return t[n - 1];  // rows longer than 19*1024 vectors: the remainder is streamed twice
+}
+
+const void* finalize_kernel() { return (const void*)&cis_finalize_kernel; }
+const void* weights_kernel() { return (const void*)&cis_weights_kernel; }
+
+}  // namespace cis

@@ -1,0 +1,236 @@
+"""Parity helpers: run the CPU oracle on the same inputs as the HIP path and compare.
+
+Tolerances (the readings used by every parity test):
+
+* valid / bad-id flags and the zero rows of invalid tokens: bit-exact.
+* truncation flags: bit-exact, except tokens whose oracle margin |Delta - log1p(lambda*phi)|
+  is below 1e-5, where either flag is a correct result (the weight is continuous there).
+* l_train: |gpu - ref| <= 1e-5 |ref| + 2e-6 (float32 log-sum-exp resolution).
+* w: relative 1e-5.
+* term: |gpu - ref| <= 1e-5 |ref| + 2e-6 |scale w A|; loss: <= 1e-5 sum_t |term_t| + 1e-6.
+* bf16 gradient: every element is one of the two bfloat16 values bracketing the float64
+  gradient (a faithful rounding; the float64 value rounded to nearest is reported as the
+  bit-equal fraction), except elements with |g| < 2^-126 that may be flushed to zero; per row,
+  ||g - g64|| / ||g64|| <= 2e-3.
+* float32 gradient: |g - g64| <= 2e-5 |g64| + 2^-126.
+"""
+
+from __future__ import annotations
+
+import math
+import multiprocessing as mp
+import os
+
+import numpy as np
+import torch
+
+from oracle import cis as O
+
+F32_TINY = 2.0 ** -126
+
+
+def host_logits(logits: torch.Tensor):
+    """Host copy of device logits whose rows read exactly as float64: a Bf16Matrix of the
+    bfloat16 bit patterns, or a float64 array for float32 logits."""
+    if logits.dtype == torch.bfloat16:
+        bits = logits.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        return O.Bf16Matrix(bits)
+    return logits.cpu().double().numpy()
+
+
+def f32(x: float) -> float:
+    return float(np.float32(x))
+
+
+# ------------------------------------------------------------------------------------------
+# gradient comparison of one block of rows (runs inside the pool workers)
+# ------------------------------------------------------------------------------------------
+def grad_stats(g: np.ndarray, g64: np.ndarray, bf16: bool) -> dict:
+    """Counts for the gradient criteria on a block of rows (both float64 arrays [n, V])."""
+    st = {"n_el": int(g.size), "n_rows": int(g.shape[0])}
+    nrm = np.linalg.norm(g64, axis=1)
+    rel = np.linalg.norm(g - g64, axis=1) / np.where(nrm > 0, nrm, 1.0)
+    st["max_row_rel_l2"] = float(rel.max()) if rel.size else 0.0
+    st["zero_row_violations"] = int(np.sum(np.any(g[nrm == 0] != 0, axis=1)))
+    if bf16:
+        lo, hi = O.bf16_neighbors(g64)
+        ok = (g >= lo) & (g <= hi)
+        ok |= (np.abs(g64) < F32_TINY) & (np.abs(g) <= F32_TINY)
+        st["not_faithful"] = int((~ok).sum())
+        rn = O.bf16_bits_to_float64(O.round_float64_to_bf16_bits(g64))
+        st["bit_equal"] = int(np.sum(g == rn))
+        st["within_2e-3_rel"] = int(np.sum(np.abs(g - g64) <= 2e-3 * np.abs(g64)))
+    else:
+        err = np.abs(g - g64)
+        st["not_faithful"] = int(np.sum(err > 2e-5 * np.abs(g64) + F32_TINY))
+        st["max_rel"] = float(np.max(err / np.maximum(np.abs(g64), F32_TINY))) if g.size else 0.0
+        st["bit_equal"] = int(np.sum(g == g64.astype(np.float32)))
+        st["within_2e-3_rel"] = int(np.sum(err <= 2e-3 * np.abs(g64)))
+    return st
+
+
+def merge_grad_stats(parts) -> dict:
+    out = {}
+    for st in parts:
+        for k, v in st.items():
+            if k.startswith("max"):
+                out[k] = max(out.get(k, 0.0), v)
+            else:
+                out[k] = out.get(k, 0) + v
+    return out
+
+
+# ------------------------------------------------------------------------------------------
+# oracle over many rows (process pool; each worker runs the plain oracle on a block of rows)
+# ------------------------------------------------------------------------------------------
+_SHARED = {}
+
+
+def _worker(args):
+    rows, with_grad = args
+    d = _SHARED
+    res = O.cis_loss(d["z"], d["ids"], d["linf"], d["adv"], d["mask"], d["lam"], d["kappa"],
+                     d["scale"], with_grad=with_grad, rows=rows)
+    gst = None
+    if with_grad and d.get("gdev") is not None:
+        fin = (res.flags & O.FLAG_NONFINITE) == 0
+        gdev = d["gdev"]
+        g = O.bf16_bits_to_float64(gdev[rows]) if gdev.dtype == np.uint16 else \
+            gdev[rows].astype(np.float64)
+        gst = grad_stats(g[fin], res.grad[fin], gdev.dtype == np.uint16)
+        res.grad = None
+    return rows, res, gst
+
+
+def _nproc() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(n, 16))
+
+
+def run_oracle(z, ids, linf, adv, mask, lam, kappa, scale, rows=None, with_grad=True,
+               gdev=None, procs=None) -> dict:
+    """Oracle results for `rows` (all rows if None) as a dict of arrays indexed like rows.
+
+    With `gdev` (the device gradient on the host: uint16 bf16 bits or float32, [T, V]) the
+    workers compare gradients themselves and only the merged counts come back ("grad_stats");
+    otherwise the float64 gradient rows are returned under "grad".
+    """
+    T = z.shape[0]
+    rows = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
+    _SHARED.clear()
+    _SHARED.update(z=z, ids=ids, linf=linf, adv=adv, mask=mask, lam=lam, kappa=kappa,
+                   scale=scale, gdev=gdev)
+    procs = _nproc() if procs is None else procs
+    blocks = [b for b in np.array_split(rows, max(1, min(len(rows), procs * 4))) if len(b)]
+    if procs > 1 and len(blocks) > 1:
+        ctx = mp.get_context("fork")
+        with ctx.Pool(procs) as pool:
+            parts = pool.map(_worker, [(b, with_grad) for b in blocks])
+    else:
+        parts = [_worker((b, with_grad)) for b in blocks]
+    _SHARED.clear()
+    out = {k: [] for k in ("logp_train", "w", "trunc", "term", "flags", "grad")}
+    gsts = []
+    for b, r, gst in parts:
+        out["logp_train"].append(r.logp_train)
+        out["w"].append(r.w)
+        out["trunc"].append(r.trunc)
+        out["term"].append(r.term)
+        out["flags"].append(r.flags)
+        if r.grad is not None:
+            out["grad"].append(r.grad)
+        if gst is not None:
+            gsts.append(gst)
+    res = {k: np.concatenate(v) for k, v in out.items() if v}
+    res["rows"] = rows
+    if gsts:
+        res["grad_stats"] = merge_grad_stats(gsts)
+    return res
+
+
+def device_grad_host(g: torch.Tensor, V: int) -> np.ndarray:
+    g = g[:, :V]
+    if g.dtype == torch.bfloat16:
+        return g.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    return g.contiguous().cpu().numpy()
+
+
+def oracle_for_batch(b, rows=None, with_grad=True, grad=None) -> dict:
+    """Oracle on batch `b`; pass the device gradient as `grad` to compare it in the workers."""
+    z = host_logits(b.logits)
+    mask = None if b.mask is None else b.mask.cpu().numpy()
+    gdev = None if grad is None else device_grad_host(grad, b.V)
+    return run_oracle(z, b.ids.cpu().numpy(), b.logp_infer.cpu().double().numpy(),
+                      b.adv.cpu().double().numpy(), mask, f32(b.lam), f32(b.kappa), f32(b.scale),
+                      rows=rows, with_grad=with_grad or grad is not None, gdev=gdev)
+
+
+# ------------------------------------------------------------------------------------------
+# comparison
+# ------------------------------------------------------------------------------------------
+def trunc_margin(ref: dict, linf: np.ndarray, lam: float, kappa: float) -> np.ndarray:
+    """|Delta - log1p(lambda*phi)| of the oracle for each compared row (inf on invalid rows)."""
+    rows = ref["rows"]
+    lt = ref["logp_train"]
+    one_m_p = -np.expm1(lt)
+    phi = np.maximum(one_m_p, kappa)
+    m = np.abs((lt - linf[rows]) - np.log1p(lam * phi))
+    return np.where(ref["flags"] & O.FLAG_VALID, m, np.inf)
+
+
+def compare_scalars(out: dict, ref: dict, b, report: dict) -> None:
+    rows = ref["rows"]
+    lam, kappa, scale = f32(b.lam), f32(b.kappa), f32(b.scale)
+    linf = b.logp_infer.cpu().double().numpy()
+    adv = b.adv.cpu().double().numpy()
+    valid = (ref["flags"] & O.FLAG_VALID) > 0
+    fin = valid & ((ref["flags"] & O.FLAG_NONFINITE) == 0)
+
+    lt = out["logp_train"].cpu().double().numpy()[rows]
+    w = out["w"].cpu().double().numpy()[rows]
+    tr = out["trunc"].cpu().numpy()[rows].astype(bool)
+    term = out["terms"].cpu().double().numpy()[rows]
+
+    # invalid rows: exact zeros
+    assert np.all(lt[~valid] == 0) and np.all(w[~valid] == 0) and np.all(term[~valid] == 0)
+    assert not tr[~valid].any()
+
+    err_lt = np.where(lt == ref["logp_train"], 0.0, np.abs(lt - ref["logp_train"]))[fin]
+    assert np.all(err_lt <= 1e-5 * np.abs(ref["logp_train"][fin]) + 2e-6), \
+        f"logp_train: max err {err_lt.max():.3g}"
+    rel_w = (np.abs(w - ref["w"]) / np.maximum(np.abs(ref["w"]), 1e-300))[fin]
+    assert np.all(rel_w <= 1e-5), f"w: max rel err {rel_w.max():.3g}"
+    coefmag = np.abs(scale * ref["w"] * adv[rows])
+    err_t = np.abs(term - ref["term"])[fin]
+    assert np.all(err_t <= 1e-5 * np.abs(ref["term"][fin]) + 2e-6 * coefmag[fin]), \
+        f"term: max err {err_t.max():.3g}"
+
+    margin = trunc_margin(ref, linf, lam, kappa)
+    differ = (tr != ref["trunc"]) & fin
+    assert np.all(margin[differ] < 1e-5), \
+        f"{int((differ & (margin >= 1e-5)).sum())} truncation flags differ outside the margin"
+    report.update(rows=int(len(rows)), valid=int(valid.sum()), trunc=int(ref["trunc"].sum()),
+                  trunc_in_margin_differ=int(differ.sum()),
+                  max_rel_w=float(rel_w.max()) if rel_w.size else 0.0,
+                  max_err_logp=float(err_lt.max()) if err_lt.size else 0.0)
+
+
+def compare_loss(out: dict, ref_all: dict, report: dict) -> None:
+    """Scalar loss against the oracle's fsum over all rows (ref_all must cover every row)."""
+    L = float(out["loss"].item())
+    terms = ref_all["term"]
+    L64 = math.fsum(terms.tolist())
+    bound = 1e-5 * float(np.sum(np.abs(terms))) + 1e-6
+    assert abs(L - L64) <= bound, f"loss {L} vs {L64} (bound {bound:.3g})"
+    report.update(loss=L, loss_ref=L64)
+
+
+def check_grad_stats(st: dict, report: dict) -> None:
+    assert st["not_faithful"] == 0, f"{st['not_faithful']} gradient elements out of tolerance"
+    assert st["zero_row_violations"] == 0
+    assert st["max_row_rel_l2"] <= 2e-3, f"row rel L2 {st['max_row_rel_l2']:.3g}"
+    report["grad"] = dict(st, bit_equal_frac=st["bit_equal"] / max(st["n_el"], 1),
+                          within_2e_3_frac=st["within_2e-3_rel"] / max(st["n_el"], 1))

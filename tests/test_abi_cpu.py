@@ -1,0 +1,116 @@
+"""The C-ABI library on the host: it loads, exports every entry point include/cis.h declares,
+and rejects bad arguments before touching a device. No kernel is launched here."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_32444_amd as cis
+from paper_2609_32444_amd import _binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cis.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(cis_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = cis.load_library()
+    names = declared_functions()
+    assert set(names) == {"cis_workspace_bytes", "cis_status_string", "cis_weights",
+                          "cis_loss_fwd", "cis_loss_bwd"}
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_workspace_bytes_layout():
+    assert cis.workspace_bytes(-1) == 0
+    assert cis.workspace_bytes(0) == 256
+    for T in (1, 255, 256, 16384, 65536, 524288):
+        n = cis.workspace_bytes(T)
+        assert n % 256 == 0 and n >= 256 + 5 * T
+
+
+def test_status_strings():
+    for code in range(0, -10, -1):
+        s = cis.status_string(code)
+        assert s and s != "unknown status"
+    assert cis.status_string(-99) == "unknown status"
+
+
+NULL = None
+FAKE = 0x10000   # a 16-byte aligned non-null address; never dereferenced on these paths
+
+
+def _fwd(**kw):
+    a = dict(logits=FAKE, dtype=0, T=4, V=8, ld=8, ids=FAKE, linf=FAKE, adv=FAKE, mask=NULL,
+             lam=1.0, kappa=5e-3, scale=-0.25, lt=NULL, w=NULL, tr=NULL, terms=NULL, loss=NULL,
+             ws=FAKE, wsb=1 << 20, stream=NULL)
+    a.update(kw)
+    return cis.load_library().cis_loss_fwd(
+        a["logits"], a["dtype"], a["T"], a["V"], a["ld"], a["ids"], a["linf"], a["adv"],
+        a["mask"], a["lam"], a["kappa"], a["scale"], a["lt"], a["w"], a["tr"], a["terms"],
+        a["loss"], a["ws"], a["wsb"], a["stream"])
+
+
+def _bwd(**kw):
+    a = dict(logits=FAKE, dtype=0, T=4, V=8, ld=8, ids=FAKE, linf=FAKE, adv=FAKE, mask=NULL,
+             lam=1.0, kappa=5e-3, scale=-0.25, dl=FAKE * 16, ldg=8, ws=FAKE, wsb=1 << 20)
+    a.update(kw)
+    return cis.load_library().cis_loss_bwd(
+        a["logits"], a["dtype"], a["T"], a["V"], a["ld"], a["ids"], a["linf"], a["adv"],
+        a["mask"], a["lam"], a["kappa"], a["scale"], a["dl"], a["ldg"], NULL, NULL, NULL, NULL,
+        NULL, a["ws"], a["wsb"], NULL)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=7), -3),
+    (dict(T=-1), -2), (dict(V=0), -2), (dict(ld=7), -2),
+    (dict(V=(1 << 28) + 1, ld=(1 << 28) + 8), -2),
+    (dict(lam=-1.0), -4), (dict(lam=float("inf")), -4), (dict(lam=float("nan")), -4),
+    (dict(kappa=-0.1), -4), (dict(kappa=1.5), -4), (dict(scale=float("nan")), -4),
+    (dict(ws=NULL), -1), (dict(logits=NULL), -1), (dict(ids=NULL), -1), (dict(adv=NULL), -1),
+    (dict(linf=NULL), -1),
+    (dict(ws=FAKE + 16), -5), (dict(logits=FAKE + 2), -5), (dict(V=7, ld=7), -5),
+    (dict(wsb=100), -7),
+])
+def test_fwd_argument_errors(kw, code):
+    assert _fwd(**kw) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dl=NULL), -1), (dict(ldg=4), -2), (dict(dl=FAKE * 16 + 8), -5),
+    (dict(ldg=12), -5),                              # 24-byte row stride
+    (dict(dl=FAKE, ldg=16), -8),                     # same base, different stride
+    (dict(dl=FAKE + 32), -8),                        # partial overlap
+])
+def test_bwd_argument_errors(kw, code):
+    assert _bwd(**kw) == code
+
+
+def test_weights_argument_errors():
+    lib = cis.load_library()
+    assert lib.cis_weights(FAKE, FAKE, NULL, -1, 1.0, 0.0, FAKE, NULL, NULL) == -2
+    assert lib.cis_weights(FAKE, FAKE, NULL, 4, -1.0, 0.0, FAKE, NULL, NULL) == -4
+    assert lib.cis_weights(FAKE, FAKE, NULL, 4, 1.0, 2.0, FAKE, NULL, NULL) == -4
+    assert lib.cis_weights(NULL, FAKE, NULL, 4, 1.0, 0.0, FAKE, NULL, NULL) == -1
+    assert lib.cis_weights(FAKE, FAKE, NULL, 4, 1.0, 0.0, NULL, NULL, NULL) == -1
+    assert lib.cis_weights(NULL, NULL, NULL, 0, 1.0, 0.0, NULL, NULL, NULL) == 0
+
+
+def test_binding_raises_cis_error_type():
+    e = _binding.CisError("cis_loss_fwd", -4)
+    assert e.status == -4 and "lambda" in str(e)
+
+
+def test_lambda_from_logodds():
+    import math
+    assert cis.lambda_from_logodds(0.0) == 0.0
+    assert abs(cis.lambda_from_logodds(1.0) - (math.e - 1)) < 1e-15
+    assert abs(cis.lambda_from_logodds(math.log(3.3)) - 2.3) < 1e-12

@@ -1,0 +1,191 @@
+"""Edge cases of the HIP path against the CPU oracle: ragged and tiny vocabularies, every
+row-kernel variant (register-resident and streamed rows), row strides, empty and fully masked
+batches, invalid ids, extreme probabilities, kappa = 0, lambda = 0, in-place gradients, float32
+logits, the elementwise weight kernel, and argument errors raised through the binding."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_32444_amd as cis
+from oracle import cis as O
+from tests import parity as P
+from workloads import make_random_batch
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def run_and_check(b, bwd=True, report=None, **kw):
+    fn = cis.loss_bwd if bwd else cis.loss_fwd
+    out = fn(b.logits, b.ids, b.logp_infer, b.adv, b.mask, lam=b.lam, kappa=b.kappa,
+             scale=b.scale, V=b.V, **kw)
+    torch.cuda.synchronize()
+    report = {} if report is None else report
+    ref = P.oracle_for_batch(b, with_grad=False, grad=out["dlogits"] if bwd else None)
+    P.compare_scalars(out, ref, b, report)
+    P.compare_loss(out, ref, report)
+    if bwd:
+        P.check_grad_stats(ref["grad_stats"], report)
+    st = cis.read_stats(out["workspace"])
+    assert st["n_valid"] == int(((ref["flags"] & O.FLAG_VALID) > 0).sum())
+    assert st["n_bad_id"] == int(((ref["flags"] & O.FLAG_BAD_ID) > 0).sum())
+    return out, ref, report
+
+
+# V values chosen to hit every row-kernel variant of both element types, ragged last vectors
+# (V % 8 != 0), single partial vectors, and rows longer than the register-resident capacity.
+BF16_VS = [1, 2, 7, 8, 9, 1000, 1001, 2048, 2049, 8192, 16384, 30000, 32768, 65536, 100000,
+           151936, 160000, 200000]
+F32_VS = [1, 3, 4, 5, 1024, 4097, 20000, 70000]
+
+
+@pytest.mark.parametrize("V", BF16_VS)
+def test_bf16_vocab_sizes(V):
+    ld = ((V + 7) // 8) * 8 + (8 if V % 3 == 0 else 0)
+    T = 24 if V <= 70000 else 8
+    b = make_random_batch(T, V, torch.bfloat16, DEV, seed=V, ld=ld, mask_p=0.85)
+    run_and_check(b)
+
+
+@pytest.mark.parametrize("V", F32_VS)
+def test_f32_vocab_sizes(V):
+    ld = ((V + 3) // 4) * 4
+    b = make_random_batch(16, V, torch.float32, DEV, seed=V + 1, ld=ld, mask_p=0.85)
+    run_and_check(b)
+
+
+@pytest.mark.parametrize("V", [1000, 151936, 262144])
+def test_forward_only_matches(V):
+    b = make_random_batch(12, V, torch.bfloat16, DEV, seed=5, mask_p=0.8)
+    run_and_check(b, bwd=False)
+
+
+def test_empty_batch():
+    b = make_random_batch(1, 16, torch.bfloat16, DEV, seed=1)
+    z = b.logits[:0]
+    e64 = torch.empty(0, dtype=torch.int64, device=DEV)
+    e32 = torch.empty(0, dtype=torch.float32, device=DEV)
+    out = cis.loss_bwd(z, e64, e32, e32, None, lam=1.0, kappa=5e-3, scale=1.0, V=16)
+    torch.cuda.synchronize()
+    assert out["loss"].item() == 0.0 and out["dlogits"].shape == (0, 16)
+    assert cis.read_stats(out["workspace"])["n_valid"] == 0
+
+
+def test_all_masked_and_invalid_ids():
+    b = make_random_batch(32, 3000, torch.bfloat16, DEV, seed=2)
+    b.mask.zero_()
+    out, ref, _ = run_and_check(b)
+    assert torch.count_nonzero(out["dlogits"]) == 0 and out["loss"].item() == 0.0
+    b = make_random_batch(32, 3000, torch.bfloat16, DEV, seed=3)
+    b.ids[::3] = -1
+    b.ids[1::5] = 3000
+    b.ids[2::7] = 1 << 40
+    out, ref, _ = run_and_check(b)
+    st = cis.read_stats(out["workspace"])
+    assert st["n_bad_id"] > 0
+    bad = ((b.ids < 0) | (b.ids >= 3000)) & (b.mask > 0)
+    assert torch.count_nonzero(out["dlogits"][bad]) == 0
+
+
+def test_confident_rows_and_extremes():
+    """p -> 1 (1 - p down to ~1e-30), l_infer = -inf, z_y = -inf, -inf and huge-negative logits."""
+    T, V = 16, 5000
+    b = make_random_batch(T, V, torch.bfloat16, DEV, seed=4, mask_p=1.0)
+    z = b.logits
+    y = b.ids
+    for t, gap in enumerate([5, 10, 15, 20, 30, 40, 60, 80]):
+        z[t, y[t]] = float(z[t].float().max()) + gap
+    b.logp_infer[8] = -math.inf
+    z[9, y[9]] = -math.inf
+    z[10, ::2] = -math.inf
+    z[10, y[10]] = 1.0
+    z[11, :] = -3.0e38
+    z[11, y[11]] = 0.5
+    z[12, 7] = -math.inf
+    b.logp_infer[13] = 0.0
+    out, ref, rep = run_and_check(b)
+    assert out["w"][9].item() == 0.0 and out["trunc"][8].item() == 1
+    for t in range(8):
+        lt = out["logp_train"][t].item()
+        assert lt <= 0
+
+
+@pytest.mark.parametrize("kappa,c", [(0.0, 1.0), (0.0, 0.25), (5e-3, 0.0), (1.0, 1.0),
+                                     (0.1, 3.0), (5e-3, 30.0)])
+def test_threshold_and_floor_settings(kappa, c):
+    b = make_random_batch(64, 4096, torch.bfloat16, DEV, seed=int(100 * kappa + 10 * c),
+                          delta_sd=1.5, c=c, kappa=kappa)
+    # make a third of the rows confident so that the floor matters
+    rows = torch.arange(0, 64, 3, device=DEV)
+    b.logits[rows, b.ids[rows]] = b.logits[rows].float().max(dim=1).values.to(torch.bfloat16) + 9
+    out, ref, rep = run_and_check(b)
+    if c == 0.0:
+        w = out["w"].cpu().numpy()
+        k = np.exp(out["logp_train"].cpu().double().numpy() - b.logp_infer.cpu().double().numpy())
+        assert np.allclose(w, np.minimum(k, 1.0), rtol=1e-5)
+
+
+def test_in_place_gradient():
+    b = make_random_batch(40, 9001, torch.bfloat16, DEV, seed=9, ld=9008)
+    ref_out = cis.loss_bwd(b.logits, b.ids, b.logp_infer, b.adv, b.mask, lam=b.lam,
+                           kappa=b.kappa, scale=b.scale, V=b.V)
+    torch.cuda.synchronize()
+    g_sep = ref_out["dlogits"].clone()
+    store = torch.empty(40, 9008, dtype=torch.bfloat16, device=DEV)
+    store[:, :b.V] = b.logits
+    buf = store[:, :b.V]            # same row stride as the logits (ld = 9008)
+    out = cis.loss_bwd(buf, b.ids, b.logp_infer, b.adv, b.mask, lam=b.lam, kappa=b.kappa,
+                       scale=b.scale, V=b.V, dlogits=buf)
+    torch.cuda.synchronize()
+    assert torch.equal(buf.view(torch.int16), g_sep.view(torch.int16))
+    assert torch.equal(out["w"], ref_out["w"])
+
+
+def test_padding_columns_untouched():
+    V, ld = 1001, 1016
+    b = make_random_batch(8, V, torch.bfloat16, DEV, seed=11, ld=ld)
+    g = torch.full((8, ld), 7.0, dtype=torch.bfloat16, device=DEV)
+    cis.loss_bwd(b.logits, b.ids, b.logp_infer, b.adv, b.mask, lam=b.lam, kappa=b.kappa,
+                 scale=b.scale, V=V, dlogits=g)
+    torch.cuda.synchronize()
+    assert torch.all(g[:, V:] == 7.0)
+
+
+def test_weights_kernel_matches_oracle():
+    rng = np.random.default_rng(0)
+    n = 100003
+    lt = -np.abs(rng.normal(0, 2, n)) * rng.choice([1e-9, 1e-4, 1e-2, 1, 3], n)
+    li = lt - rng.normal(0, 1.0, n)
+    li[::1000] = -np.inf
+    mask = (rng.random(n) > 0.1).astype(np.uint8)
+    lt32, li32 = lt.astype(np.float32), li.astype(np.float32)
+    for lam, kappa in [(2.3, 5e-3), (math.e - 1, 0.0), (0.0, 5e-3), (6.0, 1.0)]:
+        w, tr = cis.weights(torch.from_numpy(lt32).to(DEV), torch.from_numpy(li32).to(DEV),
+                            torch.from_numpy(mask).to(DEV), lam=lam, kappa=kappa)
+        w64, tr64 = O.cis_weights(lt32.astype(np.float64), li32.astype(np.float64), mask,
+                                  float(np.float32(lam)), float(np.float32(kappa)))
+        w = w.cpu().double().numpy()
+        tr = tr.cpu().numpy().astype(bool)
+        assert np.all(np.abs(w - w64) <= 1e-5 * np.abs(w64) + 1e-38)
+        phi = np.maximum(-np.expm1(lt32.astype(np.float64)), np.float32(kappa))
+        margin = np.abs((lt32.astype(np.float64) - li32) - np.log1p(np.float32(lam) * phi))
+        assert np.all((tr == tr64) | (margin < 1e-5))
+
+
+def test_binding_errors():
+    b = make_random_batch(4, 64, torch.bfloat16, DEV, seed=1)
+    with pytest.raises(cis.CisError) as e:
+        cis.loss_fwd(b.logits, b.ids, b.logp_infer, b.adv, b.mask, lam=-1.0)
+    assert e.value.status == -4
+    with pytest.raises(cis.CisError) as e:
+        cis.loss_bwd(b.logits, b.ids, b.logp_infer, b.adv, b.mask, lam=1.0, kappa=2.0)
+    assert e.value.status == -4
+    odd = torch.zeros(4, 63, dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(cis.CisError) as e:
+        cis.loss_fwd(odd, b.ids, b.logp_infer, b.adv, None, lam=1.0)
+    assert e.value.status == -5
+    with pytest.raises(ValueError):
+        cis.loss_fwd(b.logits, b.ids.int(), b.logp_infer, b.adv, b.mask, lam=1.0)

@@ -1,0 +1,2 @@
+"""Seeded synthetic inputs for the CIS loss (no CIS arithmetic; see workloads.synth)."""
+from .synth import CONFIGS, KAPPA, Batch, group_advantages, lambda_of, make_batch, make_random_batch  # noqa: F401
