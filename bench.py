@@ -102,14 +102,16 @@ def cpu_baseline(b, V: int, target_s: float = 15.0):
     # probe one row to size the sample
     rows_all = np.nonzero(b.mask.cpu().numpy())[0]
     rng = np.random.default_rng(0)
-    probe = rows_all[:2]
+    probe = rows_all[:9]
     import torch
     zp = O.Bf16Matrix(b.logits[torch.as_tensor(probe, device=b.logits.device)].contiguous()
                       .view(torch.int16).cpu().numpy().view(np.uint16))
+    args = (b.ids[probe].cpu().numpy(), b.logp_infer[probe].cpu().double().numpy(),
+            b.adv[probe].cpu().double().numpy(), None, b.lam, b.kappa, b.scale)
+    O.cis_loss(zp, *args, rows=np.arange(1))           # warm-up row
     t0 = time.perf_counter()
-    O.cis_loss(zp, b.ids[probe].cpu().numpy(), b.logp_infer[probe].cpu().double().numpy(),
-               b.adv[probe].cpu().double().numpy(), None, b.lam, b.kappa, b.scale)
-    per_row = (time.perf_counter() - t0) / len(probe)
+    O.cis_loss(zp, *args, rows=np.arange(1, len(probe)))
+    per_row = (time.perf_counter() - t0) / (len(probe) - 1)
     n = int(min(len(rows_all), max(cores * 4, target_s / max(per_row, 1e-6))))
     n = max(cores, (n // cores) * cores)
     rows = np.sort(rng.choice(rows_all, size=n, replace=False))
@@ -162,6 +164,8 @@ def main():
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-ceiling", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a device copy of MIB mebibytes (counter calibration) and exit")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -176,6 +180,15 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        n = args.copy_probe << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n}), flush=True)
+        return
     b = make_batch(args.config, device="cuda", c=args.c)
     torch.cuda.synchronize()
     bwd = args.mode == "bwd"

@@ -116,7 +116,7 @@ def _logits_args(logits: torch.Tensor, V: Optional[int]):
         raise ValueError(f"logits dtype must be bfloat16 or float32, got {logits.dtype}")
     T = logits.shape[0]
     V = logits.shape[1] if V is None else int(V)
-    ld = logits.stride(0) if T > 1 else max(logits.shape[1], V)
+    ld = logits.stride(0) if T > 1 else max(logits.stride(0), V)
     return dtype, T, V, ld
 
 
@@ -135,6 +135,13 @@ def _outputs(T: int, dev, want):
 
 
 _ALL = ("logp_train", "w", "trunc", "terms")
+
+
+def _new_grad(T: int, V: int, like: torch.Tensor) -> torch.Tensor:
+    """A [T, V] gradient view whose row stride is padded to a multiple of 16 bytes."""
+    epv = 16 // like.element_size()
+    ld = (V + epv - 1) // epv * epv
+    return torch.empty((T, ld), dtype=like.dtype, device=like.device)[:, :V]
 
 
 def _loss(bwd: bool, logits, ids, logp_infer, adv, mask, lam, kappa, scale, V, dlogits, want,
@@ -160,11 +167,11 @@ def _loss(bwd: bool, logits, ids, logp_infer, adv, mask, lam, kappa, scale, V, d
                 workspace.numel() * workspace.element_size(), _stream(dev))
         if bwd:
             if dlogits is None:
-                dlogits = torch.empty((T, V), dtype=logits.dtype, device=dev)
+                dlogits = _new_grad(T, V, logits)
             if dlogits.dtype != logits.dtype or dlogits.dim() != 2 or dlogits.stride(1) != 1 \
                     or dlogits.shape[0] != T or dlogits.shape[1] < V or dlogits.device != dev:
                 raise ValueError("dlogits must be a [T, >=V] tensor like logits")
-            ldg = dlogits.stride(0) if T > 1 else max(dlogits.shape[1], V)
+            ldg = dlogits.stride(0)
             rc = lib.cis_loss_bwd(*common, _ptr(dlogits), ldg, *tail)
             fn = "cis_loss_bwd"
         else:
@@ -219,9 +226,9 @@ class LossCall:
                 _ptr(self.workspace), self.workspace.numel())
         lib = load_library()
         if bwd:
-            self.dlogits = torch.empty((T, V), dtype=logits.dtype, device=dev)
+            self.dlogits = _new_grad(T, V, logits)
             self._fn, self._name = lib.cis_loss_bwd, "cis_loss_bwd"
-            self._args = common + (_ptr(self.dlogits), self.dlogits.stride(0) if T > 1 else V) + tail
+            self._args = common + (_ptr(self.dlogits), self.dlogits.stride(0)) + tail
             self.out["dlogits"] = self.dlogits
         else:
             self._fn, self._name = lib.cis_loss_fwd, "cis_loss_fwd"

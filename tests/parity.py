@@ -9,9 +9,11 @@ Tolerances (the readings used by every parity test):
 * w: relative 1e-5.
 * term: |gpu - ref| <= 1e-5 |ref| + 2e-6 |scale w A|; loss: <= 1e-5 sum_t |term_t| + 1e-6.
 * bf16 gradient: every element is one of the two bfloat16 values bracketing the float64
-  gradient (a faithful rounding; the float64 value rounded to nearest is reported as the
-  bit-equal fraction), except elements with |g| < 2^-126 that may be flushed to zero; per row,
-  ||g - g64|| / ||g64|| <= 2e-3.
+  gradient (a faithful rounding; agreement with the float64 value rounded to nearest is
+  reported as the bit-equal fraction), except elements with |g| < 2^-126 that may be flushed
+  to zero; per row, ||g - g_ref|| / ||g_ref|| <= 2e-3 with g_ref the float64 gradient rounded
+  to nearest bfloat16 (bfloat16's own unit roundoff, 2^-8, exceeds 2e-3, so the bound is
+  taken against the best bfloat16 answer), leaving out entries below 2^-126.
 * float32 gradient: |g - g64| <= 2e-5 |g64| + 2^-126.
 """
 
@@ -49,8 +51,8 @@ def grad_stats(g: np.ndarray, g64: np.ndarray, bf16: bool) -> dict:
     """Counts for the gradient criteria on a block of rows (both float64 arrays [n, V])."""
     st = {"n_el": int(g.size), "n_rows": int(g.shape[0])}
     nrm = np.linalg.norm(g64, axis=1)
-    rel = np.linalg.norm(g - g64, axis=1) / np.where(nrm > 0, nrm, 1.0)
-    st["max_row_rel_l2"] = float(rel.max()) if rel.size else 0.0
+    rel64 = np.linalg.norm(g - g64, axis=1) / np.where(nrm > 0, nrm, 1.0)
+    st["max_row_rel_l2_vs_f64"] = float(rel64.max()) if rel64.size else 0.0
     st["zero_row_violations"] = int(np.sum(np.any(g[nrm == 0] != 0, axis=1)))
     if bf16:
         lo, hi = O.bf16_neighbors(g64)
@@ -60,12 +62,20 @@ def grad_stats(g: np.ndarray, g64: np.ndarray, bf16: bool) -> dict:
         rn = O.bf16_bits_to_float64(O.round_float64_to_bf16_bits(g64))
         st["bit_equal"] = int(np.sum(g == rn))
         st["within_2e-3_rel"] = int(np.sum(np.abs(g - g64) <= 2e-3 * np.abs(g64)))
+        # per row, against the correctly rounded bfloat16 reference; entries below the float32
+        # normal range (which may be flushed) are left out of both sides
+        keep = np.abs(g64) >= F32_TINY
+        rnk = np.where(keep, rn, 0.0)
+        nrn = np.linalg.norm(rnk, axis=1)
+        rel = np.linalg.norm(np.where(keep, g, 0.0) - rnk, axis=1) / np.where(nrn > 0, nrn, 1.0)
     else:
+        rel = rel64
         err = np.abs(g - g64)
         st["not_faithful"] = int(np.sum(err > 2e-5 * np.abs(g64) + F32_TINY))
         st["max_rel"] = float(np.max(err / np.maximum(np.abs(g64), F32_TINY))) if g.size else 0.0
         st["bit_equal"] = int(np.sum(g == g64.astype(np.float32)))
         st["within_2e-3_rel"] = int(np.sum(err <= 2e-3 * np.abs(g64)))
+    st["max_row_rel_l2"] = float(rel.max()) if rel.size else 0.0
     return st
 
 
@@ -198,7 +208,8 @@ def compare_scalars(out: dict, ref: dict, b, report: dict) -> None:
     assert np.all(lt[~valid] == 0) and np.all(w[~valid] == 0) and np.all(term[~valid] == 0)
     assert not tr[~valid].any()
 
-    err_lt = np.where(lt == ref["logp_train"], 0.0, np.abs(lt - ref["logp_train"]))[fin]
+    with np.errstate(invalid="ignore"):
+        err_lt = np.where(lt == ref["logp_train"], 0.0, np.abs(lt - ref["logp_train"]))[fin]
     assert np.all(err_lt <= 1e-5 * np.abs(ref["logp_train"][fin]) + 2e-6), \
         f"logp_train: max err {err_lt.max():.3g}"
     rel_w = (np.abs(w - ref["w"]) / np.maximum(np.abs(ref["w"]), 1e-300))[fin]

@@ -78,3 +78,17 @@ def test_neighbors_bracket_and_are_adjacent():
     mid = 0.5 * (lo + hi)
     r = O.bf16_bits_to_float64(O.round_float64_to_bf16_bits(mid))
     assert np.all((r == lo) | (r == hi))
+
+
+def test_bf16_matrix_rows_match_torch_conversion():
+    rng = np.random.default_rng(2)
+    x = torch.from_numpy(rng.normal(0, 5, (7, 301)).astype(np.float32)).to(torch.bfloat16)
+    x[0, :5] = torch.tensor([float("inf"), -float("inf"), 0.0, -0.0, 3.0e38])
+    bits = x.view(torch.int16).numpy().view(np.uint16)
+    m = O.Bf16Matrix(bits)
+    assert m.shape == (7, 301)
+    ref = x.to(torch.float64).numpy()
+    for t in range(7):
+        row = m[t]
+        assert row.dtype == np.float64
+        assert np.array_equal(row, ref[t]) and np.array_equal(np.signbit(row), np.signbit(ref[t]))
