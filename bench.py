@@ -52,7 +52,7 @@ def algorithmic_bytes(T_valid: int, T_invalid: int, V: int, esize: int, bwd: boo
 def hbm_traffic(mode: str, workload: str):
     """HBM bytes per launch from committed rocprofv3 counter passes, if they were taken on the
     current kernel source (else None)."""
-    path = os.path.join(ROOT, "profiles", "traffic.json")
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_cis_row_kernel.json")
     if not os.path.exists(path):
         return None
     try:
@@ -65,24 +65,37 @@ def hbm_traffic(mode: str, workload: str):
         return None
 
 
-def copy_ceiling_gbs(nbytes: int, torch) -> float:
-    """Device-to-device copy of nbytes (read + write) as a measured bandwidth ceiling."""
-    n = nbytes // 2
-    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+def bandwidth_ceilings(rows: int, row_bytes: int, torch) -> dict:
+    """Measured ceilings on this device for the row kernel's access pattern (libcis_probe.so):
+    copy (equal read and write), read only and write only of rows x row_bytes, in GB/s."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_32444_amd", "libcis_probe.so"))
+    lib.cis_probe_bandwidth.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                                        ctypes.c_void_p, ctypes.c_void_p]
+    n = rows * row_bytes
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
     dst = torch.empty(n, dtype=torch.uint8, device="cuda")
-    for _ in range(2):
-        dst.copy_(src)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = 5
-    e0.record()
-    for _ in range(reps):
-        dst.copy_(src)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
+    sink = torch.zeros(1024, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    grid = torch.cuda.get_device_properties(0).multi_processor_count
+    out = {}
+    for mode, name, moved in ((0, "copy", 2 * n), (1, "read", n), (2, "write", n)):
+        def go():
+            rc = lib.cis_probe_bandwidth(mode, src.data_ptr(), dst.data_ptr(), rows, row_bytes,
+                                         grid, sink.data_ptr(), stream)
+            assert rc == 0, rc
+        go(); go()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(5):
+            go()
+        e1.record()
+        torch.cuda.synchronize()
+        out[name] = moved / (e0.elapsed_time(e1) / 5 * 1e-3) / 1e9
     del src, dst
-    return 2 * n / (ms * 1e-3) / 1e9
+    return out
 
 
 def cpu_baseline(b, V: int, target_s: float = 15.0):
@@ -255,7 +268,10 @@ def main():
         },
     }
     if not args.no_copy_ceiling:
-        line["roofline"]["copy_ceiling_gbs"] = copy_ceiling_gbs(min(alg, 8 << 30), torch)
+        ceil = bandwidth_ceilings(T, ((V * esize + 15) // 16) * 16, torch)
+        line["roofline"]["measured_ceiling_gbs"] = ceil
+        line["roofline"]["frac_of_measured_copy"] = achieved_gbs / ceil["copy"] if bwd else \
+            achieved_gbs / ceil["read"]
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(b, V)
     print(json.dumps(line), flush=True)

@@ -1,0 +1,36 @@
+/*
+ * cis_probe.h — bandwidth probes used to measure the roofline of the CIS row kernel
+ * (libcis_probe.so). Not part of the loss; a measurement helper for benchmarks.
+ */
+#ifndef CIS_PROBE_H
+#define CIS_PROBE_H
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * cis_probe_bandwidth — streams `rows` rows of `row_bytes` bytes with the row kernel's access
+ * pattern (one 1024-thread workgroup per row at a time, 16-byte non-temporal buffer accesses,
+ * the whole row in flight) on `stream`, without synchronising.
+ *
+ *   mode 0: copy src -> dst; 1: read src only; 2: write dst only
+ *   src, dst   device buffers of rows*row_bytes bytes (src unused in mode 2, dst in mode 1)
+ *   row_bytes  multiple of 16, at most 19*1024*16
+ *   grid       workgroups (persistent over rows), >= 1
+ *   sink       device uint32[1024] receiving nothing in practice (read mode keeps its loads
+ *              alive through it); required in mode 1
+ * Returns 0, or -1 (NULL pointer), -2 (row_bytes), -4 (mode/rows/grid), -6 (launch failed).
+ */
+int cis_probe_bandwidth(int mode, const void* src, void* dst, int64_t rows, int64_t row_bytes,
+                        int grid, uint32_t* sink, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CIS_PROBE_H */

@@ -14,6 +14,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB_PATH = os.path.join(HERE, "libcis.so")
 SOURCES = [os.path.join(HERE, "csrc", "cis_kernels.hip"), os.path.join(HERE, "csrc", "cis_api.cpp")]
+# bandwidth probes for the roofline (a separate library; not part of the loss)
+PROBE_PATH = os.path.join(HERE, "libcis_probe.so")
+PROBE_SOURCES = [os.path.join(HERE, "csrc", "bw_probe.hip")]
 HEADERS = [os.path.join(ROOT, "include", "cis.h"), os.path.join(HERE, "csrc", "cis_internal.h")]
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in device code (the compiler's host pass warns
@@ -32,10 +35,9 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (set HIPCC or install ROCm)")
 
 
-def build(verbose: bool = False) -> str:
-    """Compiles libcis.so; always recompiles. Returns the library path."""
-    tmp = LIB_PATH + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *SOURCES, "-o", tmp]
+def _compile(sources, out_path, verbose):
+    tmp = out_path + ".tmp"
+    cmd = [hipcc(), *HIPCC_FLAGS, *sources, "-o", tmp]
     proc = subprocess.run(cmd, capture_output=True, text=True)
     if proc.returncode != 0:
         sys.stderr.write(proc.stdout + proc.stderr)
@@ -45,7 +47,13 @@ def build(verbose: bool = False) -> str:
         out = "\n".join(l for l in (proc.stdout + proc.stderr).splitlines() if noise not in l)
         if out.strip():
             print(out)
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, out_path)
+
+
+def build(verbose: bool = False) -> str:
+    """Compiles libcis.so and libcis_probe.so; always recompiles. Returns libcis.so's path."""
+    _compile(SOURCES, LIB_PATH, verbose)
+    _compile(PROBE_SOURCES, PROBE_PATH, verbose)
     return LIB_PATH
 
 

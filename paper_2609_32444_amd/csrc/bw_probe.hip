@@ -1,0 +1,63 @@
+// Bandwidth probes for the roofline: plain HBM copy, read and write kernels shaped like the
+// row kernel's traffic (one 1024-thread workgroup per row, 16-byte buffer accesses, every
+// vector of a row in flight at once, non-temporal). They measure what this device achieves for
+// pure reads, pure writes and an equal mix; they are not part of the loss.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/cis_probe.h"
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kBlock = 1024;
+constexpr int kSlots = 19;
+constexpr int kRsrcWord3 = 0x00020000;
+constexpr int kAuxNT = 2;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, kRsrcWord3);
+}
+
+// mode 0: copy, 1: read only, 2: write only
+template <int MODE>
+__global__ __launch_bounds__(kBlock) void probe_kernel(const void* src, void* dst, int64_t rows,
+                                                       uint32_t row_bytes, uint32_t* sink) {
+  uint32_t acc = 0;
+  for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
+    const __amdgpu_buffer_rsrc_t rs = rsrc((const char*)src + r * row_bytes, row_bytes);
+    const __amdgpu_buffer_rsrc_t ws = rsrc((char*)dst + r * row_bytes, row_bytes);
+    u32x4 v[kSlots];
+#pragma unroll
+    for (int k = 0; k < kSlots; ++k) {
+      const uint32_t o = (threadIdx.x + k * kBlock) * 16u;
+      v[k] = MODE == 2 ? u32x4{o, o, o, o} : __builtin_amdgcn_raw_buffer_load_b128(rs, o, 0, kAuxNT);
+    }
+#pragma unroll
+    for (int k = 0; k < kSlots; ++k) {
+      const uint32_t o = (threadIdx.x + k * kBlock) * 16u;
+      if (MODE == 1)
+        acc ^= v[k].x ^ v[k].y ^ v[k].z ^ v[k].w;
+      else
+        __builtin_amdgcn_raw_buffer_store_b128(v[k], ws, o, 0, kAuxNT);
+    }
+  }
+  if (MODE == 1 && acc == 0x9E3779B9u) sink[threadIdx.x] = acc;  // keeps the loads alive
+}
+
+}  // namespace
+
+extern "C" int cis_probe_bandwidth(int mode, const void* src, void* dst, int64_t rows,
+                                   int64_t row_bytes, int grid, uint32_t* sink,
+                                   hipStream_t stream) {
+  if (mode < 0 || mode > 2 || rows < 0 || grid < 1) return -4;
+  if (row_bytes <= 0 || row_bytes % 16 != 0 || row_bytes > (int64_t)kSlots * kBlock * 16)
+    return -2;
+  if ((mode != 2 && !src) || (mode != 1 && !dst) || (mode == 1 && !sink)) return -1;
+  void* args[] = {&src, &dst, &rows, &row_bytes, &sink};
+  uint32_t rb = (uint32_t)row_bytes;
+  args[3] = &rb;
+  const void* fn = mode == 0 ? (const void*)&probe_kernel<0>
+                 : mode == 1 ? (const void*)&probe_kernel<1> : (const void*)&probe_kernel<2>;
+  return hipLaunchKernel(fn, dim3(grid), dim3(kBlock), args, 0, stream) == hipSuccess ? 0 : -6;
+}

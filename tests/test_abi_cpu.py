@@ -20,6 +20,12 @@ def declared_functions():
     return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(cis_\w+)\s*\(", text, flags=re.M)))
 
 
+def test_probe_library_exports():
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_32444_amd", "libcis_probe.so"))
+    assert hasattr(lib, "cis_probe_bandwidth")
+
+
 def test_library_exports_every_declared_symbol():
     lib = cis.load_library()
     names = declared_functions()
