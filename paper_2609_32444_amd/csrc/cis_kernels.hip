@@ -58,6 +58,7 @@ struct Bf16 {
   static constexpr int kPerVec = 8;
   static constexpr int kBytes = 2;
   static constexpr uint32_t kNegInf2 = 0xFF80FF80u;
+  static constexpr uint32_t kSignMask = 0x80008000u;
 
   __device__ static __forceinline__ void unpack(const u32x4 v, float (&f)[8]) {
 #pragma unroll
@@ -66,13 +67,11 @@ struct Bf16 {
       f[2 * k + 1] = __uint_as_float(v[k] & 0xFFFF0000u);
     }
   }
-  template <bool NEG>
-  __device__ static __forceinline__ u32x4 pack(const float (&f)[8]) {
+  __device__ static __forceinline__ u32x4 pack(const float (&f)[8]) {  // round to nearest even
     u32x4 out;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      bf16x2 p = {(__bf16)(NEG ? -f[2 * k] : f[2 * k]),
-                  (__bf16)(NEG ? -f[2 * k + 1] : f[2 * k + 1])};
+      bf16x2 p = {(__bf16)f[2 * k], (__bf16)f[2 * k + 1]};
       out[k] = __builtin_bit_cast(uint32_t, p);
     }
     return out;
@@ -117,16 +116,16 @@ struct Bf16 {
 struct F32 {
   static constexpr int kPerVec = 4;
   static constexpr int kBytes = 4;
+  static constexpr uint32_t kSignMask = 0x80000000u;
 
   __device__ static __forceinline__ void unpack(const u32x4 v, float (&f)[4]) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) f[k] = __uint_as_float(v[k]);
   }
-  template <bool NEG>
   __device__ static __forceinline__ u32x4 pack(const float (&f)[4]) {
     u32x4 out;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) out[k] = __float_as_uint(NEG ? -f[k] : f[k]);
+    for (int k = 0; k < 4; ++k) out[k] = __float_as_uint(f[k]);
     return out;
   }
   __device__ static __forceinline__ u32x4 neg_inf_vec() {
@@ -200,6 +199,24 @@ __device__ __forceinline__ void opaque(u32x4 (&r)[NV]) {
   static_for<NV>([&](auto I) { opaque_one<I>(r); });
 }
 
+// Keeps the scheduler from moving instructions across slot boundaries. Without it, once a row
+// is resident it unpacks every slot up front (one register per element) or hoists the next
+// row's loads above the current sweep (two rows of registers).
+__device__ __forceinline__ void slot_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+// Returns 0, computed after all of its inputs are available. Added to a refill load's offset,
+// it makes the load wait until the vector it overwrites has been consumed.
+__device__ __forceinline__ uint32_t after(u32x4 x) {
+  uint32_t z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z) : "v"(x));
+  return z;
+}
+__device__ __forceinline__ uint32_t after(float a, float b, float c, float d) {
+  uint32_t z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z) : "v"(a), "v"(b), "v"(c), "v"(d));
+  return z;
+}
+
 // Row geometry shared by the sweeps. Vector v = i*BLOCK + tid of the row is "slot i" of thread
 // tid; slot L = (nvec-1)/BLOCK holds the last vector. When L <= NV, slots 0..L-1 (all complete)
 // live in r[0..L-1] and slot L (possibly partial, possibly ending in padding) in one extra
@@ -214,57 +231,31 @@ struct RowGeom {
   bool rp_mine;      // this thread holds a vector of slot L
 };
 
+// Offset of slot i for this thread, or an out-of-range offset when slot i is not resident (its
+// loads then return zeros and move no data, its stores are dropped).
+template <int BLOCK>
+__device__ __forceinline__ uint32_t slot_off(int i, const RowGeom& g, uint32_t voff) {
+  return i < g.nres ? voff + (uint32_t)(i * BLOCK * 16) : kOutOfRange;
+}
+__device__ __forceinline__ uint32_t rp_off(int BLOCK, const RowGeom& g, uint32_t voff) {
+  return (g.has_rp && g.rp_mine) ? voff + (uint32_t)(g.L * BLOCK * 16) : kOutOfRange;
+}
+
 // Writes elements [0, n) of gradient vector v one by one (the partial last vector).
 template <class E>
 __device__ __forceinline__ void store_partial(void* grow, int v, u32x4 val, int n) {
   for (int e = 0; e < n; ++e) E::store_elem(grow, v * E::kPerVec + e, E::elem_bits(val, e));
 }
 
-// Writes a zero gradient row. The write descriptor covers complete vectors only.
-template <class E, int BLOCK>
-__device__ __forceinline__ void zero_row(__amdgpu_buffer_rsrc_t ws, void* grow, const RowGeom& g,
-                                         int tid) {
-  const u32x4 z = {0u, 0u, 0u, 0u};
-  for (int v = tid; v < g.nvec; v += BLOCK) bstore(z, ws, (uint32_t)v * 16u, 0u);
-  if (g.ragged && g.last_mine) store_partial<E>(grow, g.nvec - 1, z, g.tail);
-}
-
-// Gradient of one 16-byte vector of logits: sign * exp2(z*log2e - b2), rounded.
-template <class E, bool NEG>
-__device__ __forceinline__ u32x4 grad_vec(u32x4 zv, float b2) {
+// Gradient of one 16-byte vector of logits: exp2(z*log2e - b2) rounded to the storage format,
+// with the sign applied as an xor of the sign bits (sgn = 0 or the format's sign mask).
+template <class E>
+__device__ __forceinline__ u32x4 grad_vec(u32x4 zv, float b2, uint32_t sgn) {
   float f[E::kPerVec];
   E::unpack(zv, f);
 #pragma unroll
   for (int e = 0; e < E::kPerVec; ++e) f[e] = fast_exp2(__builtin_fmaf(f[e], kLog2e, -b2));
-  return E::template pack<NEG>(f);
-}
-
-// Sweep 2 of one row. Every vector is stored through the write descriptor (which drops the
-// partial last vector and out-of-range lanes); the partial last vector is then written element
-// by element, and finally the sampled element is overwritten with coef*(1-p) by the thread that
-// stored its vector (same-thread program order).
-template <class E, int BLOCK, int NV, bool NEG>
-__device__ __forceinline__ void grad_sweep(const u32x4 (&r)[NV], u32x4 rp,
-                                           __amdgpu_buffer_rsrc_t rs, __amdgpu_buffer_rsrc_t ws,
-                                           void* grow, const RowGeom& g, uint32_t voff, float b2,
-                                           int y, bool y_mine, uint32_t gy_bits) {
-  static_for<NV>([&](auto I) {
-    constexpr int i = I;
-    if (i < g.nres)
-      bstore(grad_vec<E, NEG>(r[i], b2), ws, voff + (uint32_t)(i * BLOCK * 16), 0u);
-  });
-  if (g.has_rp) {
-    bstore(grad_vec<E, NEG>(rp, b2), ws,
-           g.rp_mine ? voff + (uint32_t)(g.L * BLOCK * 16) : kOutOfRange, 0u);
-  } else {
-    for (uint32_t o = voff + (uint32_t)(NV * BLOCK * 16); o < (uint32_t)g.nvec * 16u;
-         o += (uint32_t)(BLOCK * 16))
-      bstore(grad_vec<E, NEG>(bload(rs, o, 0u), b2), ws, o, 0u);
-  }
-  if (g.ragged && g.last_mine)
-    store_partial<E>(grow, g.nvec - 1,
-                     grad_vec<E, NEG>(bload(rs, (uint32_t)(g.nvec - 1) * 16u, 0u), b2), g.tail);
-  if (y_mine) E::store_elem(grow, y, gy_bits);
+  return E::pack(f) ^ u32x4{sgn, sgn, sgn, sgn};
 }
 
 // Exp-sum of one vector relative to mb = max*log2e, optionally leaving out element `skip`.
@@ -287,7 +278,19 @@ __device__ __forceinline__ void accum_vec_skip(const float (&f)[E::kPerVec], flo
   }
 }
 
-template <class E, int BLOCK, int NV, bool BWD>
+__device__ __forceinline__ bool row_valid(const RowArgs& a, int64_t row) {
+  const int64_t y = a.ids[row];
+  return (a.mask ? (a.mask[row] != 0) : true) && y >= 0 && y < (int64_t)a.V;
+}
+
+// One persistent workgroup per row at a time.
+//   BWD: write the gradient (sweep 2); otherwise forward only.
+//   PF:  refill each register with the next row's vector during the row's last sweep, so the
+//        next row's loads overlap this row's arithmetic (the first row is loaded up front).
+//        Without PF each row's loads are issued at the top of its iteration.
+// An invalid row (masked, or id out of range) runs the same sweeps with its arithmetic skipped:
+// its loads have zero records (no data is read) and it stores a zero gradient row.
+template <class E, int BLOCK, int NV, bool BWD, bool PF>
 __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
   constexpr int EPV = E::kPerVec;
   constexpr int NW = BLOCK / 64;
@@ -297,16 +300,15 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 
   const int V = a.V;
   int buf = 0;
+  u32x4 r[NV];
+  u32x4 rp;
 
-  for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) {
-    // The row geometry is loop-invariant, but letting the compiler hoist everything derived
-    // from it (one mask or address per slot) out of the row loop exhausts the register file;
-    // re-deriving it from opaque copies each row costs a few scalar instructions.
-    int tid = threadIdx.x;
+  // Row geometry. It is loop-invariant, but letting the compiler hoist everything derived from
+  // it (one mask or address per slot) out of the row loop exhausts the register file, so it is
+  // re-derived from opaque copies each row (a few scalar instructions).
+  auto geometry = [&](int tid) {
     int nvec_r = a.nvec;
-    asm volatile("" : "+v"(tid));
     asm volatile("" : "+s"(nvec_r));
-    const int wid = __builtin_amdgcn_readfirstlane(tid) >> 6;
     RowGeom g;
     g.nvec = nvec_r;
     g.tail = V - (g.nvec - 1) * EPV;  // valid elements in the last vector, 1..EPV
@@ -316,104 +318,123 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     g.ragged = g.tail != EPV;
     g.last_mine = ((g.nvec - 1) % BLOCK) == tid;
     g.rp_mine = g.L * BLOCK + tid < g.nvec;
+    return g;
+  };
+  // Read descriptor of a row: its complete and partial vectors, or nothing for invalid rows.
+  auto row_rsrc = [&](int64_t row, bool valid, const RowGeom& g) {
+    return make_rsrc((const char*)a.logits + (valid ? row : 0) * a.row_bytes,
+                     valid ? (uint32_t)g.nvec * 16u : 0u);
+  };
+  auto load_row = [&](__amdgpu_buffer_rsrc_t rs, const RowGeom& g, uint32_t voff) {
+    static_for<NV>([&](auto I) { r[I] = bload(rs, slot_off<BLOCK>(I, g, voff), 0u); });
+    rp = bload(rs, rp_off(BLOCK, g, voff), 0u);
+  };
+
+  if (PF) {
+    int tid = threadIdx.x;
+    const RowGeom g = geometry(tid);
+    const int64_t row = blockIdx.x;
+    const bool v0 = row < a.T && row_valid(a, row);
+    load_row(row_rsrc(row, v0, g), g, (uint32_t)tid * 16u);
+  }
+
+  for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) {
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int wid = __builtin_amdgcn_readfirstlane(tid) >> 6;
+    const RowGeom g = geometry(tid);
     uint32_t voff = (uint32_t)tid * 16u;
 
     const int64_t y64 = a.ids[row];
     const bool on = a.mask ? (a.mask[row] != 0) : true;
-    const bool in_range = (y64 >= 0) && (y64 < (int64_t)V);
+    const bool valid = on && (y64 >= 0) && (y64 < (int64_t)V);
+    const int y = valid ? (int)y64 : 0;
+    const int vy = y / EPV, ey = y % EPV;
+    const int slot_y = vy / BLOCK;
+    const bool y_mine = (vy % BLOCK) == tid;
+    const __amdgpu_buffer_rsrc_t rs = row_rsrc(row, valid, g);
     void* grow = BWD ? (void*)((char*)a.dlogits + row * a.grow_bytes) : nullptr;
     // write descriptor: complete vectors only
     const __amdgpu_buffer_rsrc_t ws =
         make_rsrc(grow, BWD ? (uint32_t)(g.nvec - (g.ragged ? 1 : 0)) * 16u : 0u);
+    // the next row of this workgroup (prefetched during this row's last sweep)
+    const int64_t nrow = row + gridDim.x;
+    const bool nvalid = PF && nrow < a.T && row_valid(a, nrow);
+    const __amdgpu_buffer_rsrc_t nrs = row_rsrc(nrow, nvalid, g);
 
-    if (!(on && in_range)) {
-      if (BWD) zero_row<E, BLOCK>(ws, grow, g, tid);
-      if (tid == 0) {
-        if (a.logp_train_out) a.logp_train_out[row] = 0.f;
-        if (a.w_out) a.w_out[row] = 0.f;
-        if (a.trunc_out) a.trunc_out[row] = 0;
-        if (a.terms_user) a.terms_user[row] = 0.f;
-        a.terms_ws[row] = 0.f;
-        a.flags_ws[row] = on ? kFlagBadId : 0;
-      }
-      continue;
-    }
+    if (!PF) load_row(rs, g, voff);
 
-    const int y = (int)y64;
-    const int vy = y / EPV, ey = y % EPV;
-    const int slot_y = vy / BLOCK;
-    const bool y_mine = (vy % BLOCK) == tid;
-    const void* rowp = (const char*)a.logits + row * a.row_bytes;
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(rowp, (uint32_t)g.nvec * 16u);
-
-    // ---- load the resident part of the row ----------------------------------------------
-    u32x4 r[NV];
-    static_for<NV>([&](auto I) {
-      constexpr int i = I;
-      if (i < g.nres) r[i] = bload(rs, voff + (uint32_t)(i * BLOCK * 16), 0u);
-    });
-    u32x4 rp = E::neg_inf_vec();
-    if (g.has_rp) rp = bload(rs, g.rp_mine ? voff + (uint32_t)(g.L * BLOCK * 16) : kOutOfRange, 0u);
-    // Entries of rp that are not logits of this row become -inf: lanes past the last vector
-    // and the padding after V in a ragged last vector (after every load is in flight).
-    if (g.has_rp) {
+    // ---- sweep 1a: max ------------------------------------------------------------------
+    float m = kMinRef;
+    if (valid) {
+      // Entries of rp that are not logits of this row become -inf: lanes past the last
+      // vector and the padding after V in a ragged last vector.
       rp = g.rp_mine ? rp : E::neg_inf_vec();
       if (g.ragged && g.last_mine) rp = E::mask_tail(rp, g.tail);
-    }
-
-    // ---- sweep 1: max, then the exp-sum excluding the sampled id --------------------------
-    float m = kMinRef;
-    static_for<NV>([&](auto I) {
-      constexpr int i = I;
-      if (i < g.nres) {
-        float f[EPV];
-        E::unpack(r[i], f);
-#pragma unroll
-        for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
-      }
-    });
-    if (g.has_rp) {
-      float f[EPV];
-      E::unpack(rp, f);
-#pragma unroll
-      for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
-    } else {
-      // streamed slots NV..L: running max only (their exp-sum is taken below)
-      for (uint32_t o = voff + (uint32_t)(NV * BLOCK * 16); o < (uint32_t)g.nvec * 16u;
-           o += (uint32_t)(BLOCK * 16)) {
-        float f[EPV];
-        E::unpack(bload(rs, o, 0u), f);
-        const int j0 = (int)(o >> 4) * EPV;
-#pragma unroll
-        for (int e = 0; e < EPV; ++e)
-          if (j0 + e < V) m = fmaxf(m, f[e]);
-      }
-    }
-    opaque(r);
-    float s = 0.f;
-    float zy_mine = 0.f;
-    {
-      const float mb = m * kLog2e;
-      float acc[4] = {0.f, 0.f, 0.f, 0.f};
       static_for<NV>([&](auto I) {
         constexpr int i = I;
         if (i < g.nres) {
           float f[EPV];
           E::unpack(r[i], f);
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
+        }
+        slot_fence();
+      });
+      if (g.has_rp) {
+        float f[EPV];
+        E::unpack(rp, f);
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
+      } else {
+        // streamed slots NV..L: running max only (their exp-sum is taken below)
+        for (uint32_t o = voff + (uint32_t)(NV * BLOCK * 16); o < (uint32_t)g.nvec * 16u;
+             o += (uint32_t)(BLOCK * 16)) {
+          float f[EPV];
+          E::unpack(bload(rs, o, 0u), f);
+          const int j0 = (int)(o >> 4) * EPV;
+#pragma unroll
+          for (int e = 0; e < EPV; ++e)
+            if (j0 + e < V) m = fmaxf(m, f[e]);
+        }
+      }
+    }
+    opaque(r);
+
+    // ---- sweep 1b: exp-sum excluding the sampled id ---------------------------------------
+    // (forward only with PF: the row's last sweep, so each register is refilled with the next
+    // row's vector right after it has been read)
+    constexpr bool kRefill1 = PF && !BWD;
+    float s = 0.f, zy_mine = 0.f;
+    {
+      const float mb = m * kLog2e;
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+      static_for<NV>([&](auto I) {
+        constexpr int i = I;
+        float f[EPV];
+        E::unpack(r[i], f);
+        if (kRefill1)
+          r[i] = bload(nrs, slot_off<BLOCK>(i, g, voff) + after(f[0], f[2], f[4], f[EPV - 1]), 0u);
+        if (valid && i < g.nres) {
           if (i == slot_y)
             accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
           else
             accum_vec<E>(f, mb, acc);
         }
+        slot_fence();
       });
-      if (g.has_rp) {
+      {
         float f[EPV];
         E::unpack(rp, f);
-        if (slot_y == g.L)
-          accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
-        else
-          accum_vec<E>(f, mb, acc);
-      } else {
+        if (kRefill1) rp = bload(nrs, rp_off(BLOCK, g, voff) + after(f[0], f[2], f[4], f[EPV - 1]), 0u);
+        if (valid && g.has_rp) {
+          if (slot_y == g.L)
+            accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
+          else
+            accum_vec<E>(f, mb, acc);
+        }
+      }
+      if (valid && !g.has_rp) {
         for (uint32_t o = voff + (uint32_t)(NV * BLOCK * 16); o < (uint32_t)g.nvec * 16u;
              o += (uint32_t)(BLOCK * 16)) {
           float f[EPV];
@@ -429,63 +450,99 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
       }
       s = (acc[0] + acc[1]) + (acc[2] + acc[3]);
     }
-    opaque(r);
+    if (BWD) opaque(r);
     asm volatile("" : "+v"(voff));
 
-    // ---- block reduction (fixed order) -------------------------------------------------
-    wave_lse_reduce(m, s);
-    if ((tid & 63) == 0) {
-      sh_m[buf][wid] = m;
-      sh_s[buf][wid] = s;
-    }
-    if (y_mine) sh_zy[buf] = zy_mine;
-    __syncthreads();
-    float M = sh_m[buf][0], sr = sh_s[buf][0];
+    // ---- block reduction and epilogue: l_train, 1 - p, weight (Algorithm 1), loss term -----
+    float coef = 0.f, b2 = INFINITY, one_m_p = 0.f;
+    if (valid) {
+      wave_lse_reduce(m, s);
+      if ((tid & 63) == 0) {
+        sh_m[buf][wid] = m;
+        sh_s[buf][wid] = s;
+      }
+      if (y_mine) sh_zy[buf] = zy_mine;
+      __syncthreads();
+      float M = sh_m[buf][0], sr = sh_s[buf][0];
 #pragma unroll
-    for (int w = 1; w < NW; ++w) lse_combine(M, sr, sh_m[buf][w], sh_s[buf][w]);
-    const float zy = sh_zy[buf];
-    buf ^= 1;
-
-    // ---- epilogue: l_train, 1 - p, CIS weight (Algorithm 1), loss term ------------------
-    // M: max over the row (sampled element included); sr: sum_{j != y} exp(z_j - M).
-    const float s_rest = sr;
-    const float e_y = expf(zy - M);
-    const float ssum = e_y + s_rest;
-    const float lse = M + logf(ssum);
-    const float ltr = (e_y >= s_rest) ? -log1pf(s_rest / e_y) : (zy - M) - logf(ssum);
-    const float one_m_p = s_rest / ssum;
-    const float delta = ltr - a.logp_infer[row];
-    const float lam_phi = a.lam * fmaxf(one_m_p, a.kappa);
-    const bool trunc = delta > log1pf(lam_phi);
-    const float w = trunc ? 1.0f + lam_phi : expf(delta);
-    const float coef = a.scale * w * a.adv[row];
-    const float term = (coef == 0.f) ? 0.f : coef * ltr;
-    const bool nonfinite = !(isfinite(lse) && M > kMinRef && M < kMaxRef) || isnan(w);
-
-    if (tid == 0) {
-      if (a.logp_train_out) a.logp_train_out[row] = ltr;
-      if (a.w_out) a.w_out[row] = w;
-      if (a.trunc_out) a.trunc_out[row] = trunc ? 1 : 0;
-      if (a.terms_user) a.terms_user[row] = term;
-      a.terms_ws[row] = term;
-      a.flags_ws[row] = kFlagValid | (trunc ? kFlagTrunc : 0) | (nonfinite ? kFlagNonFinite : 0);
+      for (int w = 1; w < NW; ++w) lse_combine(M, sr, sh_m[buf][w], sh_s[buf][w]);
+      const float zy = sh_zy[buf];
+      buf ^= 1;
+      // M: max over the row (sampled element included); sr: sum_{j != y} exp(z_j - M).
+      const float s_rest = sr;
+      const float e_y = expf(zy - M);
+      const float ssum = e_y + s_rest;
+      const float lse = M + logf(ssum);
+      const float ltr = (e_y >= s_rest) ? -log1pf(s_rest / e_y) : (zy - M) - logf(ssum);
+      one_m_p = s_rest / ssum;
+      const float delta = ltr - a.logp_infer[row];
+      const float lam_phi = a.lam * fmaxf(one_m_p, a.kappa);
+      const bool trunc = delta > log1pf(lam_phi);
+      const float w = trunc ? 1.0f + lam_phi : expf(delta);
+      coef = a.scale * w * a.adv[row];
+      const float term = (coef == 0.f) ? 0.f : coef * ltr;
+      const bool nonfinite = !(isfinite(lse) && M > kMinRef && M < kMaxRef) || isnan(w);
+      if (tid == 0) {
+        if (a.logp_train_out) a.logp_train_out[row] = ltr;
+        if (a.w_out) a.w_out[row] = w;
+        if (a.trunc_out) a.trunc_out[row] = trunc ? 1 : 0;
+        if (a.terms_user) a.terms_user[row] = term;
+        a.terms_ws[row] = term;
+        a.flags_ws[row] = kFlagValid | (trunc ? kFlagTrunc : 0) | (nonfinite ? kFlagNonFinite : 0);
+      }
+      // g_j = -coef * exp(z_j - lse) = sign * exp2(z_j*log2e - b2) with sign = -sign(coef)
+      // and b2 = (lse - ln|coef|) * log2e, formed in double and rounded once; coef = 0 keeps
+      // b2 = +inf, which gives an all-zero row.
+      if (BWD && coef != 0.f) {
+        const double lse_d = (double)M + log((double)ssum);
+        b2 = (float)((lse_d - log(fabs((double)coef))) * kLog2eD);
+      }
+    } else if (tid == 0) {
+      if (a.logp_train_out) a.logp_train_out[row] = 0.f;
+      if (a.w_out) a.w_out[row] = 0.f;
+      if (a.trunc_out) a.trunc_out[row] = 0;
+      if (a.terms_user) a.terms_user[row] = 0.f;
+      a.terms_ws[row] = 0.f;
+      a.flags_ws[row] = on ? kFlagBadId : 0;
     }
 
     // ---- sweep 2: gradient ----------------------------------------------------------------
+    // Every vector is stored through the write descriptor (which drops the partial last vector
+    // and out-of-range lanes); the partial last vector is then written element by element, and
+    // finally the sampled element is overwritten with coef*(1-p) by the thread that stored its
+    // vector (same-thread program order). Invalid rows store zeros.
     if (BWD) {
-      if (coef == 0.f) {
-        zero_row<E, BLOCK>(ws, grow, g, tid);
-      } else {
-        // g_j = -coef * exp(z_j - lse) = -sign(coef) * exp2(z_j*log2e - b2) with
-        // b2 = (lse - ln|coef|) * log2e, formed in double and rounded once.
-        const double lse_d = (double)M + log((double)ssum);
-        const float b2 = (float)((lse_d - log(fabs((double)coef))) * kLog2eD);
-        const uint32_t gy_bits = E::bits_of(coef * one_m_p);
-        if (coef > 0.f)
-          grad_sweep<E, BLOCK, NV, true>(r, rp, rs, ws, grow, g, voff, b2, y, y_mine, gy_bits);
-        else
-          grad_sweep<E, BLOCK, NV, false>(r, rp, rs, ws, grow, g, voff, b2, y, y_mine, gy_bits);
+      const uint32_t sgn = coef > 0.f ? E::kSignMask : 0u;
+      static_for<NV>([&](auto I) {
+        constexpr int i = I;
+        const uint32_t o = slot_off<BLOCK>(i, g, voff);
+        u32x4 out = {0u, 0u, 0u, 0u};
+        if (valid) out = grad_vec<E>(r[i], b2, sgn);
+        if (PF) r[i] = bload(nrs, o + after(out), 0u);
+        bstore(out, ws, o, 0u);
+        slot_fence();
+      });
+      {
+        const uint32_t o = rp_off(BLOCK, g, voff);
+        u32x4 out = {0u, 0u, 0u, 0u};
+        if (valid) out = grad_vec<E>(rp, b2, sgn);
+        if (PF) rp = bload(nrs, o + after(out), 0u);
+        bstore(out, ws, o, 0u);
       }
+      if (!g.has_rp) {
+        for (uint32_t o = voff + (uint32_t)(NV * BLOCK * 16); o < (uint32_t)g.nvec * 16u;
+             o += (uint32_t)(BLOCK * 16)) {
+          u32x4 out = {0u, 0u, 0u, 0u};
+          if (valid) out = grad_vec<E>(bload(rs, o, 0u), b2, sgn);
+          bstore(out, ws, o, 0u);
+        }
+      }
+      if (g.ragged && g.last_mine) {
+        u32x4 out = {0u, 0u, 0u, 0u};
+        if (valid) out = grad_vec<E>(bload(rs, (uint32_t)(g.nvec - 1) * 16u, 0u), b2, sgn);
+        store_partial<E>(grow, g.nvec - 1, out, g.tail);
+      }
+      if (valid && y_mine) E::store_elem(grow, y, E::bits_of(coef * one_m_p));
     }
   }
 }
@@ -567,7 +624,7 @@ __global__ __launch_bounds__(kWeightsBlock) void cis_weights_kernel(const Weight
 // ------------------------------------------------------------------------------------------
 // Variant tables
 // ------------------------------------------------------------------------------------------
-#define CIS_V(E, B, N, BWD) RowVariant{B, N, (const void*)&cis_row_kernel<E, B, N, BWD>}
+#define CIS_V(E, B, N, BWD) RowVariant{B, N, (const void*)&cis_row_kernel<E, B, N, BWD, !BWD>}
 #define CIS_TABLE(E, BWD)                                                                   \
   {CIS_V(E, 256, 1, BWD),   CIS_V(E, 256, 3, BWD),                                          \
    CIS_V(E, 256, 7, BWD),   CIS_V(E, 256, 11, BWD),  CIS_V(E, 256, 15, BWD),                \
