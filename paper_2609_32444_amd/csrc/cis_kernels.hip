@@ -5,10 +5,12 @@
 // Row kernel design (one persistent workgroup per row at a time):
 //   * Each thread owns the 16-byte vectors v = tid, tid + BLOCK, ... of the row. The first
 //     NV of them stay in VGPRs from the load to the gradient store, so a row that fits in
-//     NV*BLOCK vectors is read from HBM exactly once; vectors beyond that are re-read.
-//   * Sweep 1: per-lane max, then per-lane sum of exp(z - max) excluding the sampled id
-//     (its element is set to -inf in registers), combined across the wave with shuffles and
-//     across waves through LDS in a fixed order (deterministic).
+//     NV*BLOCK vectors is read from HBM exactly once. Vectors beyond that are streamed: read
+//     once for the exp-sum and, with the gradient, once more.
+//   * Sweep 1: per-lane max over the resident vectors, an online (max, exp-sum) pass over the
+//     streamed ones, then the exp-sum of the resident vectors; the sampled id is left out of
+//     the sum. Lanes combine across the wave with shuffles and across waves through LDS in a
+//     fixed order (deterministic).
 //   * Epilogue: l_train, 1 - p (complement mass), the CIS weight of Algorithm 1 and the
 //     loss term, all computed redundantly by every thread from the same LDS values.
 //   * Sweep 2 (backward): g_j = -coef * exp(z_j - lse), evaluated as one FMA and one v_exp_f32
@@ -41,7 +43,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.44269504088896340736f;
-constexpr double kLog2eD = 1.44269504088896340736;
 // Lowest reference point for a lane's running max. Keeping every max >= -2^127 keeps
 // max*log2(e) finite, so exp(z - max) can be evaluated with a single FMA even for lanes that
 // only hold -inf (padding) entries. A row whose largest logit is outside [-2^127, 2^127] is
@@ -278,6 +279,51 @@ __device__ __forceinline__ void accum_vec_skip(const float (&f)[E::kPerVec], flo
   }
 }
 
+// Streamed part of a long row (slots NV..L): folds every logit except the sampled one into the
+// lane's running (max m, exp-sum s) online, rescaling s when the max grows; records z_y if this
+// thread holds it. Padding after V is skipped. With PIPE the next vector's load is in flight
+// while the current one is summed (four more registers).
+template <class E, int BLOCK, int NV, bool PIPE>
+__device__ __forceinline__ void stream_lse(__amdgpu_buffer_rsrc_t rs, const RowGeom& g,
+                                           uint32_t voff, int V, int y, float& m, float& s,
+                                           float& zy_mine) {
+  constexpr int EPV = E::kPerVec;
+  const uint32_t end = (uint32_t)g.nvec * 16u, step = (uint32_t)(BLOCK * 16);
+  uint32_t o = voff + (uint32_t)(NV * BLOCK * 16);
+  u32x4 cur = PIPE ? bload(rs, o < end ? o : kOutOfRange, 0u) : u32x4{0u, 0u, 0u, 0u};
+  for (; o < end; o += step) {
+    u32x4 nxt = cur;
+    if (PIPE)
+      nxt = bload(rs, o + step < end ? o + step : kOutOfRange, 0u);
+    else
+      cur = bload(rs, o, 0u);
+    float f[EPV];
+    E::unpack(cur, f);
+    const int j0 = (int)(o >> 4) * EPV;
+    if (j0 + EPV > V) {  // ragged last vector
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) f[e] = (j0 + e < V) ? f[e] : -INFINITY;
+    }
+    float mv = m;  // the max includes the sampled logit, the sum leaves it out
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) mv = fmaxf(mv, f[e]);
+    if (j0 <= y && y < j0 + EPV) {  // this vector holds the sampled logit
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) {
+        if (j0 + e == y) zy_mine = f[e];
+        f[e] = (j0 + e == y) ? -INFINITY : f[e];
+      }
+    }
+    const float mb = mv * kLog2e;
+    float acc = s * fast_exp2((m - mv) * kLog2e);
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) acc += fast_exp2(__builtin_fmaf(f[e], kLog2e, -mb));
+    s = acc;
+    m = mv;
+    cur = nxt;
+  }
+}
+
 __device__ __forceinline__ bool row_valid(const RowArgs& a, int64_t row) {
   const int64_t y = a.ids[row];
   return (a.mask ? (a.mask[row] != 0) : true) && y >= 0 && y < (int64_t)a.V;
@@ -386,26 +432,19 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
         E::unpack(rp, f);
 #pragma unroll
         for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
-      } else {
-        // streamed slots NV..L: running max only (their exp-sum is taken below)
-        for (uint32_t o = voff + (uint32_t)(NV * BLOCK * 16); o < (uint32_t)g.nvec * 16u;
-             o += (uint32_t)(BLOCK * 16)) {
-          float f[EPV];
-          E::unpack(bload(rs, o, 0u), f);
-          const int j0 = (int)(o >> 4) * EPV;
-#pragma unroll
-          for (int e = 0; e < EPV; ++e)
-            if (j0 + e < V) m = fmaxf(m, f[e]);
-        }
       }
     }
     opaque(r);
+
+    // ---- streamed slots NV..L (rows longer than the registers hold): one online pass for
+    // max and exp-sum, the next vector's load in flight while the current one is summed ------
+    float s = 0.f, zy_mine = 0.f;
+    if (valid && !g.has_rp) stream_lse<E, BLOCK, NV, !PF>(rs, g, voff, V, y, m, s, zy_mine);
 
     // ---- sweep 1b: exp-sum excluding the sampled id ---------------------------------------
     // (forward only with PF: the row's last sweep, so each register is refilled with the next
     // row's vector right after it has been read)
     constexpr bool kRefill1 = PF && !BWD;
-    float s = 0.f, zy_mine = 0.f;
     {
       const float mb = m * kLog2e;
       float acc[4] = {0.f, 0.f, 0.f, 0.f};
@@ -414,7 +453,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
         float f[EPV];
         E::unpack(r[i], f);
         if (kRefill1)
-          r[i] = bload(nrs, slot_off<BLOCK>(i, g, voff) + after(f[0], f[2], f[4], f[EPV - 1]), 0u);
+          r[i] = bload(nrs, slot_off<BLOCK>(i, g, voff) + after(f[0], f[EPV / 4], f[EPV / 2], f[EPV - 1]), 0u);
         if (valid && i < g.nres) {
           if (i == slot_y)
             accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
@@ -426,7 +465,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
       {
         float f[EPV];
         E::unpack(rp, f);
-        if (kRefill1) rp = bload(nrs, rp_off(BLOCK, g, voff) + after(f[0], f[2], f[4], f[EPV - 1]), 0u);
+        if (kRefill1) rp = bload(nrs, rp_off(BLOCK, g, voff) + after(f[0], f[EPV / 4], f[EPV / 2], f[EPV - 1]), 0u);
         if (valid && g.has_rp) {
           if (slot_y == g.L)
             accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
@@ -434,21 +473,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
             accum_vec<E>(f, mb, acc);
         }
       }
-      if (valid && !g.has_rp) {
-        for (uint32_t o = voff + (uint32_t)(NV * BLOCK * 16); o < (uint32_t)g.nvec * 16u;
-             o += (uint32_t)(BLOCK * 16)) {
-          float f[EPV];
-          E::unpack(bload(rs, o, 0u), f);
-          const int j0 = (int)(o >> 4) * EPV;
-#pragma unroll
-          for (int e = 0; e < EPV; ++e) {
-            const int j = j0 + e;
-            if (j == y) zy_mine = f[e];
-            if (j < V && j != y) acc[e & 3] += fast_exp2(__builtin_fmaf(f[e], kLog2e, -mb));
-          }
-        }
-      }
-      s = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+      s += (acc[0] + acc[1]) + (acc[2] + acc[3]);
     }
     if (BWD) opaque(r);
     asm volatile("" : "+v"(voff));
@@ -491,12 +516,9 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
         a.flags_ws[row] = kFlagValid | (trunc ? kFlagTrunc : 0) | (nonfinite ? kFlagNonFinite : 0);
       }
       // g_j = -coef * exp(z_j - lse) = sign * exp2(z_j*log2e - b2) with sign = -sign(coef)
-      // and b2 = (lse - ln|coef|) * log2e, formed in double and rounded once; coef = 0 keeps
-      // b2 = +inf, which gives an all-zero row.
-      if (BWD && coef != 0.f) {
-        const double lse_d = (double)M + log((double)ssum);
-        b2 = (float)((lse_d - log(fabs((double)coef))) * kLog2eD);
-      }
+      // and b2 = (lse - ln|coef|) * log2e; coef = 0 keeps b2 = +inf, which gives an all-zero
+      // row. The float32 offset is accurate to a few 1e-6 relative, far inside bf16 rounding.
+      if (BWD && coef != 0.f) b2 = (lse - logf(fabsf(coef))) * kLog2e;
     } else if (tid == 0) {
       if (a.logp_train_out) a.logp_train_out[row] = 0.f;
       if (a.w_out) a.w_out[row] = 0.f;
@@ -530,11 +552,16 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
         bstore(out, ws, o, 0u);
       }
       if (!g.has_rp) {
-        for (uint32_t o = voff + (uint32_t)(NV * BLOCK * 16); o < (uint32_t)g.nvec * 16u;
-             o += (uint32_t)(BLOCK * 16)) {
+        // streamed slots: re-read with the next vector's load in flight
+        const uint32_t end = (uint32_t)g.nvec * 16u, step = (uint32_t)(BLOCK * 16);
+        uint32_t o = voff + (uint32_t)(NV * BLOCK * 16);
+        u32x4 cur = bload(rs, o < end ? o : kOutOfRange, 0u);
+        for (; o < end; o += step) {
+          const u32x4 nxt = bload(rs, o + step < end ? o + step : kOutOfRange, 0u);
           u32x4 out = {0u, 0u, 0u, 0u};
-          if (valid) out = grad_vec<E>(bload(rs, o, 0u), b2, sgn);
+          if (valid) out = grad_vec<E>(cur, b2, sgn);
           bstore(out, ws, o, 0u);
+          cur = nxt;
         }
       }
       if (g.ragged && g.last_mine) {
@@ -625,16 +652,18 @@ __global__ __launch_bounds__(kWeightsBlock) void cis_weights_kernel(const Weight
 // Variant tables
 // ------------------------------------------------------------------------------------------
 #define CIS_V(E, B, N, BWD) RowVariant{B, N, (const void*)&cis_row_kernel<E, B, N, BWD, !BWD>}
-#define CIS_TABLE(E, BWD)                                                                   \
+#define CIS_TABLE(E, BWD, LAST)                                                             \
   {CIS_V(E, 256, 1, BWD),   CIS_V(E, 256, 3, BWD),                                          \
    CIS_V(E, 256, 7, BWD),   CIS_V(E, 256, 11, BWD),  CIS_V(E, 256, 15, BWD),                \
    CIS_V(E, 1024, 7, BWD),  CIS_V(E, 1024, 11, BWD), CIS_V(E, 1024, 15, BWD),               \
-   CIS_V(E, 1024, 18, BWD)}
+   CIS_V(E, 1024, LAST, BWD)}
 
-static const RowVariant kBf16Bwd[] = CIS_TABLE(Bf16, true);
-static const RowVariant kBf16Fwd[] = CIS_TABLE(Bf16, false);
-static const RowVariant kF32Bwd[] = CIS_TABLE(F32, true);
-static const RowVariant kF32Fwd[] = CIS_TABLE(F32, false);
+// The fp32 forward kernel with 18 resident slots would spill the prefetched row to scratch,
+// so its widest variant keeps 15 (longer rows stream their remainder).
+static const RowVariant kBf16Bwd[] = CIS_TABLE(Bf16, true, 18);
+static const RowVariant kBf16Fwd[] = CIS_TABLE(Bf16, false, 18);
+static const RowVariant kF32Bwd[] = CIS_TABLE(F32, true, 18);
+static const RowVariant kF32Fwd[] = CIS_TABLE(F32, false, 15);
 #undef CIS_TABLE
 #undef CIS_V
 
@@ -643,7 +672,9 @@ const RowVariant& select_row_variant(int dtype, bool bwd, int32_t nvec) {
   constexpr int n = sizeof(kBf16Bwd) / sizeof(kBf16Bwd[0]);
   for (int i = 0; i < n; ++i)
     if ((int64_t)t[i].block * (t[i].nv + 1) >= nvec) return t[i];
-  return t[n - 1];  // rows longer than 19*1024 vectors: the remainder is streamed twice
+  // longer rows: the last variant streams the vectors beyond its registers (read once for
+  // the exp-sum and, with the gradient, once more)
+  return t[n - 1];
 }
 
 const void* finalize_kernel() { return (const void*)&cis_finalize_kernel; }
