@@ -63,7 +63,8 @@ struct WeightsArgs {
 // vectors per thread.
 struct RowVariant {
   int block;
-  int nv;
+  int nv;                   // slots held in registers
+  int nl;                   // further slots held in LDS (0: the last slot sits in a register)
   const void* fn;           // __global__ function (for hipLaunchKernel / occupancy queries)
 };
 

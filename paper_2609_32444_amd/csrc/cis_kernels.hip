@@ -5,8 +5,9 @@
 // Row kernel design (one persistent workgroup per row at a time):
 //   * Each thread owns the 16-byte vectors v = tid, tid + BLOCK, ... of the row. The first
 //     NV of them stay in VGPRs from the load to the gradient store, so a row that fits in
-//     NV*BLOCK vectors is read from HBM exactly once. Vectors beyond that are streamed: read
-//     once for the exp-sum and, with the gradient, once more.
+//     NV*BLOCK vectors is read from HBM exactly once. Long rows park the next NL slots in
+//     LDS (filled by buffer loads that write LDS directly, no register round trip); vectors
+//     beyond that are streamed: read once for the exp-sum and, with the gradient, once more.
 //   * Sweep 1: per-lane max over the resident vectors, an online (max, exp-sum) pass over the
 //     streamed ones, then the exp-sum of the resident vectors; the sampled id is left out of
 //     the sum. Lanes combine across the wave with shuffles and across waves through LDS in a
@@ -172,6 +173,25 @@ __device__ __forceinline__ void bstore(u32x4 v, __amdgpu_buffer_rsrc_t r, uint32
   __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, kAuxNT);
 }
 
+// 16-byte buffer load that writes LDS directly: lane l of the wave stores its vector at
+// lds_wave + 16*l, where lds_wave is the wave's (uniform) base address. The load is counted
+// by vmcnt like any other buffer load, and the compiler does not order later LDS reads after
+// it: lds_fill_wait() must precede the first read of the data.
+__device__ __forceinline__ void bload_lds(__amdgpu_buffer_rsrc_t r, u32x4* lds_wave,
+                                          uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(
+      r, (__attribute__((address_space(3))) void*)lds_wave, 16, voff, 0, 0, kAuxNT);
+}
+__device__ __forceinline__ void lds_fill_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Elements at index >= V become -inf (the last vector of a row and lanes past it).
+template <class E>
+__device__ __forceinline__ void mask_past_end(float (&f)[E::kPerVec], int v, int V) {
+  const int j0 = v * E::kPerVec;
+#pragma unroll
+  for (int e = 0; e < E::kPerVec; ++e) f[e] = (j0 + e < V) ? f[e] : -INFINITY;
+}
+
 // (m, s) pairs represent s * exp(m): combine two of them.
 __device__ __forceinline__ void lse_combine(float& m, float& s, float m2, float s2) {
   const float mn = fmaxf(m, m2);
@@ -230,6 +250,8 @@ struct RowGeom {
   bool ragged;       // the last vector ends in padding (V % elements-per-vector != 0)
   bool last_mine;    // this thread holds the last vector
   bool rp_mine;      // this thread holds a vector of slot L
+  int nlds;          // slots NV..NV+nlds-1 live in LDS (only when slot L is not in rp)
+  int sbeg;          // first streamed slot (streaming covers sbeg..L)
 };
 
 // Offset of slot i for this thread, or an out-of-range offset when slot i is not resident (its
@@ -279,17 +301,17 @@ __device__ __forceinline__ void accum_vec_skip(const float (&f)[E::kPerVec], flo
   }
 }
 
-// Streamed part of a long row (slots NV..L): folds every logit except the sampled one into the
+// Streamed part of a long row (slots sbeg..L): folds every logit except the sampled one into the
 // lane's running (max m, exp-sum s) online, rescaling s when the max grows; records z_y if this
 // thread holds it. Padding after V is skipped. With PIPE the next vector's load is in flight
 // while the current one is summed (four more registers).
-template <class E, int BLOCK, int NV, bool PIPE>
+template <class E, int BLOCK, bool PIPE>
 __device__ __forceinline__ void stream_lse(__amdgpu_buffer_rsrc_t rs, const RowGeom& g,
                                            uint32_t voff, int V, int y, float& m, float& s,
                                            float& zy_mine) {
   constexpr int EPV = E::kPerVec;
   const uint32_t end = (uint32_t)g.nvec * 16u, step = (uint32_t)(BLOCK * 16);
-  uint32_t o = voff + (uint32_t)(NV * BLOCK * 16);
+  uint32_t o = voff + (uint32_t)g.sbeg * step;
   u32x4 cur = PIPE ? bload(rs, o < end ? o : kOutOfRange, 0u) : u32x4{0u, 0u, 0u, 0u};
   for (; o < end; o += step) {
     u32x4 nxt = cur;
@@ -336,13 +358,18 @@ __device__ __forceinline__ bool row_valid(const RowArgs& a, int64_t row) {
 //        Without PF each row's loads are issued at the top of its iteration.
 // An invalid row (masked, or id out of range) runs the same sweeps with its arithmetic skipped:
 // its loads have zero records (no data is read) and it stores a zero gradient row.
-template <class E, int BLOCK, int NV, bool BWD, bool PF>
+//   NL:  slots held in LDS for rows longer than NV+1 slots (BWD only: the forward pass reads
+//        every vector once anyway).
+template <class E, int BLOCK, int NV, int NL, bool BWD, bool PF>
 __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
+  static_assert(NL == 0 || (BWD && !PF), "LDS slots are for the fused pass");
   constexpr int EPV = E::kPerVec;
   constexpr int NW = BLOCK / 64;
   __shared__ float sh_m[2][NW];
   __shared__ float sh_s[2][NW];
   __shared__ float sh_zy[2];
+  // slot NV+k of thread tid at lds_row[k*BLOCK + tid]; each wave fills and reads its own part
+  __shared__ u32x4 lds_row[NL > 0 ? NL * BLOCK : 1];
 
   const int V = a.V;
   int buf = 0;
@@ -364,6 +391,8 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     g.ragged = g.tail != EPV;
     g.last_mine = ((g.nvec - 1) % BLOCK) == tid;
     g.rp_mine = g.L * BLOCK + tid < g.nvec;
+    g.nlds = g.has_rp ? 0 : min(NL, g.L + 1 - NV);
+    g.sbeg = NV + g.nlds;
     return g;
   };
   // Read descriptor of a row: its complete and partial vectors, or nothing for invalid rows.
@@ -371,9 +400,22 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     return make_rsrc((const char*)a.logits + (valid ? row : 0) * a.row_bytes,
                      valid ? (uint32_t)g.nvec * 16u : 0u);
   };
-  auto load_row = [&](__amdgpu_buffer_rsrc_t rs, const RowGeom& g, uint32_t voff) {
+  auto load_row = [&](__amdgpu_buffer_rsrc_t rs, const RowGeom& g, uint32_t voff, int wid) {
     static_for<NV>([&](auto I) { r[I] = bload(rs, slot_off<BLOCK>(I, g, voff), 0u); });
     rp = bload(rs, rp_off(BLOCK, g, voff), 0u);
+    // (unused LDS slots get out-of-range offsets rather than a branch, so every row issues
+    // the same loads and the compiler's wait counts stay exact)
+    static_for<NL>([&](auto K) {
+      constexpr int k = K;
+      const uint32_t o = k < g.nlds ? voff + (uint32_t)((NV + k) * BLOCK * 16) : kOutOfRange;
+      bload_lds(rs, &lds_row[k * BLOCK + wid * 64], o);
+    });
+  };
+  // vector of LDS slot k (unpacked), with elements past the row's end set to -inf when slot
+  // k is the row's last
+  auto lds_vec = [&](int k, const RowGeom& g, int tid, float (&f)[EPV]) {
+    E::unpack(lds_row[k * BLOCK + tid], f);
+    if (NV + k == g.L) mask_past_end<E>(f, g.L * BLOCK + tid, V);
   };
 
   if (PF) {
@@ -381,7 +423,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     const RowGeom g = geometry(tid);
     const int64_t row = blockIdx.x;
     const bool v0 = row < a.T && row_valid(a, row);
-    load_row(row_rsrc(row, v0, g), g, (uint32_t)tid * 16u);
+    load_row(row_rsrc(row, v0, g), g, (uint32_t)tid * 16u, 0);
   }
 
   for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) {
@@ -408,15 +450,11 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     const bool nvalid = PF && nrow < a.T && row_valid(a, nrow);
     const __amdgpu_buffer_rsrc_t nrs = row_rsrc(nrow, nvalid, g);
 
-    if (!PF) load_row(rs, g, voff);
+    if (!PF) load_row(rs, g, voff, wid);
 
     // ---- sweep 1a: max ------------------------------------------------------------------
     float m = kMinRef;
     if (valid) {
-      // Entries of rp that are not logits of this row become -inf: lanes past the last
-      // vector and the padding after V in a ragged last vector.
-      rp = g.rp_mine ? rp : E::neg_inf_vec();
-      if (g.ragged && g.last_mine) rp = E::mask_tail(rp, g.tail);
       static_for<NV>([&](auto I) {
         constexpr int i = I;
         if (i < g.nres) {
@@ -427,11 +465,27 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
         }
         slot_fence();
       });
+      // Entries of rp that are not logits of this row become -inf: lanes past the last
+      // vector and the padding after V in a ragged last vector.
+      rp = g.rp_mine ? rp : E::neg_inf_vec();
+      if (g.ragged && g.last_mine) rp = E::mask_tail(rp, g.tail);
       if (g.has_rp) {
         float f[EPV];
         E::unpack(rp, f);
 #pragma unroll
         for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
+      }
+      if (NL > 0 && g.nlds > 0) {
+        lds_fill_wait();
+        static_for<NL>([&](auto K) {
+          constexpr int k = K;
+          if (k < g.nlds) {
+            float f[EPV];
+            lds_vec(k, g, tid, f);
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
+          }
+        });
       }
     }
     opaque(r);
@@ -439,7 +493,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     // ---- streamed slots NV..L (rows longer than the registers hold): one online pass for
     // max and exp-sum, the next vector's load in flight while the current one is summed ------
     float s = 0.f, zy_mine = 0.f;
-    if (valid && !g.has_rp) stream_lse<E, BLOCK, NV, !PF>(rs, g, voff, V, y, m, s, zy_mine);
+    if (valid && !g.has_rp) stream_lse<E, BLOCK, !PF>(rs, g, voff, V, y, m, s, zy_mine);
 
     // ---- sweep 1b: exp-sum excluding the sampled id ---------------------------------------
     // (forward only with PF: the row's last sweep, so each register is refilled with the next
@@ -472,6 +526,19 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
           else
             accum_vec<E>(f, mb, acc);
         }
+      }
+      if (NL > 0 && valid) {
+        static_for<NL>([&](auto K) {
+          constexpr int k = K;
+          if (k < g.nlds) {
+            float f[EPV];
+            lds_vec(k, g, tid, f);
+            if (NV + k == slot_y)
+              accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
+            else
+              accum_vec<E>(f, mb, acc);
+          }
+        });
       }
       s += (acc[0] + acc[1]) + (acc[2] + acc[3]);
     }
@@ -551,10 +618,18 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
         if (PF) rp = bload(nrs, o + after(out), 0u);
         bstore(out, ws, o, 0u);
       }
+      static_for<NL>([&](auto K) {
+        constexpr int k = K;
+        if (k < g.nlds) {
+          u32x4 out = {0u, 0u, 0u, 0u};
+          if (valid) out = grad_vec<E>(lds_row[k * BLOCK + tid], b2, sgn);
+          bstore(out, ws, voff + (uint32_t)((NV + k) * BLOCK * 16), 0u);
+        }
+      });
       if (!g.has_rp) {
         // streamed slots: re-read with the next vector's load in flight
         const uint32_t end = (uint32_t)g.nvec * 16u, step = (uint32_t)(BLOCK * 16);
-        uint32_t o = voff + (uint32_t)(NV * BLOCK * 16);
+        uint32_t o = voff + (uint32_t)g.sbeg * step;
         u32x4 cur = bload(rs, o < end ? o : kOutOfRange, 0u);
         for (; o < end; o += step) {
           const u32x4 nxt = bload(rs, o + step < end ? o + step : kOutOfRange, 0u);
@@ -651,19 +726,21 @@ __global__ __launch_bounds__(kWeightsBlock) void cis_weights_kernel(const Weight
 // ------------------------------------------------------------------------------------------
 // Variant tables
 // ------------------------------------------------------------------------------------------
-#define CIS_V(E, B, N, BWD) RowVariant{B, N, (const void*)&cis_row_kernel<E, B, N, BWD, !BWD>}
-#define CIS_TABLE(E, BWD, LAST)                                                             \
-  {CIS_V(E, 256, 1, BWD),   CIS_V(E, 256, 3, BWD),                                          \
-   CIS_V(E, 256, 7, BWD),   CIS_V(E, 256, 11, BWD),  CIS_V(E, 256, 15, BWD),                \
-   CIS_V(E, 1024, 7, BWD),  CIS_V(E, 1024, 11, BWD), CIS_V(E, 1024, 15, BWD),               \
-   CIS_V(E, 1024, LAST, BWD)}
+#define CIS_V(E, B, N, L, BWD) \
+  RowVariant{B, N, L, (const void*)&cis_row_kernel<E, B, N, L, BWD, !BWD>}
+#define CIS_TABLE(E, BWD, LAST, LDS)                                                        \
+  {CIS_V(E, 256, 1, 0, BWD),   CIS_V(E, 256, 3, 0, BWD),                                    \
+   CIS_V(E, 256, 7, 0, BWD),   CIS_V(E, 256, 11, 0, BWD),  CIS_V(E, 256, 15, 0, BWD),       \
+   CIS_V(E, 1024, 7, 0, BWD),  CIS_V(E, 1024, 11, 0, BWD), CIS_V(E, 1024, 15, 0, BWD),      \
+   CIS_V(E, 1024, LAST, 0, BWD), CIS_V(E, 1024, LAST, LDS, BWD)}
 
 // The fp32 forward kernel with 18 resident slots would spill the prefetched row to scratch,
-// so its widest variant keeps 15 (longer rows stream their remainder).
-static const RowVariant kBf16Bwd[] = CIS_TABLE(Bf16, true, 18);
-static const RowVariant kBf16Fwd[] = CIS_TABLE(Bf16, false, 18);
-static const RowVariant kF32Bwd[] = CIS_TABLE(F32, true, 18);
-static const RowVariant kF32Fwd[] = CIS_TABLE(F32, false, 15);
+// so its widest variant keeps 15 (longer rows stream their remainder). The fused pass adds 9
+// LDS slots (144 KiB) for long rows; the forward pass reads each vector once without them.
+static const RowVariant kBf16Bwd[] = CIS_TABLE(Bf16, true, 18, 9);
+static const RowVariant kBf16Fwd[] = CIS_TABLE(Bf16, false, 18, 0);
+static const RowVariant kF32Bwd[] = CIS_TABLE(F32, true, 18, 9);
+static const RowVariant kF32Fwd[] = CIS_TABLE(F32, false, 15, 0);
 #undef CIS_TABLE
 #undef CIS_V
 
@@ -671,7 +748,7 @@ const RowVariant& select_row_variant(int dtype, bool bwd, int32_t nvec) {
   const RowVariant* t = dtype == CIS_BF16 ? (bwd ? kBf16Bwd : kBf16Fwd) : (bwd ? kF32Bwd : kF32Fwd);
   constexpr int n = sizeof(kBf16Bwd) / sizeof(kBf16Bwd[0]);
   for (int i = 0; i < n; ++i)
-    if ((int64_t)t[i].block * (t[i].nv + 1) >= nvec) return t[i];
+    if ((int64_t)t[i].block * (t[i].nv + (t[i].nl > 0 ? t[i].nl : 1)) >= nvec) return t[i];
   // longer rows: the last variant streams the vectors beyond its registers (read once for
   // the exp-sum and, with the gradient, once more)
   return t[n - 1];

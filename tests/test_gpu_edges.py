@@ -37,9 +37,11 @@ def run_and_check(b, bwd=True, report=None, **kw):
 
 # V values chosen to hit every row-kernel variant of both element types, ragged last vectors
 # (V % 8 != 0), single partial vectors, and rows longer than the register-resident capacity.
+# The fused kernel holds up to 19*1024 vectors in registers and 9*1024 more in LDS (bf16:
+# 155648 and 221184 logits; fp32: 77824 and 110592); longer rows stream the rest.
 BF16_VS = [1, 2, 7, 8, 9, 1000, 1001, 2048, 2049, 8192, 16384, 30000, 32768, 65536, 100000,
-           151936, 160000, 200000]
-F32_VS = [1, 3, 4, 5, 1024, 4097, 20000, 70000]
+           151936, 155648, 155649, 160000, 200000, 200003, 221184, 221185, 250001]
+F32_VS = [1, 3, 4, 5, 1024, 4097, 20000, 70000, 77825, 90001, 110592, 130001]
 
 
 @pytest.mark.parametrize("V", BF16_VS)
@@ -54,6 +56,15 @@ def test_bf16_vocab_sizes(V):
 def test_f32_vocab_sizes(V):
     ld = ((V + 3) // 4) * 4
     b = make_random_batch(16, V, torch.float32, DEV, seed=V + 1, ld=ld, mask_p=0.85)
+    run_and_check(b)
+
+
+@pytest.mark.parametrize("V,dtype", [(200003, torch.bfloat16), (90001, torch.float32)])
+def test_long_rows_many_per_workgroup(V, dtype):
+    # more rows than resident workgroups: each workgroup refills its LDS slots row after row
+    epv = 8 if dtype == torch.bfloat16 else 4
+    ld = ((V + epv - 1) // epv) * epv
+    b = make_random_batch(600, V, dtype, DEV, seed=V + 7, ld=ld, mask_p=0.9)
     run_and_check(b)
 
 
