@@ -346,9 +346,37 @@ __device__ __forceinline__ void stream_lse(__amdgpu_buffer_rsrc_t rs, const RowG
   }
 }
 
-__device__ __forceinline__ bool row_valid(const RowArgs& a, int64_t row) {
-  const int64_t y = a.ids[row];
-  return (a.mask ? (a.mask[row] != 0) : true) && y >= 0 && y < (int64_t)a.V;
+// Per-row inputs other than the logits. Each workgroup fetches them one row ahead, so their
+// load latency overlaps the previous row instead of stalling the start (or the epilogue) of
+// the row that needs them.
+struct RowScalars {
+  int64_t y;
+  float logp_infer, adv;
+  bool on;  // mask bit (true when there is no mask)
+  __device__ bool valid(int V) const { return on && y >= 0 && y < (int64_t)V; }
+};
+// Scalar (SGPR) load of a kernel input that no thread writes while the kernel runs; the row
+// index is uniform, so one load serves the whole wave and the value stays out of VGPRs.
+template <class T>
+__device__ __forceinline__ T sload(const T* p) {
+  return *(const __attribute__((address_space(4))) T*)p;
+}
+// Byte `i` of a uint8 array through a scalar load of the aligned 4-byte word that holds it
+// (scalar loads read whole dwords; the word never crosses a page, so it is always mapped).
+__device__ __forceinline__ uint32_t sload_byte(const uint8_t* p, int64_t i) {
+  const uintptr_t addr = (uintptr_t)(p + i);
+  const uint32_t word = sload((const uint32_t*)(addr & ~(uintptr_t)3));
+  return (word >> (8u * (uint32_t)(addr & 3))) & 0xFFu;
+}
+__device__ __forceinline__ RowScalars fetch_row_scalars(const RowArgs& a, int64_t row) {
+  RowScalars s{0, 0.f, 0.f, false};
+  if (row < a.T) {
+    s.y = sload(a.ids + row);
+    s.on = a.mask ? (sload_byte(a.mask, row) != 0) : true;
+    s.logp_infer = sload(a.logp_infer + row);
+    s.adv = sload(a.adv + row);
+  }
+  return s;
 }
 
 // One persistent workgroup per row at a time.
@@ -422,10 +450,11 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     int tid = threadIdx.x;
     const RowGeom g = geometry(tid);
     const int64_t row = blockIdx.x;
-    const bool v0 = row < a.T && row_valid(a, row);
+    const bool v0 = fetch_row_scalars(a, row).valid(V);
     load_row(row_rsrc(row, v0, g), g, (uint32_t)tid * 16u, 0);
   }
 
+  RowScalars cur = fetch_row_scalars(a, blockIdx.x);
   for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) {
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
@@ -433,10 +462,11 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     const RowGeom g = geometry(tid);
     uint32_t voff = (uint32_t)tid * 16u;
 
-    const int64_t y64 = a.ids[row];
-    const bool on = a.mask ? (a.mask[row] != 0) : true;
-    const bool valid = on && (y64 >= 0) && (y64 < (int64_t)V);
-    const int y = valid ? (int)y64 : 0;
+    const RowScalars rsc = cur;
+    const int64_t nrow = row + gridDim.x;
+    cur = fetch_row_scalars(a, nrow);  // the next row's, for the next iteration
+    const bool valid = rsc.valid(V);
+    const int y = valid ? (int)rsc.y : 0;
     const int vy = y / EPV, ey = y % EPV;
     const int slot_y = vy / BLOCK;
     const bool y_mine = (vy % BLOCK) == tid;
@@ -446,8 +476,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     const __amdgpu_buffer_rsrc_t ws =
         make_rsrc(grow, BWD ? (uint32_t)(g.nvec - (g.ragged ? 1 : 0)) * 16u : 0u);
     // the next row of this workgroup (prefetched during this row's last sweep)
-    const int64_t nrow = row + gridDim.x;
-    const bool nvalid = PF && nrow < a.T && row_valid(a, nrow);
+    const bool nvalid = PF && cur.valid(V);
     const __amdgpu_buffer_rsrc_t nrs = row_rsrc(nrow, nvalid, g);
 
     if (!PF) load_row(rs, g, voff, wid);
@@ -567,11 +596,11 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
       const float lse = M + logf(ssum);
       const float ltr = (e_y >= s_rest) ? -log1pf(s_rest / e_y) : (zy - M) - logf(ssum);
       one_m_p = s_rest / ssum;
-      const float delta = ltr - a.logp_infer[row];
+      const float delta = ltr - rsc.logp_infer;
       const float lam_phi = a.lam * fmaxf(one_m_p, a.kappa);
       const bool trunc = delta > log1pf(lam_phi);
       const float w = trunc ? 1.0f + lam_phi : expf(delta);
-      coef = a.scale * w * a.adv[row];
+      coef = a.scale * w * rsc.adv;
       const float term = (coef == 0.f) ? 0.f : coef * ltr;
       const bool nonfinite = !(isfinite(lse) && M > kMinRef && M < kMaxRef) || isnan(w);
       if (tid == 0) {
@@ -592,7 +621,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
       if (a.trunc_out) a.trunc_out[row] = 0;
       if (a.terms_user) a.terms_user[row] = 0.f;
       a.terms_ws[row] = 0.f;
-      a.flags_ws[row] = on ? kFlagBadId : 0;
+      a.flags_ws[row] = rsc.on ? kFlagBadId : 0;
     }
 
     // ---- sweep 2: gradient ----------------------------------------------------------------
