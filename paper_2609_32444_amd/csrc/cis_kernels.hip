@@ -757,25 +757,37 @@ __global__ __launch_bounds__(kWeightsBlock) void cis_weights_kernel(const Weight
 // ------------------------------------------------------------------------------------------
 #define CIS_V(E, B, N, L, BWD) \
   RowVariant{B, N, L, (const void*)&cis_row_kernel<E, B, N, L, BWD, !BWD>}
-#define CIS_TABLE(E, BWD, LAST, LDS)                                                        \
-  {CIS_V(E, 256, 1, 0, BWD),   CIS_V(E, 256, 3, 0, BWD),                                    \
-   CIS_V(E, 256, 7, 0, BWD),   CIS_V(E, 256, 11, 0, BWD),  CIS_V(E, 256, 15, 0, BWD),       \
-   CIS_V(E, 1024, 7, 0, BWD),  CIS_V(E, 1024, 11, 0, BWD), CIS_V(E, 1024, 15, 0, BWD),      \
-   CIS_V(E, 1024, LAST, 0, BWD), CIS_V(E, 1024, LAST, LDS, BWD)}
 
-// The fp32 forward kernel with 18 resident slots would spill the prefetched row to scratch,
-// so its widest variant keeps 15 (longer rows stream their remainder). The fused pass adds 9
-// LDS slots (144 KiB) for long rows; the forward pass reads each vector once without them.
-static const RowVariant kBf16Bwd[] = CIS_TABLE(Bf16, true, 18, 9);
-static const RowVariant kBf16Fwd[] = CIS_TABLE(Bf16, false, 18, 0);
-static const RowVariant kF32Bwd[] = CIS_TABLE(F32, true, 18, 9);
-static const RowVariant kF32Fwd[] = CIS_TABLE(F32, false, 15, 0);
-#undef CIS_TABLE
+// Row capacity of a variant: block*(nv+1) vectors (block*(nv+nl) with LDS slots); a row goes
+// to the first variant that holds it. The ladders were chosen by timing every (block, nv)
+// pair over V = 1024 ... 262144: small blocks with many slots per thread win on short rows
+// (more rows in flight per CU), 1024-thread blocks on long ones. The fused pass prefers
+// fewer slots per thread than the forward pass, and adds 9 LDS slots (144 KiB) for rows
+// beyond its registers; the fp32 forward kernel stops at 15 slots (18 would spill the
+// prefetched row to scratch).
+#define CIS_BWD_TABLE(E)                                                                    \
+  {CIS_V(E, 64, 1, 0, true),    CIS_V(E, 64, 3, 0, true),    CIS_V(E, 64, 7, 0, true),     \
+   CIS_V(E, 64, 15, 0, true),   CIS_V(E, 512, 3, 0, true),   CIS_V(E, 512, 9, 0, true),    \
+   CIS_V(E, 1024, 7, 0, true),  CIS_V(E, 1024, 11, 0, true), CIS_V(E, 1024, 15, 0, true),  \
+   CIS_V(E, 1024, 18, 0, true), CIS_V(E, 1024, 18, 9, true)}
+#define CIS_FWD_TABLE(E, LAST)                                                              \
+  {CIS_V(E, 64, 1, 0, false),   CIS_V(E, 64, 3, 0, false),   CIS_V(E, 64, 7, 0, false),    \
+   CIS_V(E, 64, 15, 0, false),  CIS_V(E, 128, 15, 0, false), CIS_V(E, 256, 15, 0, false),  \
+   CIS_V(E, 512, 15, 0, false), CIS_V(E, 1024, 11, 0, false), CIS_V(E, 1024, LAST, 0, false)}
+
+static const RowVariant kBf16Bwd[] = CIS_BWD_TABLE(Bf16);
+static const RowVariant kBf16Fwd[] = CIS_FWD_TABLE(Bf16, 18);
+static const RowVariant kF32Bwd[] = CIS_BWD_TABLE(F32);
+static const RowVariant kF32Fwd[] = CIS_FWD_TABLE(F32, 15);
+#undef CIS_BWD_TABLE
+#undef CIS_FWD_TABLE
 #undef CIS_V
 
 const RowVariant& select_row_variant(int dtype, bool bwd, int32_t nvec) {
+  constexpr int nb = sizeof(kBf16Bwd) / sizeof(kBf16Bwd[0]);
+  constexpr int nf = sizeof(kBf16Fwd) / sizeof(kBf16Fwd[0]);
   const RowVariant* t = dtype == CIS_BF16 ? (bwd ? kBf16Bwd : kBf16Fwd) : (bwd ? kF32Bwd : kF32Fwd);
-  constexpr int n = sizeof(kBf16Bwd) / sizeof(kBf16Bwd[0]);
+  const int n = bwd ? nb : nf;
   for (int i = 0; i < n; ++i)
     if ((int64_t)t[i].block * (t[i].nv + (t[i].nl > 0 ? t[i].nl : 1)) >= nvec) return t[i];
   // longer rows: the last variant streams the vectors beyond its registers (read once for

@@ -37,11 +37,14 @@ def run_and_check(b, bwd=True, report=None, **kw):
 
 # V values chosen to hit every row-kernel variant of both element types, ragged last vectors
 # (V % 8 != 0), single partial vectors, and rows longer than the register-resident capacity.
-# The fused kernel holds up to 19*1024 vectors in registers and 9*1024 more in LDS (bf16:
-# 155648 and 221184 logits; fp32: 77824 and 110592); longer rows stream the rest.
-BF16_VS = [1, 2, 7, 8, 9, 1000, 1001, 2048, 2049, 8192, 16384, 30000, 32768, 65536, 100000,
-           151936, 155648, 155649, 160000, 200000, 200003, 221184, 221185, 250001]
-F32_VS = [1, 3, 4, 5, 1024, 4097, 20000, 70000, 77825, 90001, 110592, 130001]
+# Fused-pass row capacities in 16-byte vectors: 128, 256, 512, 1024, 2048, 5120, 8192, 12288,
+# 16384, 19456 in registers, then 27648 with LDS (bf16: 8 logits per vector, fp32: 4); longer
+# rows stream the rest. The lists put rows in every variant, at and just past capacities.
+BF16_VS = [1, 2, 7, 8, 9, 1000, 1001, 2048, 2049, 4097, 8192, 12000, 16384, 30000, 32768,
+           40961, 65536, 90001, 100000, 130001, 151936, 155648, 155649, 160000, 200000, 200003,
+           221184, 221185, 250001]
+F32_VS = [1, 3, 4, 5, 1024, 2000, 3000, 4097, 20000, 30001, 45001, 60001, 70000, 77825, 90001,
+          110592, 130001]
 
 
 @pytest.mark.parametrize("V", BF16_VS)
@@ -68,9 +71,16 @@ def test_long_rows_many_per_workgroup(V, dtype):
     run_and_check(b)
 
 
-@pytest.mark.parametrize("V", [1000, 151936, 262144])
-def test_forward_only_matches(V):
-    b = make_random_batch(12, V, torch.bfloat16, DEV, seed=5, mask_p=0.8)
+# forward-pass capacities (vectors): 128, 256, 512, 1024, 2048, 4096, 8192, 12288, then 19456
+# (bf16) or 16384 (fp32), beyond which rows stream
+@pytest.mark.parametrize("V,dtype", [(V, torch.bfloat16) for V in
+                                     (1000, 2048, 4000, 8000, 16000, 30001, 60000, 90001, 151936,
+                                      155649, 262144)] +
+                                    [(V, torch.float32) for V in (1000, 16000, 60001, 65537)])
+def test_forward_only_matches(V, dtype):
+    epv = 8 if dtype == torch.bfloat16 else 4
+    ld = ((V + epv - 1) // epv) * epv
+    b = make_random_batch(12, V, dtype, DEV, seed=5, mask_p=0.8, ld=ld)
     run_and_check(b, bwd=False)
 
 
