@@ -755,25 +755,30 @@ __global__ __launch_bounds__(kWeightsBlock) void cis_weights_kernel(const Weight
 // ------------------------------------------------------------------------------------------
 // Variant tables
 // ------------------------------------------------------------------------------------------
-#define CIS_V(E, B, N, L, BWD) \
-  RowVariant{B, N, L, (const void*)&cis_row_kernel<E, B, N, L, BWD, !BWD>}
+#define CIS_V(E, B, N, L, BWD, PF) \
+  RowVariant{B, N, L, (const void*)&cis_row_kernel<E, B, N, L, BWD, PF>}
 
 // Row capacity of a variant: block*(nv+1) vectors (block*(nv+nl) with LDS slots); a row goes
 // to the first variant that holds it. The ladders were chosen by timing every (block, nv)
 // pair over V = 1024 ... 262144: small blocks with many slots per thread win on short rows
 // (more rows in flight per CU), 1024-thread blocks on long ones. The fused pass prefers
-// fewer slots per thread than the forward pass, and adds 9 LDS slots (144 KiB) for rows
-// beyond its registers; the fp32 forward kernel stops at 15 slots (18 would spill the
-// prefetched row to scratch).
+// fewer slots per thread than the forward pass, prefetches the next row during the gradient
+// sweep only on short rows (on long ones it costs more than it hides), and adds 9 LDS slots
+// (144 KiB) for rows beyond its registers. The fp32 forward kernel stops at 15 slots (18
+// would spill the prefetched row to scratch).
 #define CIS_BWD_TABLE(E)                                                                    \
-  {CIS_V(E, 64, 1, 0, true),    CIS_V(E, 64, 3, 0, true),    CIS_V(E, 64, 7, 0, true),     \
-   CIS_V(E, 64, 15, 0, true),   CIS_V(E, 512, 3, 0, true),   CIS_V(E, 512, 9, 0, true),    \
-   CIS_V(E, 1024, 7, 0, true),  CIS_V(E, 1024, 11, 0, true), CIS_V(E, 1024, 15, 0, true),  \
-   CIS_V(E, 1024, 18, 0, true), CIS_V(E, 1024, 18, 9, true)}
+  {CIS_V(E, 64, 1, 0, true, true),     CIS_V(E, 64, 3, 0, true, true),                      \
+   CIS_V(E, 64, 7, 0, true, true),     CIS_V(E, 64, 15, 0, true, true),                     \
+   CIS_V(E, 512, 3, 0, true, false),   CIS_V(E, 256, 15, 0, true, true),                    \
+   CIS_V(E, 1024, 7, 0, true, false),  CIS_V(E, 1024, 11, 0, true, false),                  \
+   CIS_V(E, 1024, 15, 0, true, false), CIS_V(E, 1024, 18, 0, true, false),                  \
+   CIS_V(E, 1024, 18, 9, true, false)}
 #define CIS_FWD_TABLE(E, LAST)                                                              \
-  {CIS_V(E, 64, 1, 0, false),   CIS_V(E, 64, 3, 0, false),   CIS_V(E, 64, 7, 0, false),    \
-   CIS_V(E, 64, 15, 0, false),  CIS_V(E, 128, 15, 0, false), CIS_V(E, 256, 15, 0, false),  \
-   CIS_V(E, 512, 15, 0, false), CIS_V(E, 1024, 11, 0, false), CIS_V(E, 1024, LAST, 0, false)}
+  {CIS_V(E, 64, 1, 0, false, true),    CIS_V(E, 64, 3, 0, false, true),                     \
+   CIS_V(E, 64, 7, 0, false, true),    CIS_V(E, 64, 15, 0, false, true),                    \
+   CIS_V(E, 128, 15, 0, false, true),  CIS_V(E, 256, 15, 0, false, true),                   \
+   CIS_V(E, 512, 15, 0, false, true),  CIS_V(E, 1024, 11, 0, false, true),                  \
+   CIS_V(E, 1024, LAST, 0, false, true)}
 
 static const RowVariant kBf16Bwd[] = CIS_BWD_TABLE(Bf16);
 static const RowVariant kBf16Fwd[] = CIS_FWD_TABLE(Bf16, 18);

@@ -37,7 +37,7 @@ def run_and_check(b, bwd=True, report=None, **kw):
 
 # V values chosen to hit every row-kernel variant of both element types, ragged last vectors
 # (V % 8 != 0), single partial vectors, and rows longer than the register-resident capacity.
-# Fused-pass row capacities in 16-byte vectors: 128, 256, 512, 1024, 2048, 5120, 8192, 12288,
+# Fused-pass row capacities in 16-byte vectors: 128, 256, 512, 1024, 2048, 4096, 8192, 12288,
 # 16384, 19456 in registers, then 27648 with LDS (bf16: 8 logits per vector, fp32: 4); longer
 # rows stream the rest. The lists put rows in every variant, at and just past capacities.
 BF16_VS = [1, 2, 7, 8, 9, 1000, 1001, 2048, 2049, 4097, 8192, 12000, 16384, 30000, 32768,
