@@ -59,7 +59,8 @@ enum {
   CIS_ERR_NULL = -1,      /* a required pointer is NULL                                       */
   CIS_ERR_SHAPE = -2,     /* T < 0, V outside [1, 2^28], ld < V or ld_g < V                  */
   CIS_ERR_DTYPE = -3,     /* dtype is not a cis_dtype_t                                       */
-  CIS_ERR_PARAM = -4,     /* lambda < 0 or not finite, kappa outside [0,1], scale not finite  */
+  CIS_ERR_PARAM = -4,     /* lambda < 0 or not finite, kappa outside [0,1], scale not finite, */
+                          /* an unknown operator or bounds outside their ranges (cis_params_t) */
   CIS_ERR_ALIGN = -5,     /* logits/dlogits base or row stride in bytes not a multiple of 16; */
                           /* workspace not 256-byte aligned                                   */
   CIS_ERR_LAUNCH = -6,    /* the HIP runtime rejected a kernel launch                         */
@@ -68,21 +69,30 @@ enum {
   CIS_ERR_DEVICE = -9     /* the current device is not a gfx950 GPU, or no device            */
 };
 
-/* Per-call statistics, written at byte offset 0 of the workspace by cis_loss_fwd/_bwd once
- * every row is done (read it after synchronising the stream). */
+/* Per-call statistics, written at byte offset 0 of the workspace by every entry point that
+ * takes a workspace, once every row is done (read it after synchronising the stream). The
+ * last three fields are the training diagnostics of App. D.4/D.5. */
 typedef struct cis_stats {
   double  loss;         /* sum_t term_t, accumulated in double in a fixed order             */
   int64_t n_valid;      /* rows with mask != 0 and 0 <= id < V                              */
   int64_t n_bad_id;     /* rows with mask != 0 and id outside [0, V)                        */
   int64_t n_nonfinite;  /* valid rows whose log-sum-exp is not finite or whose w is NaN     */
-  int64_t n_trunc;      /* valid rows whose weight was truncated (k > 1 + lambda*phi)      */
-  int64_t reserved[3];
+  int64_t n_trunc;      /* valid rows the operator acted on ("acted on", App. D.4): for CIS */
+                        /* the truncated rows (k > 1 + lambda*phi)                          */
+  double  max_abs_logk; /* largest |log k_t| over valid rows (NaN ignored; 0 if none)      */
+  double  trunc_excess; /* sum over valid rows of (k_t - w_t) in double, fixed order        */
+  int64_t reserved;
 } cis_stats_t;
 
-/* Bytes of device workspace cis_loss_fwd/_bwd need for T rows (T >= 0). The workspace holds
- * the cis_stats_t, the per-row loss terms and per-row status flags; its previous contents
- * do not matter. Returns 0 for T < 0. */
+/* Bytes of device workspace cis_loss_fwd/_bwd and cis_weights_ex (without sequence
+ * operators) need for T rows (T >= 0). The workspace holds the cis_stats_t and per-row
+ * scratch (loss terms, flags, diagnostics); its previous contents do not matter. Returns 0
+ * for T < 0. */
 size_t cis_workspace_bytes(int64_t T);
+
+/* Workspace for the _ex entry points with n_seq responses (n_seq >= 0; pass 0 for token-level
+ * operators). Returns 0 for T < 0 or n_seq < 0. */
+size_t cis_workspace_bytes_ex(int64_t T, int64_t n_seq);
 
 /* Static, human-readable text for a status code. */
 const char* cis_status_string(int status);
@@ -152,6 +162,123 @@ int cis_loss_bwd(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld
                  float* logp_train_out, float* w_out, uint8_t* trunc_out,
                  float* loss_terms_out, float* loss_out,
                  void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* =========================================================================================
+ * The operator family and the decoupled PPO-clip path.
+ *
+ * The weight on the token loss (App. C.1 "Operators", Table tab:baselines), from the
+ * training-side log-probability l_p (probability p) and the inference-side one l_q (q), with
+ * k = exp(l_p - l_q). Defaults in parentheses are the paper's hyperparameters.
+ *
+ *   CIS_OP_CIS        min{k, 1 + lambda*max(1 - p, kappa)}            (Algorithm 1; 2.3, 5e-3)
+ *   CIS_OP_NONE       1
+ *   CIS_OP_EXACT      k clamped to [lo, hi]                            ([1e-6, 1e6])
+ *   CIS_OP_TIS        min(k, hi)                                       (C = hi = 2)
+ *   CIS_OP_ICEPOP     k if lo <= k <= hi, else 0                       ([0.5, 5])
+ *   CIS_OP_KPOP       k if max(KL_B(p||q), KL_B(q||p)) <= hi, else 0; the Bernoulli KL in
+ *                     float64 with p, q clamped to [1e-8, 1 - 1e-8]     (App. D.5; phi = hi = 2)
+ *   CIS_OP_TWO_SIDED  max{CIS weight, (1 + p)/2}: the displacement also lifted to e^eps >= 1/2
+ *   CIS_OP_QFIXED     min{k, 1/(q + (1 - q)/(1 + lambda))}: a displacement bound
+ *                     eps <= log(1 + lambda) mapped to a ratio cap with q held fixed
+ *   CIS_OP_SEQ_TIS    min(K, hi) on every token of a response, K = prod of its tokens' k (C = 2)
+ *   CIS_OP_SEQ_MIS    K if lo <= K <= hi else 0 on every token of a response ([0.5, 2])
+ *
+ * Band and clamp edges are inclusive; caps are strict (a token at k = C is not truncated).
+ * A token is "acted on" when the operator changed its weight (truncated, masked, clamped or
+ * lifted); for the sequence operators, every valid token of an acted-on response. The
+ * sequence operators need every token's k before any gradient, so they take l_p from
+ * logp_old (the decoupled path) or from cis_weights_ex's logp_p.
+ * ========================================================================================= */
+typedef enum {
+  CIS_OP_CIS = 0,
+  CIS_OP_NONE = 1,
+  CIS_OP_EXACT = 2,
+  CIS_OP_TIS = 3,
+  CIS_OP_ICEPOP = 4,
+  CIS_OP_KPOP = 5,
+  CIS_OP_TWO_SIDED = 6,
+  CIS_OP_QFIXED = 7,
+  CIS_OP_SEQ_TIS = 8,
+  CIS_OP_SEQ_MIS = 9
+} cis_op_t;
+
+/* Operator and loss parameters (a host struct, read during the call). */
+typedef struct cis_params {
+  int32_t op;           /* cis_op_t                                                          */
+  float lambda;         /* CIS, two-sided, q-fixed: >= 0, finite                             */
+  float kappa;          /* CIS, two-sided: in [0, 1]                                         */
+  float lo, hi;         /* EXACT clamp, ICEPOP / SEQ_MIS band (0 <= lo <= hi); TIS / SEQ_TIS */
+                        /* cap and KPOP bound (hi >= 0); hi may be +inf                      */
+  float clip_low;       /* decoupled path: the update ratio is clipped to                    */
+  float clip_high;      /*   [1 - clip_low, 1 + clip_high]; 0 <= clip_low <= 1, clip_high >= 0 */
+  float scale;          /* loss normalisation (finite)                                       */
+} cis_params_t;
+
+/*
+ * cis_weights_ex — the operator family as one pass over recorded log-probabilities.
+ *
+ *   logp_p [T] float      training-side log-probability of each token (<= 0)
+ *   logp_q [T] float      inference-side log-probability recorded at sampling
+ *   mask   [T] uint8      nonzero = token counts; NULL = every token counts
+ *   seq_offsets [n_seq+1] int64   sequence operators only: response s is the token range
+ *                         [seq_offsets[s], seq_offsets[s+1]), rising from 0 to T (tokens
+ *                         outside every response get weight 0); NULL / 0 otherwise
+ *   params                operator and its bounds (clip_* and scale unused)
+ *   w_out     [T] float   weight (0 on masked tokens)
+ *   acted_out [T] uint8   1 where the operator acted; NULL = not written
+ *   eps_out   [T] float   log-odds displacement logit p - logit q (Sec. 3.1); +inf when only
+ *                         p = 1, -inf when only q = 1, log k when both are 1; NULL = not written
+ *   workspace             >= cis_workspace_bytes_ex(T, n_seq), 256-byte aligned; receives a
+ *                         cis_stats_t (n_valid, n_trunc, max_abs_logk, trunc_excess; loss 0)
+ * Here 1 - p is -expm1(logp_p). Errors: CIS_ERR_NULL, CIS_ERR_SHAPE (T < 0, n_seq < 0, or a
+ * sequence operator with n_seq < 1 while T > 0), CIS_ERR_PARAM, CIS_ERR_ALIGN,
+ * CIS_ERR_WORKSPACE, CIS_ERR_LAUNCH, CIS_ERR_DEVICE.
+ */
+int cis_weights_ex(const float* logp_p, const float* logp_q, const uint8_t* mask, int64_t T,
+                   const int64_t* seq_offsets, int64_t n_seq, const cis_params_t* params,
+                   float* w_out, uint8_t* acted_out, float* eps_out,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * cis_loss_fwd_ex / cis_loss_bwd_ex — the loss of cis_loss_fwd / cis_loss_bwd with any
+ * operator, and the decoupled PPO-clip objective of Eq. (1).
+ *
+ *   logp_old [T] float  NULL: the rate-1 path of cis_loss_fwd, with p from the same logits
+ *                       (complement mass), term = scale*w*A*l_train and gradient
+ *                       scale*w*A*(onehot - softmax); sequence operators are rejected.
+ *                       Non-NULL: the decoupled path (App. C.1). logp_old is the training
+ *                       log-probability at the rollout snapshot theta_old; the weight uses
+ *                       p = exp(logp_old) (1 - p = -expm1(logp_old)) and the update ratio is
+ *                       rho = exp(l_train - logp_old):
+ *                         term = scale * w * min(rho*A, clip(rho)*A),
+ *                         dL/dz = scale * w * A * rho * (onehot - softmax) where rho*A is the
+ *                                 smaller branch (A > 0: rho <= 1 + clip_high; A < 0:
+ *                                 rho >= 1 - clip_low; ties unclipped), 0 elsewhere.
+ *   seq_offsets, n_seq  as for cis_weights_ex (decoupled path only)
+ *   params              operator, bounds, PPO clip and scale
+ *   acted_out [T] uint8 1 where the operator acted (the trunc_out of cis_loss_fwd)
+ *   eps_out   [T] float per-token displacement as in cis_weights_ex; NULL = not written
+ *   workspace           >= cis_workspace_bytes_ex(T, n_seq)
+ *   other arguments, outputs and errors as for cis_loss_fwd / cis_loss_bwd, plus
+ *   CIS_ERR_PARAM for a sequence operator without logp_old.
+ * A row is non-finite when its log-sum-exp is not finite, its weight is NaN, or (decoupled)
+ * its update ratio is NaN.
+ */
+int cis_loss_fwd_ex(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
+                    const int64_t* ids, const float* logp_infer, const float* logp_old,
+                    const float* adv, const uint8_t* mask, const int64_t* seq_offsets,
+                    int64_t n_seq, const cis_params_t* params,
+                    float* logp_train_out, float* w_out, uint8_t* acted_out,
+                    float* loss_terms_out, float* eps_out, float* loss_out,
+                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+int cis_loss_bwd_ex(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
+                    const int64_t* ids, const float* logp_infer, const float* logp_old,
+                    const float* adv, const uint8_t* mask, const int64_t* seq_offsets,
+                    int64_t n_seq, const cis_params_t* params, void* dlogits, int64_t ld_g,
+                    float* logp_train_out, float* w_out, uint8_t* acted_out,
+                    float* loss_terms_out, float* eps_out, float* loss_out,
+                    void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

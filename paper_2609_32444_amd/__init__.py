@@ -11,18 +11,38 @@ from ._binding import (  # noqa: F401
     CIS_BF16,
     CIS_F32,
     LossCall,
+    OP_CIS,
+    OP_EXACT,
+    OP_ICEPOP,
+    OP_KPOP,
+    OP_NONE,
+    OP_QFIXED,
+    OP_SEQ_MIS,
+    OP_SEQ_TIS,
+    OP_TIS,
+    OP_TWO_SIDED,
+    Params,
+    SEQ_OPS,
     lambda_from_logodds,
     library_path,
     load_library,
     loss_bwd,
+    loss_bwd_ex,
     loss_fwd,
+    loss_fwd_ex,
+    params,
     read_stats,
     status_string,
     weights,
+    weights_ex,
     workspace_bytes,
+    workspace_bytes_ex,
 )
 
 __all__ = [
-    "CisError", "CIS_BF16", "CIS_F32", "LossCall", "lambda_from_logodds", "library_path", "load_library",
-    "loss_bwd", "loss_fwd", "read_stats", "status_string", "weights", "workspace_bytes",
+    "CisError", "CIS_BF16", "CIS_F32", "LossCall", "OP_CIS", "OP_EXACT", "OP_ICEPOP", "OP_KPOP",
+    "OP_NONE", "OP_QFIXED", "OP_SEQ_MIS", "OP_SEQ_TIS", "OP_TIS", "OP_TWO_SIDED", "Params",
+    "SEQ_OPS", "lambda_from_logodds", "library_path", "load_library", "loss_bwd", "loss_bwd_ex",
+    "loss_fwd", "loss_fwd_ex", "params", "read_stats", "status_string", "weights", "weights_ex",
+    "workspace_bytes", "workspace_bytes_ex",
 ]

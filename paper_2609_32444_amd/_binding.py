@@ -23,6 +23,27 @@ _int = ctypes.c_int
 _size = ctypes.c_size_t
 
 
+# Operators of the weight on the token loss (cis_op_t in include/cis.h).
+OP_CIS, OP_NONE, OP_EXACT, OP_TIS, OP_ICEPOP, OP_KPOP, OP_TWO_SIDED, OP_QFIXED, OP_SEQ_TIS, \
+    OP_SEQ_MIS = range(10)
+SEQ_OPS = (OP_SEQ_TIS, OP_SEQ_MIS)
+
+
+class Params(ctypes.Structure):
+    """cis_params_t: operator, its bounds, the PPO clip and the loss scale."""
+    _fields_ = [("op", ctypes.c_int32), ("lam", ctypes.c_float), ("kappa", ctypes.c_float),
+                ("lo", ctypes.c_float), ("hi", ctypes.c_float), ("clip_low", ctypes.c_float),
+                ("clip_high", ctypes.c_float), ("scale", ctypes.c_float)]
+
+
+def params(op: int = OP_CIS, *, lam: float = 2.3, kappa: float = 5e-3, lo: float = 0.0,
+           hi: float = math.inf, clip_low: float = 0.2, clip_high: float = 0.28,
+           scale: float = 1.0) -> Params:
+    """A cis_params_t; unused fields are ignored by the operator (see include/cis.h)."""
+    return Params(int(op), float(lam), float(kappa), float(lo), float(hi), float(clip_low),
+                  float(clip_high), float(scale))
+
+
 class CisError(RuntimeError):
     """A libcis call returned a nonzero status."""
 
@@ -56,6 +77,19 @@ def load_library() -> ctypes.CDLL:
     lib.cis_loss_bwd.argtypes = [_vp, _int, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _f32, _f32, _f32,
                                  _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _size, _vp]
     lib.cis_loss_bwd.restype = _int
+    lib.cis_workspace_bytes_ex.argtypes = [_i64, _i64]
+    lib.cis_workspace_bytes_ex.restype = _size
+    lib.cis_weights_ex.argtypes = [_vp, _vp, _vp, _i64, _vp, _i64, ctypes.POINTER(Params),
+                                   _vp, _vp, _vp, _vp, _size, _vp]
+    lib.cis_weights_ex.restype = _int
+    lib.cis_loss_fwd_ex.argtypes = [_vp, _int, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp,
+                                    _i64, ctypes.POINTER(Params), _vp, _vp, _vp, _vp, _vp, _vp,
+                                    _vp, _size, _vp]
+    lib.cis_loss_fwd_ex.restype = _int
+    lib.cis_loss_bwd_ex.argtypes = [_vp, _int, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _vp,
+                                    _i64, ctypes.POINTER(Params), _vp, _i64, _vp, _vp, _vp, _vp,
+                                    _vp, _vp, _vp, _size, _vp]
+    lib.cis_loss_bwd_ex.restype = _int
     _LIB = lib
     return lib
 
@@ -66,6 +100,10 @@ def status_string(status: int) -> str:
 
 def workspace_bytes(T: int) -> int:
     return int(load_library().cis_workspace_bytes(int(T)))
+
+
+def workspace_bytes_ex(T: int, n_seq: int = 0) -> int:
+    return int(load_library().cis_workspace_bytes_ex(int(T), int(n_seq)))
 
 
 def lambda_from_logodds(c: float) -> float:
@@ -266,12 +304,115 @@ def weights(logp_train, logp_infer, mask=None, *, lam, kappa=5e-3, w_out=None, t
     return w_out, trunc_out
 
 
-_STATS = struct.Struct("<d7q")
+_STATS = struct.Struct("<d4qddq")
 
 
 def read_stats(workspace: torch.Tensor) -> dict:
     """Copies the cis_stats_t at the start of a workspace to the host (synchronises)."""
     raw = bytes(workspace[:_STATS.size].cpu().numpy().tobytes())
-    loss, n_valid, n_bad_id, n_nonfinite, n_trunc, _, _, _ = _STATS.unpack(raw)
+    loss, n_valid, n_bad_id, n_nonfinite, n_trunc, max_abs_logk, excess, _ = _STATS.unpack(raw)
     return {"loss": loss, "n_valid": n_valid, "n_bad_id": n_bad_id, "n_nonfinite": n_nonfinite,
-            "n_trunc": n_trunc}
+            "n_trunc": n_trunc, "max_abs_logk": max_abs_logk, "trunc_excess": excess}
+
+
+def _offsets(seq_offsets, T, dev):
+    if seq_offsets is None:
+        return None, 0
+    if seq_offsets.device != dev or seq_offsets.dtype != torch.int64 or seq_offsets.dim() != 1 \
+            or not seq_offsets.is_contiguous() or seq_offsets.shape[0] < 2:
+        raise ValueError("seq_offsets must be a contiguous int64 [n_seq + 1] tensor on "
+                         f"{dev} (n_seq >= 1)")
+    return seq_offsets, seq_offsets.shape[0] - 1
+
+
+def _workspace(workspace, nbytes, dev):
+    if workspace is None:
+        return torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    if workspace.device != dev or workspace.numel() * workspace.element_size() < nbytes:
+        raise ValueError(f"workspace must hold {nbytes} bytes on {dev}")
+    return workspace
+
+
+def weights_ex(logp_p, logp_q, mask=None, *, params: Params, seq_offsets=None, workspace=None):
+    """The operator family on recorded log-probabilities (cis_weights_ex). Returns a dict with
+    "w", "acted", "eps" and "workspace" (its cis_stats_t holds the diagnostics)."""
+    dev = logp_p.device
+    T = logp_p.shape[0]
+    _check_vec("logp_p", logp_p, T, torch.float32, dev)
+    _check_vec("logp_q", logp_q, T, torch.float32, dev)
+    mask = _check_vec("mask", _mask_u8(mask), T, torch.uint8, dev, optional=True)
+    offs, n_seq = _offsets(seq_offsets, T, dev)
+    workspace = _workspace(workspace, workspace_bytes_ex(T, n_seq), dev)
+    out = {"w": torch.empty(T, dtype=torch.float32, device=dev),
+           "acted": torch.empty(T, dtype=torch.uint8, device=dev),
+           "eps": torch.empty(T, dtype=torch.float32, device=dev)}
+    with torch.cuda.device(dev):
+        rc = load_library().cis_weights_ex(
+            _ptr(logp_p), _ptr(logp_q), _ptr(mask), T, _ptr(offs), n_seq, ctypes.byref(params),
+            _ptr(out["w"]), _ptr(out["acted"]), _ptr(out["eps"]), _ptr(workspace),
+            workspace.numel() * workspace.element_size(), _stream(dev))
+    if rc != 0:
+        raise CisError("cis_weights_ex", rc)
+    out["workspace"] = workspace
+    return out
+
+
+_ALL_EX = ("logp_train", "w", "acted", "terms", "eps")
+
+
+def _loss_ex(bwd, logits, ids, logp_infer, adv, mask, prm, logp_old, seq_offsets, V, dlogits,
+             want, workspace):
+    dtype, T, V, ld = _logits_args(logits, V)
+    dev = logits.device
+    _check_vec("ids", ids, T, torch.int64, dev)
+    _check_vec("logp_infer", logp_infer, T, torch.float32, dev)
+    _check_vec("adv", adv, T, torch.float32, dev)
+    _check_vec("logp_old", logp_old, T, torch.float32, dev, optional=True)
+    mask = _check_vec("mask", _mask_u8(mask), T, torch.uint8, dev, optional=True)
+    offs, n_seq = _offsets(seq_offsets, T, dev)
+    workspace = _workspace(workspace, workspace_bytes_ex(T, n_seq), dev)
+    out = {}
+    for k in want:
+        out[k] = torch.empty(T, dtype=torch.uint8 if k == "acted" else torch.float32, device=dev)
+    out["loss"] = torch.empty(1, dtype=torch.float32, device=dev)
+    lib = load_library()
+    with torch.cuda.device(dev):
+        head = (_ptr(logits), dtype, T, V, ld, _ptr(ids), _ptr(logp_infer), _ptr(logp_old),
+                _ptr(adv), _ptr(mask), _ptr(offs), n_seq, ctypes.byref(prm))
+        tail = (_ptr(out.get("logp_train")), _ptr(out.get("w")), _ptr(out.get("acted")),
+                _ptr(out.get("terms")), _ptr(out.get("eps")), _ptr(out["loss"]),
+                _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(dev))
+        if bwd:
+            if dlogits is None:
+                dlogits = _new_grad(T, V, logits)
+            if dlogits.dtype != logits.dtype or dlogits.dim() != 2 or dlogits.stride(1) != 1 \
+                    or dlogits.shape[0] != T or dlogits.shape[1] < V or dlogits.device != dev:
+                raise ValueError("dlogits must be a [T, >=V] tensor like logits")
+            rc = lib.cis_loss_bwd_ex(*head, _ptr(dlogits), dlogits.stride(0), *tail)
+            fn = "cis_loss_bwd_ex"
+        else:
+            rc = lib.cis_loss_fwd_ex(*head, *tail)
+            fn = "cis_loss_fwd_ex"
+    if rc != 0:
+        raise CisError(fn, rc)
+    out["workspace"] = workspace
+    if bwd:
+        out["dlogits"] = dlogits
+    return out
+
+
+def loss_fwd_ex(logits, ids, logp_infer, adv, mask=None, *, params: Params, logp_old=None,
+                seq_offsets=None, V=None, want=_ALL_EX, workspace=None):
+    """Forward pass with any operator; with logp_old, the decoupled PPO-clip objective
+    (cis_loss_fwd_ex). Keys: the requested per-row outputs ("logp_train", "w", "acted",
+    "terms", "eps"), "loss" and "workspace"."""
+    return _loss_ex(False, logits, ids, logp_infer, adv, mask, params, logp_old, seq_offsets, V,
+                    None, want, workspace)
+
+
+def loss_bwd_ex(logits, ids, logp_infer, adv, mask=None, *, params: Params, logp_old=None,
+                seq_offsets=None, V=None, dlogits=None, want=_ALL_EX, workspace=None):
+    """Fused forward and backward pass with any operator (cis_loss_bwd_ex); like loss_fwd_ex
+    plus "dlogits"."""
+    return _loss_ex(True, logits, ids, logp_infer, adv, mask, params, logp_old, seq_offsets, V,
+                    dlogits, want, workspace)

@@ -74,31 +74,129 @@ int check_params(float lam, float kappa, float scale) {
   return CIS_OK;
 }
 
-int loss_common(bool bwd, const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
-                const int64_t* ids, const float* logp_infer, const float* adv,
-                const uint8_t* mask, float lam, float kappa, float scale, void* dlogits,
-                int64_t ld_g, float* logp_train_out, float* w_out, uint8_t* trunc_out,
-                float* loss_terms_out, float* loss_out, void* workspace, size_t workspace_bytes,
-                hipStream_t stream) {
-  if (dtype != CIS_BF16 && dtype != CIS_F32) return CIS_ERR_DTYPE;
-  if (T < 0 || V < 1 || ld < V || (bwd && ld_g < V)) return CIS_ERR_SHAPE;
-  const int esize = dtype == CIS_BF16 ? 2 : 4;
+bool is_seq_op(int op) { return op == CIS_OP_SEQ_TIS || op == CIS_OP_SEQ_MIS; }
+
+// Ranges of cis_params_t per operator (cis.h). `decoupled` also checks the PPO clip.
+int check_op_params(const cis_params_t* p, bool decoupled) {
+  if (!p) return CIS_ERR_NULL;
+  if (p->op < CIS_OP_CIS || p->op > CIS_OP_SEQ_MIS) return CIS_ERR_PARAM;
+  if (!isfinite(p->scale)) return CIS_ERR_PARAM;
+  switch (p->op) {
+    case CIS_OP_CIS:
+    case CIS_OP_TWO_SIDED:
+      if (int rc = check_params(p->lambda, p->kappa, p->scale)) return rc;
+      break;
+    case CIS_OP_QFIXED:
+      if (!(p->lambda >= 0.f) || !isfinite(p->lambda)) return CIS_ERR_PARAM;
+      break;
+    case CIS_OP_EXACT:
+    case CIS_OP_ICEPOP:
+    case CIS_OP_SEQ_MIS:
+      if (!(p->lo >= 0.f && p->lo <= p->hi)) return CIS_ERR_PARAM;
+      break;
+    case CIS_OP_TIS:
+    case CIS_OP_KPOP:
+    case CIS_OP_SEQ_TIS:
+      if (!(p->hi >= 0.f)) return CIS_ERR_PARAM;
+      break;
+    default:
+      break;
+  }
+  if (decoupled) {
+    if (!(p->clip_low >= 0.f && p->clip_low <= 1.f)) return CIS_ERR_PARAM;
+    if (!(p->clip_high >= 0.f) || !isfinite(p->clip_high)) return CIS_ERR_PARAM;
+  }
+  return CIS_OK;
+}
+
+cis::OpArgs op_args(const cis_params_t& p) {
+  return cis::OpArgs{p.op, p.lambda, p.kappa, p.lo, p.hi};
+}
+
+struct Ws {
+  char* base;
+  cis::WsLayout L;
+  float* f(size_t off) const { return reinterpret_cast<float*>(base + off); }
+  uint8_t* b(size_t off) const { return reinterpret_cast<uint8_t*>(base + off); }
+  cis_stats_t* stats() const { return reinterpret_cast<cis_stats_t*>(base); }
+};
+
+int launch_grid_stride(const void* fn, int64_t T, int block, const DeviceInfo& info, void* arg,
+                       hipStream_t stream) {
+  const int64_t need = (T + block - 1) / block;
+  const int64_t cap = (int64_t)info.num_cu * 8;
+  return launch(fn, (int)(need < cap ? need : cap), block, arg, stream);
+}
+
+// Sequence operators: per-response log K into the workspace.
+int launch_seq_sum(const float* lp, const float* lq, const uint8_t* mask, const int64_t* ids,
+                   int64_t V, const int64_t* offsets, int64_t n_seq, int64_t T, const Ws& ws,
+                   hipStream_t stream) {
+  cis::SeqSumArgs sa{lp, lq, mask, ids, offsets, reinterpret_cast<double*>(ws.base + ws.L.logK),
+                     T, n_seq, (int32_t)V};
+  const int64_t per = cis::kSeqBlock / 64;
+  return launch(cis::seq_sum_kernel(), (int)((n_seq + per - 1) / per), cis::kSeqBlock, &sa,
+                stream);
+}
+
+// Everything the loss entry points share. `ext` selects the extended kernels (operator
+// family / decoupled path); the base entry points pass the CIS operator with ext = false.
+struct LossCall {
+  bool bwd, ext;
+  const void* logits;
+  int dtype;
+  int64_t T, V, ld;
+  const int64_t* ids;
+  const float* logp_infer;
+  const float* logp_old;
+  const float* adv;
+  const uint8_t* mask;
+  const int64_t* offsets;
+  int64_t n_seq;
+  cis_params_t prm;
+  void* dlogits;
+  int64_t ld_g;
+  float *logp_train_out, *w_out;
+  uint8_t* acted_out;
+  float *terms_out, *eps_out, *loss_out;
+  void* workspace;
+  size_t workspace_bytes;
+};
+
+int run_loss(const LossCall& c, hipStream_t stream) {
+  const bool bwd = c.bwd;
+  const int64_t T = c.T, V = c.V;
+  if (c.dtype != CIS_BF16 && c.dtype != CIS_F32) return CIS_ERR_DTYPE;
+  if (T < 0 || V < 1 || c.ld < V || (bwd && c.ld_g < V) || c.n_seq < 0) return CIS_ERR_SHAPE;
+  const int esize = c.dtype == CIS_BF16 ? 2 : 4;
   const int epv = 16 / esize;
   if (V > kMaxV) return CIS_ERR_SHAPE;  // row byte offsets stay within 32 bits
-  if (ld > INT64_MAX / esize || (bwd && ld_g > INT64_MAX / esize)) return CIS_ERR_SHAPE;
-  if (int rc = check_params(lam, kappa, scale)) return rc;
-  if (!workspace) return CIS_ERR_NULL;
-  if (T > 0 && (!logits || !ids || !logp_infer || !adv || (bwd && !dlogits))) return CIS_ERR_NULL;
-  if (!aligned(workspace, 256)) return CIS_ERR_ALIGN;
-  if (workspace_bytes < cis::ws_bytes(T)) return CIS_ERR_WORKSPACE;
+  if (c.ld > INT64_MAX / esize || (bwd && c.ld_g > INT64_MAX / esize)) return CIS_ERR_SHAPE;
+  const bool decoupled = c.logp_old != nullptr;
+  if (c.ext) {
+    if (int rc = check_op_params(&c.prm, decoupled)) return rc;
+    if (is_seq_op(c.prm.op) && !decoupled) return CIS_ERR_PARAM;
+    if (is_seq_op(c.prm.op) && T > 0 && c.n_seq < 1) return CIS_ERR_SHAPE;
+  } else if (int rc = check_params(c.prm.lambda, c.prm.kappa, c.prm.scale)) {
+    return rc;
+  }
+  const bool seq = c.ext && is_seq_op(c.prm.op);
+  const int64_t n_seq = seq ? c.n_seq : 0;
+  if (!c.workspace) return CIS_ERR_NULL;
+  if (T > 0 && (!c.logits || !c.ids || !c.logp_infer || !c.adv || (bwd && !c.dlogits)))
+    return CIS_ERR_NULL;
+  if (seq && T > 0 && !c.offsets) return CIS_ERR_NULL;
+  if (!aligned(c.workspace, 256)) return CIS_ERR_ALIGN;
+  const cis::WsLayout L = cis::ws_layout(T, n_seq);
+  if (c.workspace_bytes < L.total) return CIS_ERR_WORKSPACE;
   if (T > 0) {
-    if (!aligned(logits, 16) || (ld * esize) % 16 != 0) return CIS_ERR_ALIGN;
+    if (!aligned(c.logits, 16) || (c.ld * esize) % 16 != 0) return CIS_ERR_ALIGN;
     if (bwd) {
-      if (!aligned(dlogits, 16) || (ld_g * esize) % 16 != 0) return CIS_ERR_ALIGN;
-      const uintptr_t a0 = (uintptr_t)logits, a1 = a0 + (uintptr_t)(T * ld * esize);
-      const uintptr_t b0 = (uintptr_t)dlogits, b1 = b0 + (uintptr_t)(T * ld_g * esize);
+      if (!aligned(c.dlogits, 16) || (c.ld_g * esize) % 16 != 0) return CIS_ERR_ALIGN;
+      const uintptr_t a0 = (uintptr_t)c.logits, a1 = a0 + (uintptr_t)(T * c.ld * esize);
+      const uintptr_t b0 = (uintptr_t)c.dlogits, b1 = b0 + (uintptr_t)(T * c.ld_g * esize);
       if (a0 == b0) {
-        if (ld_g != ld) return CIS_ERR_ALIAS;
+        if (c.ld_g != c.ld) return CIS_ERR_ALIAS;
       } else if (a0 < b1 && b0 < a1) {
         return CIS_ERR_ALIAS;
       }
@@ -108,41 +206,127 @@ int loss_common(bool bwd, const void* logits, int dtype, int64_t T, int64_t V, i
   const int dev = current_device(&info);
   if (dev < 0) return dev;
 
-  char* ws = static_cast<char*>(workspace);
-  float* terms_ws = reinterpret_cast<float*>(ws + cis::ws_terms_offset());
-  uint8_t* flags_ws = reinterpret_cast<uint8_t*>(ws + cis::ws_flags_offset(T));
-
+  const Ws ws{static_cast<char*>(c.workspace), L};
   if (T > 0) {
+    if (decoupled) {
+      // the weight depends only on (l_old, l_infer): one pass before the rows
+      if (seq) {
+        if (int rc = launch_seq_sum(c.logp_old, c.logp_infer, c.mask, c.ids, V, c.offsets, n_seq,
+                                    T, ws, stream))
+          return rc;
+      }
+      cis::PrepassArgs pa{};
+      pa.logp_p = c.logp_old;
+      pa.logp_q = c.logp_infer;
+      pa.mask = c.mask;
+      pa.ids = c.ids;
+      pa.offsets = c.offsets;
+      pa.logK = reinterpret_cast<const double*>(ws.base + L.logK);
+      pa.ops = op_args(c.prm);
+      pa.T = T;
+      pa.n_seq = n_seq;
+      pa.V = (int32_t)V;
+      pa.w_out = c.w_out;
+      pa.acted_out = c.acted_out;
+      pa.eps_out = c.eps_out;
+      pa.wpre_ws = ws.f(L.wpre);
+      pa.pflags_ws = ws.b(L.pflags);
+      pa.logk_ws = ws.f(L.logk);
+      pa.excess_ws = ws.f(L.excess);
+      if (int rc = launch_grid_stride(cis::prepass_kernel(), T, cis::kWeightsBlock, info, &pa,
+                                      stream))
+        return rc;
+    }
     const int32_t nvec = (int32_t)((V + epv - 1) / epv);
-    const cis::RowVariant& var = cis::select_row_variant(dtype, bwd, nvec);
-    cis::RowArgs ra;
-    ra.logits = logits;
-    ra.dlogits = dlogits;
-    ra.row_bytes = ld * esize;
-    ra.grow_bytes = bwd ? ld_g * esize : 0;
-    ra.ids = ids;
-    ra.logp_infer = logp_infer;
-    ra.adv = adv;
-    ra.mask = mask;
-    ra.logp_train_out = logp_train_out;
-    ra.w_out = w_out;
-    ra.trunc_out = trunc_out;
-    ra.terms_user = loss_terms_out;
-    ra.terms_ws = terms_ws;
-    ra.flags_ws = flags_ws;
+    const cis::RowVariant& var = c.ext ? cis::select_row_variant_ext(c.dtype, bwd, nvec)
+                                       : cis::select_row_variant(c.dtype, bwd, nvec);
+    cis::RowArgs ra{};
+    ra.logits = c.logits;
+    ra.dlogits = c.dlogits;
+    ra.row_bytes = c.ld * esize;
+    ra.grow_bytes = bwd ? c.ld_g * esize : 0;
+    ra.ids = c.ids;
+    ra.logp_infer = c.logp_infer;
+    ra.adv = c.adv;
+    ra.mask = c.mask;
+    ra.logp_train_out = c.logp_train_out;
+    ra.w_out = c.w_out;
+    ra.trunc_out = c.acted_out;
+    ra.terms_user = c.terms_out;
+    ra.terms_ws = ws.f(L.terms);
+    ra.flags_ws = ws.b(L.flags);
+    ra.logk_ws = ws.f(L.logk);
+    ra.excess_ws = ws.f(L.excess);
     ra.T = T;
     ra.V = (int32_t)V;
     ra.nvec = nvec;
-    ra.lam = lam;
-    ra.kappa = kappa;
-    ra.scale = scale;
+    ra.lam = c.prm.lambda;
+    ra.kappa = c.prm.kappa;
+    ra.scale = c.prm.scale;
+    ra.ops = op_args(c.prm);
+    ra.logp_old = c.logp_old;
+    ra.wpre_ws = ws.f(L.wpre);
+    ra.pflags_ws = ws.b(L.pflags);
+    ra.eps_out = c.eps_out;
+    ra.clip_low = c.prm.clip_low;
+    ra.clip_high = c.prm.clip_high;
     const int per_cu = blocks_per_cu(var.fn, var.block, dev);
     const int64_t resident = (int64_t)per_cu * info.num_cu;
     const int grid = (int)(T < resident ? T : resident);
     if (int rc = launch(var.fn, grid, var.block, &ra, stream)) return rc;
   }
-  cis::FinalizeArgs fa{terms_ws, flags_ws, T, reinterpret_cast<cis_stats_t*>(ws), loss_out};
+  cis::FinalizeArgs fa{ws.f(L.terms), ws.b(L.flags), ws.f(L.logk), ws.f(L.excess), T,
+                       ws.stats(), c.loss_out};
   return launch(cis::finalize_kernel(), 1, cis::kFinalizeBlock, &fa, stream);
+}
+
+LossCall base_call(bool bwd, const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
+                   const int64_t* ids, const float* logp_infer, const float* adv,
+                   const uint8_t* mask, float lam, float kappa, float scale, void* dlogits,
+                   int64_t ld_g, float* logp_train_out, float* w_out, uint8_t* trunc_out,
+                   float* loss_terms_out, float* loss_out, void* workspace,
+                   size_t workspace_bytes) {
+  LossCall c{};
+  c.bwd = bwd;
+  c.ext = false;
+  c.logits = logits;
+  c.dtype = dtype;
+  c.T = T;
+  c.V = V;
+  c.ld = ld;
+  c.ids = ids;
+  c.logp_infer = logp_infer;
+  c.adv = adv;
+  c.mask = mask;
+  c.prm = cis_params_t{CIS_OP_CIS, lam, kappa, 0.f, 0.f, 0.f, 0.f, scale};
+  c.dlogits = dlogits;
+  c.ld_g = ld_g;
+  c.logp_train_out = logp_train_out;
+  c.w_out = w_out;
+  c.acted_out = trunc_out;
+  c.terms_out = loss_terms_out;
+  c.loss_out = loss_out;
+  c.workspace = workspace;
+  c.workspace_bytes = workspace_bytes;
+  return c;
+}
+
+LossCall ext_call(bool bwd, const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
+                  const int64_t* ids, const float* logp_infer, const float* logp_old,
+                  const float* adv, const uint8_t* mask, const int64_t* offsets, int64_t n_seq,
+                  const cis_params_t* params, void* dlogits, int64_t ld_g,
+                  float* logp_train_out, float* w_out, uint8_t* acted_out, float* terms_out,
+                  float* eps_out, float* loss_out, void* workspace, size_t workspace_bytes) {
+  LossCall c = base_call(bwd, logits, dtype, T, V, ld, ids, logp_infer, adv, mask, 0.f, 0.f,
+                         0.f, dlogits, ld_g, logp_train_out, w_out, acted_out, terms_out,
+                         loss_out, workspace, workspace_bytes);
+  c.ext = true;
+  c.logp_old = logp_old;
+  c.offsets = offsets;
+  c.n_seq = n_seq;
+  c.eps_out = eps_out;
+  if (params) c.prm = *params;
+  return c;
 }
 
 }  // namespace
@@ -151,14 +335,22 @@ extern "C" {
 
 size_t cis_workspace_bytes(int64_t T) { return T < 0 ? 0 : cis::ws_bytes(T); }
 
+size_t cis_workspace_bytes_ex(int64_t T, int64_t n_seq) {
+  return (T < 0 || n_seq < 0) ? 0 : cis::ws_layout(T, n_seq).total;
+}
+
 const char* cis_status_string(int status) {
   switch (status) {
     case CIS_OK: return "ok";
     case CIS_ERR_NULL: return "a required pointer is NULL";
-    case CIS_ERR_SHAPE: return "invalid shape (T < 0, V outside [1, 2^28], or a row stride < V)";
+    case CIS_ERR_SHAPE:
+      return "invalid shape (T < 0, V outside [1, 2^28], a row stride < V, n_seq < 0, or a "
+             "sequence operator without responses)";
     case CIS_ERR_DTYPE: return "unknown dtype";
     case CIS_ERR_PARAM:
-      return "invalid parameter (lambda must be finite and >= 0, kappa in [0,1], scale finite)";
+      return "invalid parameter (lambda must be finite and >= 0, kappa in [0,1], scale finite; "
+             "operator known, its bounds in range, PPO clip in range; sequence operators need "
+             "logp_old)";
     case CIS_ERR_ALIGN:
       return "misaligned buffer (logits/dlogits base and row stride must be 16-byte multiples; "
              "workspace 256-byte aligned)";
@@ -181,10 +373,56 @@ int cis_weights(const float* logp_train, const float* logp_infer, const uint8_t*
   const int dev = current_device(&info);
   if (dev < 0) return dev;
   cis::WeightsArgs wa{logp_train, logp_infer, mask, w_out, trunc_out, T, lambda, kappa};
-  const int64_t need = (T + cis::kWeightsBlock - 1) / cis::kWeightsBlock;
-  const int64_t cap = (int64_t)info.num_cu * 8;
-  return launch(cis::weights_kernel(), (int)(need < cap ? need : cap), cis::kWeightsBlock, &wa,
-                stream);
+  return launch_grid_stride(cis::weights_kernel(), T, cis::kWeightsBlock, info, &wa, stream);
+}
+
+int cis_weights_ex(const float* logp_p, const float* logp_q, const uint8_t* mask, int64_t T,
+                   const int64_t* seq_offsets, int64_t n_seq, const cis_params_t* params,
+                   float* w_out, uint8_t* acted_out, float* eps_out, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream) {
+  if (T < 0 || n_seq < 0) return CIS_ERR_SHAPE;
+  if (int rc = check_op_params(params, false)) return rc;
+  const bool seq = is_seq_op(params->op);
+  if (seq && T > 0 && n_seq < 1) return CIS_ERR_SHAPE;
+  if (!workspace) return CIS_ERR_NULL;
+  if (T > 0 && (!logp_p || !logp_q || !w_out || (seq && !seq_offsets))) return CIS_ERR_NULL;
+  if (!aligned(workspace, 256)) return CIS_ERR_ALIGN;
+  const cis::WsLayout L = cis::ws_layout(T, seq ? n_seq : 0);
+  if (workspace_bytes < L.total) return CIS_ERR_WORKSPACE;
+  DeviceInfo info;
+  const int dev = current_device(&info);
+  if (dev < 0) return dev;
+  const Ws ws{static_cast<char*>(workspace), L};
+  if (T > 0) {
+    if (seq) {
+      if (int rc = launch_seq_sum(logp_p, logp_q, mask, nullptr, 1, seq_offsets, n_seq, T, ws,
+                                  stream))
+        return rc;
+    }
+    cis::PrepassArgs pa{};
+    pa.logp_p = logp_p;
+    pa.logp_q = logp_q;
+    pa.mask = mask;
+    pa.offsets = seq_offsets;
+    pa.logK = reinterpret_cast<const double*>(ws.base + L.logK);
+    pa.ops = op_args(*params);
+    pa.T = T;
+    pa.n_seq = seq ? n_seq : 0;
+    pa.V = 1;
+    pa.w_out = w_out;
+    pa.acted_out = acted_out;
+    pa.eps_out = eps_out;
+    pa.logk_ws = ws.f(L.logk);
+    pa.excess_ws = ws.f(L.excess);
+    pa.flags_ws = ws.b(L.flags);
+    pa.terms_ws = ws.f(L.terms);
+    if (int rc = launch_grid_stride(cis::prepass_kernel(), T, cis::kWeightsBlock, info, &pa,
+                                    stream))
+      return rc;
+  }
+  cis::FinalizeArgs fa{ws.f(L.terms), ws.b(L.flags), ws.f(L.logk), ws.f(L.excess), T,
+                       ws.stats(), nullptr};
+  return launch(cis::finalize_kernel(), 1, cis::kFinalizeBlock, &fa, stream);
 }
 
 int cis_loss_fwd(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
@@ -193,9 +431,10 @@ int cis_loss_fwd(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld
                  float* logp_train_out, float* w_out, uint8_t* trunc_out,
                  float* loss_terms_out, float* loss_out, void* workspace,
                  size_t workspace_bytes, hipStream_t stream) {
-  return loss_common(false, logits, dtype, T, V, ld, ids, logp_infer, adv, mask, lambda, kappa,
-                     scale, nullptr, 0, logp_train_out, w_out, trunc_out, loss_terms_out,
-                     loss_out, workspace, workspace_bytes, stream);
+  return run_loss(base_call(false, logits, dtype, T, V, ld, ids, logp_infer, adv, mask, lambda,
+                            kappa, scale, nullptr, 0, logp_train_out, w_out, trunc_out,
+                            loss_terms_out, loss_out, workspace, workspace_bytes),
+                  stream);
 }
 
 int cis_loss_bwd(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
@@ -204,9 +443,40 @@ int cis_loss_bwd(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld
                  int64_t ld_g, float* logp_train_out, float* w_out, uint8_t* trunc_out,
                  float* loss_terms_out, float* loss_out, void* workspace,
                  size_t workspace_bytes, hipStream_t stream) {
-  return loss_common(true, logits, dtype, T, V, ld, ids, logp_infer, adv, mask, lambda, kappa,
-                     scale, dlogits, ld_g, logp_train_out, w_out, trunc_out, loss_terms_out,
-                     loss_out, workspace, workspace_bytes, stream);
+  return run_loss(base_call(true, logits, dtype, T, V, ld, ids, logp_infer, adv, mask, lambda,
+                            kappa, scale, dlogits, ld_g, logp_train_out, w_out, trunc_out,
+                            loss_terms_out, loss_out, workspace, workspace_bytes),
+                  stream);
+}
+
+int cis_loss_fwd_ex(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
+                    const int64_t* ids, const float* logp_infer, const float* logp_old,
+                    const float* adv, const uint8_t* mask, const int64_t* seq_offsets,
+                    int64_t n_seq, const cis_params_t* params, float* logp_train_out,
+                    float* w_out, uint8_t* acted_out, float* loss_terms_out, float* eps_out,
+                    float* loss_out, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
+  if (!params) return CIS_ERR_NULL;
+  return run_loss(ext_call(false, logits, dtype, T, V, ld, ids, logp_infer, logp_old, adv, mask,
+                           seq_offsets, n_seq, params, nullptr, 0, logp_train_out, w_out,
+                           acted_out, loss_terms_out, eps_out, loss_out, workspace,
+                           workspace_bytes),
+                  stream);
+}
+
+int cis_loss_bwd_ex(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
+                    const int64_t* ids, const float* logp_infer, const float* logp_old,
+                    const float* adv, const uint8_t* mask, const int64_t* seq_offsets,
+                    int64_t n_seq, const cis_params_t* params, void* dlogits, int64_t ld_g,
+                    float* logp_train_out, float* w_out, uint8_t* acted_out,
+                    float* loss_terms_out, float* eps_out, float* loss_out, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
+  if (!params) return CIS_ERR_NULL;
+  return run_loss(ext_call(true, logits, dtype, T, V, ld, ids, logp_infer, logp_old, adv, mask,
+                           seq_offsets, n_seq, params, dlogits, ld_g, logp_train_out, w_out,
+                           acted_out, loss_terms_out, eps_out, loss_out, workspace,
+                           workspace_bytes),
+                  stream);
 }
 
 }  // extern "C"

@@ -1,5 +1,5 @@
 // Internal interface between the C-ABI entry points (cis_api.cpp) and the HIP kernels
-// (cis_kernels.hip). Not installed; not part of the public ABI.
+// (cis_kernels.hip, cis_kernels_ext.hip). Not installed; not part of the public ABI.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -9,15 +9,43 @@
 
 namespace cis {
 
-// Workspace layout (bytes): [0, 256) cis_stats_t; then float terms[T]; then uint8 flags[T].
+// Workspace layout (bytes), every array 256-byte aligned:
+//   [0, 256)  cis_stats_t
+//   terms  float[T]   per-row loss term
+//   logk   float[T]   per-row log k (diagnostics)
+//   excess float[T]   per-row k - w (diagnostics)
+//   wpre   float[T]   weight from the pre-pass (decoupled path)
+//   flags  uint8[T]   per-row status bits (kFlag*)
+//   pflags uint8[T]   pre-pass bits (kFlagTrunc = acted on)
+//   logK   double[n_seq]  per-response log K (sequence operators)
 constexpr size_t kStatsBytes = 256;
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
-inline size_t ws_terms_offset() { return kStatsBytes; }
-inline size_t ws_flags_offset(int64_t T) { return align_up(kStatsBytes + 4 * (size_t)T, 256); }
-inline size_t ws_bytes(int64_t T) { return align_up(ws_flags_offset(T) + (size_t)T, 256); }
+struct WsLayout {
+  size_t terms, logk, excess, wpre, flags, pflags, logK, total;
+};
+inline WsLayout ws_layout(int64_t T, int64_t n_seq) {
+  const size_t f = align_up(4 * (size_t)T, 256), b = align_up((size_t)T, 256);
+  WsLayout L;
+  L.terms = kStatsBytes;
+  L.logk = L.terms + f;
+  L.excess = L.logk + f;
+  L.wpre = L.excess + f;
+  L.flags = L.wpre + f;
+  L.pflags = L.flags + b;
+  L.logK = L.pflags + b;
+  L.total = L.logK + align_up(8 * (size_t)n_seq, 256);
+  return L;
+}
+inline size_t ws_bytes(int64_t T) { return ws_layout(T, 0).total; }
 
-// Per-row status bits (workspace flags[T]).
+// Per-row status bits (workspace flags[T]; kFlagTrunc = the operator acted on the row).
 enum : uint8_t { kFlagValid = 1, kFlagBadId = 2, kFlagNonFinite = 4, kFlagTrunc = 8 };
+
+// Operator parameters as the kernels see them (cis_params_t minus the loss fields).
+struct OpArgs {
+  int32_t op;
+  float lam, kappa, lo, hi;
+};
 
 // Arguments of the row kernels, passed by value.
 struct RowArgs {
@@ -35,15 +63,26 @@ struct RowArgs {
   float* terms_user;        // nullable
   float* terms_ws;          // workspace terms[T]
   uint8_t* flags_ws;        // workspace flags[T]
+  float* logk_ws;           // workspace logk[T]
+  float* excess_ws;         // workspace excess[T]
   int64_t T;
   int32_t V;
   int32_t nvec;             // ceil(V / elements per 16-byte vector)
   float lam, kappa, scale;
+  // extended kernels only
+  OpArgs ops;               // rate-1 path: the operator applied in the epilogue
+  const float* logp_old;    // non-null: decoupled path (weight from the pre-pass)
+  const float* wpre_ws;     // pre-pass weight[T]
+  const uint8_t* pflags_ws; // pre-pass acted bits[T]
+  float* eps_out;           // nullable; rate-1 path only (the pre-pass writes it otherwise)
+  float clip_low, clip_high;
 };
 
 struct FinalizeArgs {
   const float* terms_ws;
   const uint8_t* flags_ws;
+  const float* logk_ws;
+  const float* excess_ws;
   int64_t T;
   cis_stats_t* stats;
   float* loss_out;          // nullable
@@ -59,6 +98,41 @@ struct WeightsArgs {
   float lam, kappa;
 };
 
+// Per-response sum of log k over valid tokens (sequence operators).
+struct SeqSumArgs {
+  const float* logp_p;
+  const float* logp_q;
+  const uint8_t* mask;      // nullable
+  const int64_t* ids;       // nullable (weights path: validity is the mask alone)
+  const int64_t* offsets;   // [n_seq + 1]
+  double* logK;             // [n_seq]
+  int64_t T, n_seq;
+  int32_t V;
+};
+
+// Per-token weights of an operator from recorded log-probabilities: the decoupled path's
+// pre-pass and cis_weights_ex.
+struct PrepassArgs {
+  const float* logp_p;
+  const float* logp_q;
+  const uint8_t* mask;      // nullable
+  const int64_t* ids;       // nullable
+  const int64_t* offsets;   // sequence operators
+  const double* logK;       // sequence operators
+  OpArgs ops;
+  int64_t T, n_seq;
+  int32_t V;
+  float* w_out;             // nullable
+  uint8_t* acted_out;       // nullable
+  float* eps_out;           // nullable
+  float* wpre_ws;           // nullable (loss path)
+  uint8_t* pflags_ws;       // nullable (loss path)
+  float* logk_ws;
+  float* excess_ws;
+  uint8_t* flags_ws;        // nullable: weights path writes valid/acted bits here
+  float* terms_ws;          // nullable: weights path writes zeros here
+};
+
 // A compiled row-kernel variant: BLOCK threads per workgroup, NV register-resident 16-byte
 // vectors per thread.
 struct RowVariant {
@@ -68,12 +142,17 @@ struct RowVariant {
   const void* fn;           // __global__ function (for hipLaunchKernel / occupancy queries)
 };
 
-// Picks the variant for `nvec` 16-byte vectors per row; dtype is CIS_BF16 or CIS_F32.
+// Picks the variant for `nvec` 16-byte vectors per row; dtype is CIS_BF16 or CIS_F32. The
+// extended variants carry the operator family and the decoupled path in their epilogue.
 const RowVariant& select_row_variant(int dtype, bool bwd, int32_t nvec);
+const RowVariant& select_row_variant_ext(int dtype, bool bwd, int32_t nvec);
 
 const void* finalize_kernel();
 const void* weights_kernel();
+const void* seq_sum_kernel();
+const void* prepass_kernel();
 constexpr int kFinalizeBlock = 1024;
 constexpr int kWeightsBlock = 256;
+constexpr int kSeqBlock = 256;      // four responses per workgroup, one per wave
 
 }  // namespace cis

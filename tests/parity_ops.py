@@ -1,0 +1,229 @@
+"""Parity helpers for the operator family, the decoupled PPO-clip path and the diagnostics:
+run oracle.ops on the same inputs as the HIP path (process pool) and compare.
+
+Tolerances are those of tests/parity.py, plus, for decisions taken in floating point:
+
+* weights and terms: the tolerances of tests/parity.py plus 2^-126 (a sequence weight below
+  float32's normal range, e.g. K = e^-146 over a long response, may flush to zero).
+* acted-on flags: bit-exact except tokens whose oracle decision variable lies within a margin
+  of the operator's boundary (log k vs log C / log(1 + lambda*phi) / the band edges: 1e-5;
+  KPop's metric vs phi: 1e-4; sequence operators' log K: 1e-9). There either flag is correct;
+  for the masking operators the weight, term and gradient of such a token follow the flag, so
+  those rows leave the value comparisons and their terms widen the loss bound.
+* PPO gate (decoupled path): rows with |rho - bound| <= 1e-5 * bound leave the gradient
+  comparison (the gradient switches on or off there; the term is continuous).
+* displacement eps: |gpu - ref| <= 1e-4 |ref| + 1e-5, infinities exact.
+* diagnostics: acted count within the margin rows; max |log k| to 1e-5 relative (+2e-6);
+  truncated excess to 1e-4 of sum |k - w| plus the margin rows' k.
+"""
+
+from __future__ import annotations
+
+import math
+import multiprocessing as mp
+
+import numpy as np
+import torch
+
+from oracle import cis as O
+from oracle import ops as X
+from tests import parity as P
+
+_SHARED = {}
+
+
+def margin_tol(op: int) -> float:
+    """Width of the band around an operator's boundary where either acted flag is correct."""
+    return 1e-4 if op == X.OP_KPOP else (1e-9 if op in X.SEQ_OPS else 1e-5)
+
+
+def op_margin(op: int, prm, logk: np.ndarray, lp: np.ndarray, lq: np.ndarray,
+              one_m_p: np.ndarray, logK_tok: np.ndarray | None = None) -> np.ndarray:
+    """Distance of each token's decision variable from the operator's boundary (oracle side):
+    log k (or log K) from the cap / band edges, or KPop's metric from phi."""
+    with np.errstate(divide="ignore", invalid="ignore"):
+        if op in (X.OP_CIS, X.OP_TWO_SIDED):
+            m = np.abs(logk - np.log1p(prm.lam * np.maximum(one_m_p, prm.kappa)))
+            if op == X.OP_TWO_SIDED:
+                m = np.minimum(m, np.abs(logk - np.log1p(-0.5 * one_m_p)))
+        elif op == X.OP_TIS:
+            m = np.abs(logk - math.log(prm.hi))
+        elif op in (X.OP_EXACT, X.OP_ICEPOP):
+            m = np.minimum(np.abs(logk - math.log(max(prm.lo, 1e-300))),
+                           np.abs(logk - math.log(prm.hi)))
+        elif op == X.OP_KPOP:
+            m = np.array([abs(X.kpop_metric(a, b) - prm.hi) for a, b in zip(lp, lq)])
+        elif op == X.OP_QFIXED:
+            q, omq = np.exp(lq), -np.expm1(lq)
+            m = np.abs(logk + np.log(q + omq / (1.0 + prm.lam)))
+        elif op in X.SEQ_OPS:
+            lo = math.log(prm.lo) if prm.lo > 0 else -np.inf
+            m = np.minimum(np.abs(logK_tok - math.log(prm.hi)), np.abs(logK_tok - lo))
+        else:
+            m = np.full(logk.shape, np.inf)
+    return np.where(np.isfinite(m) | np.isinf(m), m, np.inf)
+
+
+def _worker(args):
+    rows, = args
+    d = _SHARED
+    if d["logp_old"] is None:
+        res = X.cis_ops_loss(d["z"], d["ids"], d["linf"], d["adv"], d["mask"], d["prm"],
+                             with_grad=d["gdev"] is not None, rows=rows)
+    else:
+        res = X.cis_ppo_loss(d["z"], d["ids"], d["linf"], d["logp_old"], d["adv"], d["mask"],
+                             d["prm"], offsets=d["offsets"], with_grad=d["gdev"] is not None,
+                             rows=rows)
+    gst = None
+    if d["gdev"] is not None:
+        keep = (res.flags & O.FLAG_VALID) > 0
+        keep &= (res.flags & O.FLAG_NONFINITE) == 0
+        keep &= d["acted_dev"][rows] == res.acted          # flags that differ: margin rows
+        if d["logp_old"] is not None:
+            hi_c, lo_c = 1.0 + d["prm"].clip_high, 1.0 - d["prm"].clip_low
+            keep &= (np.abs(res.rho - hi_c) > 1e-5 * hi_c) & (np.abs(res.rho - lo_c) > 1e-5 * lo_c)
+        # invalid rows must be exact zeros
+        inval = (res.flags & O.FLAG_VALID) == 0
+        gdev = d["gdev"]
+        g = O.bf16_bits_to_float64(gdev[rows]) if gdev.dtype == np.uint16 else \
+            gdev[rows].astype(np.float64)
+        gst = P.grad_stats(g[keep | inval], res.grad[keep | inval], gdev.dtype == np.uint16)
+        res.grad = None
+    return rows, res, gst
+
+
+def run_ops_oracle(b, prm, logp_old=None, offsets=None, rows=None, grad=None, acted=None):
+    """oracle.ops on batch `b` (rate-1 path, or decoupled with logp_old). With the device
+    gradient and acted flags, the workers compare the gradient rows themselves."""
+    z = P.host_logits(b.logits)
+    T = b.T
+    rows = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
+    _SHARED.clear()
+    _SHARED.update(
+        z=z, ids=b.ids.cpu().numpy(), linf=b.logp_infer.cpu().double().numpy(),
+        adv=b.adv.cpu().double().numpy(), mask=None if b.mask is None else b.mask.cpu().numpy(),
+        prm=prm, logp_old=None if logp_old is None else logp_old.cpu().double().numpy(),
+        offsets=None if offsets is None else offsets.cpu().numpy(),
+        gdev=None if grad is None else P.device_grad_host(grad, b.V),
+        acted_dev=None if acted is None else acted.cpu().numpy().astype(bool))
+    procs = P._nproc()
+    blocks = [blk for blk in np.array_split(rows, max(1, min(len(rows), procs * 4))) if len(blk)]
+    if procs > 1 and len(blocks) > 1:
+        with mp.get_context("fork").Pool(procs) as pool:
+            parts = pool.map(_worker, [(blk,) for blk in blocks])
+    else:
+        parts = [_worker((blk,)) for blk in blocks]
+    _SHARED.clear()
+    keys = ("logp_train", "w", "acted", "term", "flags", "logk", "eps", "gate", "rho")
+    res = {k: np.concatenate([getattr(r, k) for _, r, _ in parts]) for k in keys}
+    res["rows"] = rows
+    gsts = [g for _, _, g in parts if g is not None]
+    if gsts:
+        res["grad_stats"] = P.merge_grad_stats(gsts)
+    return res
+
+
+def compare_ops(out: dict, ref: dict, b, prm, report: dict, logp_old=None, offsets=None,
+                check_loss: bool = True) -> None:
+    """Per-row outputs, the loss and the diagnostics of an _ex call against the oracle."""
+    rows = ref["rows"]
+    scale = P.f32(prm.scale)
+    adv = b.adv.cpu().double().numpy()[rows]
+    linf = b.logp_infer.cpu().double().numpy()[rows]
+    valid = (ref["flags"] & O.FLAG_VALID) > 0
+    fin = valid & ((ref["flags"] & O.FLAG_NONFINITE) == 0)
+    g = {k: out[k].cpu().double().numpy()[rows] for k in ("logp_train", "w", "terms", "eps")}
+    acted = out["acted"].cpu().numpy()[rows].astype(bool)
+
+    assert np.all(g["logp_train"][~valid] == 0) and np.all(g["w"][~valid] == 0)
+    assert np.all(g["terms"][~valid] == 0) and not acted[~valid].any()
+    assert np.all(g["eps"][~valid] == 0)
+
+    # decision margins (oracle side)
+    if logp_old is None:
+        lp = ref["logp_train"]
+        one_m_p = -np.expm1(lp)
+    else:
+        lp = logp_old.cpu().double().numpy()[rows]
+        one_m_p = -np.expm1(lp)
+    logK_tok = None
+    if prm.op in X.SEQ_OPS:
+        offs = offsets.cpu().numpy()
+        full_valid = valid_all(b)
+        lk_all = logp_old.cpu().double().numpy() - b.logp_infer.cpu().double().numpy()
+        _, _, logK = X.seq_weights(prm.op, lk_all, full_valid, offs, prm)
+        seg = np.searchsorted(offs, rows, side="right") - 1
+        logK_tok = logK[np.clip(seg, 0, len(logK) - 1)]
+    margin = op_margin(prm.op, prm, ref["logk"], lp, linf, one_m_p, logK_tok)
+    differ = (acted != ref["acted"]) & fin
+    tol = margin_tol(prm.op)
+    assert np.all(margin[differ] < tol), \
+        f"{int((differ & (margin >= tol)).sum())} acted flags differ outside the margin"
+    same = fin & ~differ
+
+    with np.errstate(invalid="ignore"):
+        err_lt = np.where(g["logp_train"] == ref["logp_train"], 0.0,
+                          np.abs(g["logp_train"] - ref["logp_train"]))[fin]
+    assert np.all(err_lt <= 1e-5 * np.abs(ref["logp_train"][fin]) + 2e-6), \
+        f"logp_train: max err {err_lt.max():.3g}"
+    # weights below float32's normal range (a long response's K) may flush to zero
+    err_w = np.abs(g["w"] - ref["w"])[same]
+    rel_w = np.where(err_w == 0, 0.0, err_w / np.maximum(np.abs(ref["w"][same]), 1e-300))
+    assert np.all(err_w <= 1e-5 * np.abs(ref["w"][same]) + P.F32_TINY), \
+        f"w: max rel err {rel_w.max():.3g}"
+    rel_w = rel_w[np.abs(ref["w"][same]) >= P.F32_TINY]
+    if logp_old is None:
+        coefmag = np.abs(scale * ref["w"] * adv)
+    else:
+        coefmag = np.abs(scale * ref["w"] * adv) * np.maximum(ref["rho"], 1.0)
+    err_t = np.abs(g["terms"] - ref["term"])[same]
+    bound_t = 1e-5 * np.abs(ref["term"][same]) + 2e-6 * coefmag[same] + P.F32_TINY
+    if not np.all(err_t <= bound_t):
+        i = np.flatnonzero(same)[int(np.argmax(err_t - bound_t))]
+        raise AssertionError(
+            f"term out of tolerance at row {rows[i]}: gpu {g['terms'][i]!r} ref {ref['term'][i]!r} "
+            f"w gpu {g['w'][i]!r} ref {ref['w'][i]!r} rho {ref['rho'][i]!r} A {adv[i]!r} "
+            f"logp gpu {g['logp_train'][i]!r} ref {ref['logp_train'][i]!r} "
+            f"acted {bool(ref['acted'][i])} gate {bool(ref['gate'][i])}")
+    # displacement
+    e_ref, e_dev = ref["eps"][fin], g["eps"][fin]
+    inf = np.isinf(e_ref) | np.isinf(e_dev)
+    assert np.array_equal(e_ref[inf], e_dev[inf]), "infinite displacements differ"
+    assert np.all(np.abs(e_dev[~inf] - e_ref[~inf]) <= 1e-4 * np.abs(e_ref[~inf]) + 1e-5), \
+        "displacement out of tolerance"
+    report.update(rows=int(len(rows)), valid=int(valid.sum()), acted=int(ref["acted"].sum()),
+                  acted_in_margin_differ=int(differ.sum()),
+                  max_rel_w=float(rel_w.max()) if rel_w.size else 0.0,
+                  max_err_logp=float(err_lt.max()) if err_lt.size else 0.0)
+    if check_loss:
+        L = float(out["loss"].item())
+        L64 = math.fsum(ref["term"].tolist())
+        slack = float(np.sum(np.abs(g["terms"] - ref["term"])[differ]))
+        bound = 1e-5 * float(np.sum(np.abs(ref["term"]))) + 1e-6 + slack
+        assert abs(L - L64) <= bound, f"loss {L} vs {L64} (bound {bound:.3g})"
+        report.update(loss=L, loss_ref=L64)
+    report["_differ"] = differ
+
+
+def valid_all(b) -> np.ndarray:
+    ids = b.ids.cpu().numpy()
+    m = np.ones(b.T, dtype=bool) if b.mask is None else b.mask.cpu().numpy().astype(bool)
+    return m & (ids >= 0) & (ids < b.V)
+
+
+def check_diagnostics(stats: dict, ref: dict, differ: np.ndarray, report: dict) -> None:
+    """cis_stats_t diagnostics against the oracle over all rows (ref must cover every row)."""
+    valid = (ref["flags"] & O.FLAG_VALID) > 0
+    n_act = int(np.sum(ref["acted"] & valid))
+    assert abs(stats["n_trunc"] - n_act) <= int(differ.sum()), (stats["n_trunc"], n_act)
+    lk = np.abs(ref["logk"][valid])
+    mx = float(lk.max()) if lk.size else 0.0
+    assert abs(stats["max_abs_logk"] - mx) <= 1e-5 * mx + 2e-6, (stats["max_abs_logk"], mx)
+    k = np.exp(np.minimum(ref["logk"], 700.0))
+    ex = (k - ref["w"])[valid]
+    X64 = math.fsum(ex.tolist())
+    slack = float(np.sum(k[differ])) if differ.any() else 0.0
+    bound = 1e-4 * float(np.sum(np.abs(ex))) + 1e-6 * max(1, valid.sum()) + slack
+    assert abs(stats["trunc_excess"] - X64) <= bound, (stats["trunc_excess"], X64, bound)
+    report.update(n_acted=stats["n_trunc"], max_abs_logk=stats["max_abs_logk"],
+                  trunc_excess=stats["trunc_excess"], trunc_excess_ref=X64)

@@ -29,8 +29,9 @@ def test_probe_library_exports():
 def test_library_exports_every_declared_symbol():
     lib = cis.load_library()
     names = declared_functions()
-    assert set(names) == {"cis_workspace_bytes", "cis_status_string", "cis_weights",
-                          "cis_loss_fwd", "cis_loss_bwd"}
+    assert set(names) == {"cis_workspace_bytes", "cis_workspace_bytes_ex", "cis_status_string",
+                          "cis_weights", "cis_weights_ex", "cis_loss_fwd", "cis_loss_bwd",
+                          "cis_loss_fwd_ex", "cis_loss_bwd_ex"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -40,7 +41,11 @@ def test_workspace_bytes_layout():
     assert cis.workspace_bytes(0) == 256
     for T in (1, 255, 256, 16384, 65536, 524288):
         n = cis.workspace_bytes(T)
-        assert n % 256 == 0 and n >= 256 + 5 * T
+        # stats, four float arrays and two byte arrays per row
+        assert n % 256 == 0 and n >= 256 + 18 * T
+        assert cis.workspace_bytes_ex(T, 0) == n
+        assert cis.workspace_bytes_ex(T, 1000) >= n + 8 * 1000
+    assert cis.workspace_bytes_ex(-1, 0) == 0 and cis.workspace_bytes_ex(4, -1) == 0
 
 
 def test_status_strings():
@@ -120,3 +125,71 @@ def test_lambda_from_logodds():
     assert cis.lambda_from_logodds(0.0) == 0.0
     assert abs(cis.lambda_from_logodds(1.0) - (math.e - 1)) < 1e-15
     assert abs(cis.lambda_from_logodds(math.log(3.3)) - 2.3) < 1e-12
+
+
+def _prm(**kw):
+    p = cis.params(cis.OP_CIS, scale=-0.25)
+    for k, v in kw.items():
+        setattr(p, k, v)
+    return p
+
+
+def _fwd_ex(prm, **kw):
+    a = dict(logits=FAKE, dtype=0, T=4, V=8, ld=8, ids=FAKE, linf=FAKE, lold=NULL, adv=FAKE,
+             mask=NULL, offs=NULL, nseq=0, ws=FAKE, wsb=1 << 20)
+    a.update(kw)
+    pp = ctypes.byref(prm) if prm is not None else None
+    return cis.load_library().cis_loss_fwd_ex(
+        a["logits"], a["dtype"], a["T"], a["V"], a["ld"], a["ids"], a["linf"], a["lold"],
+        a["adv"], a["mask"], a["offs"], a["nseq"], pp, NULL, NULL, NULL, NULL, NULL, NULL,
+        a["ws"], a["wsb"], NULL)
+
+
+@pytest.mark.parametrize("prm,kw,code", [
+    (None, {}, -1),
+    (dict(op=10), {}, -4), (dict(op=-1), {}, -4), (dict(scale=float("inf")), {}, -4),
+    (dict(lam=-1.0), {}, -4), (dict(kappa=2.0), {}, -4),
+    (dict(op=2, lo=2.0, hi=1.0), {}, -4), (dict(op=2, lo=-1.0, hi=1.0), {}, -4),
+    (dict(op=4, lo=float("nan"), hi=1.0), {}, -4), (dict(op=3, hi=-1.0), {}, -4),
+    (dict(op=5, hi=float("nan")), {}, -4), (dict(op=7, lam=float("inf")), {}, -4),
+    # sequence operators need logp_old, and responses
+    (dict(op=8, hi=2.0), {}, -4),
+    (dict(op=9, lo=0.5, hi=2.0), dict(lold=FAKE, nseq=0), -2),
+    (dict(op=8, hi=2.0), dict(lold=FAKE, nseq=2), -1),
+    (dict(op=8, hi=2.0), dict(lold=FAKE, nseq=-1), -2),
+    # the decoupled path checks the PPO clip
+    (dict(clip_low=1.5), dict(lold=FAKE), -4), (dict(clip_high=-0.1), dict(lold=FAKE), -4),
+    (dict(clip_high=float("inf")), dict(lold=FAKE), -4),
+    ({}, dict(wsb=100), -7), ({}, dict(ws=FAKE + 16), -5), ({}, dict(dtype=9), -3),
+])
+def test_fwd_ex_argument_errors(prm, kw, code):
+    p = None if prm is None else _prm(**prm)
+    assert _fwd_ex(p, **kw) == code
+
+
+def test_fwd_ex_accepts_valid_arguments_up_to_the_device_check():
+    # on a host without a gfx950 device, valid arguments get as far as CIS_ERR_DEVICE
+    for op, extra in ((0, {}), (2, dict(lo=1e-6, hi=1e6)), (3, dict(hi=2.0)),
+                      (4, dict(lo=0.5, hi=5.0)), (5, dict(hi=2.0)), (6, {}), (7, {}), (1, {})):
+        assert _fwd_ex(_prm(op=op, **extra)) == -9
+        assert _fwd_ex(_prm(op=op, **extra), lold=FAKE) == -9
+    assert _fwd_ex(_prm(op=8, hi=2.0), lold=FAKE, offs=FAKE, nseq=2) == -9
+
+
+def test_weights_ex_argument_errors():
+    lib = cis.load_library()
+
+    def call(prm, T=4, lp=FAKE, offs=NULL, nseq=0, w=FAKE, ws=FAKE, wsb=1 << 20):
+        pp = ctypes.byref(prm) if prm is not None else None
+        return lib.cis_weights_ex(lp, FAKE, NULL, T, offs, nseq, pp, w, NULL, NULL, ws, wsb, NULL)
+    assert call(None) == -1
+    assert call(_prm(), T=-1) == -2
+    assert call(_prm(op=12)) == -4
+    assert call(_prm(op=8, hi=2.0)) == -2           # sequence operator without responses
+    assert call(_prm(op=8, hi=2.0), nseq=1) == -1   # ... or without offsets
+    assert call(_prm(), lp=NULL) == -1
+    assert call(_prm(), w=NULL) == -1
+    assert call(_prm(), ws=NULL) == -1
+    assert call(_prm(), ws=FAKE + 8) == -5
+    assert call(_prm(), wsb=16) == -7
+    assert call(_prm()) == -9

@@ -247,3 +247,33 @@ def make_random_batch(T: int, V: int, dtype=torch.bfloat16, device="cuda", seed:
     n_valid = max(int(mask.sum().item()), 1)
     return Batch(view, ids, lq, adv, mask, lambda_of(c), kappa, -1.0 / n_valid,
                  {"seed": seed, "ld": ld})
+
+
+def old_logprobs(b: Batch, sd: float = 0.3, seed: int = 0) -> torch.Tensor:
+    """Training-side log-probabilities of the sampled ids at a rollout snapshot theta_old, for
+    the decoupled objective (App. C.1: both engines' log-probabilities are recorded per token):
+    log_softmax(z + sd * N(0, 1))[y] in float32, with z the stored training logits. The update
+    ratio exp(l_train - l_old) then spreads around 1 by about sd in log space."""
+    g = _gen(b.logits.device, 7919 + seed)
+    T = b.T
+    out = torch.empty(T, dtype=torch.float32, device=b.logits.device)
+    step = max(1, min(T, (1 << 27) // max(b.V, 1)))
+    for r0 in range(0, T, step):
+        z = b.logits[r0:r0 + step].float()
+        z = z + sd * torch.randn(z.shape, generator=g, device=z.device)
+        y = b.ids[r0:r0 + step].clamp(0, b.V - 1)
+        out[r0:r0 + step] = torch.log_softmax(z, dim=1).gather(1, y[:, None])[:, 0]
+    return out
+
+
+def response_offsets(T: int, min_len: int, max_len: int, seed: int = 0,
+                     device="cuda") -> torch.Tensor:
+    """CSR offsets [n + 1] of responses packed back to back over T tokens, lengths uniform in
+    [min_len, max_len] (the last one cut at T)."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(int(seed))
+    offs = [0]
+    while offs[-1] < T:
+        n = int(torch.randint(min_len, max_len + 1, (1,), generator=g).item())
+        offs.append(min(T, offs[-1] + n))
+    return torch.tensor(offs, dtype=torch.int64, device=device)
