@@ -12,7 +12,11 @@ contains the tiny loss-reduction kernel, so this slightly understates the row ke
 `cpu_baseline` times the float64 CPU oracle on a bounded sample of the same rows, on the host's
 cores.
 
-    python bench.py [--steps K] [--warmup W] [--c C] [--mode bwd|fwd] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--c C] [--mode bwd|fwd] [--config N]
+                    [--op NAME] [--decoupled] [--no-cpu-baseline] [--no-copy-ceiling]
+
+--op / --decoupled time the operator family and the decoupled PPO-clip path (the _ex entry
+points; the decoupled call includes its weight pre-pass) on the same workload.
 """
 
 from __future__ import annotations
@@ -36,17 +40,28 @@ PER_TOKEN_SCALAR_BYTES = 30   # ids 8 + mask 1 + l_infer 4 + A 4 in; l_train 4 +
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("paper_2609_32444_amd/csrc/cis_kernels.hip", "paper_2609_32444_amd/csrc/cis_api.cpp",
-              "paper_2609_32444_amd/csrc/cis_internal.h"):
+    for f in ("paper_2609_32444_amd/csrc/cis_row.h", "paper_2609_32444_amd/csrc/cis_kernels.hip",
+              "paper_2609_32444_amd/csrc/cis_kernels_ext.hip",
+              "paper_2609_32444_amd/csrc/cis_api.cpp", "paper_2609_32444_amd/csrc/cis_internal.h"):
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(T_valid: int, T_invalid: int, V: int, esize: int, bwd: bool) -> int:
-    per_valid = esize * V * (2 if bwd else 1) + PER_TOKEN_SCALAR_BYTES
+def algorithmic_bytes(T_valid: int, T_invalid: int, V: int, esize: int, bwd: bool,
+                      decoupled: bool = False) -> int:
+    """Bytes the method must move per call: each valid row's logits once (and its gradient
+    once), each invalid row's zero gradient, and the per-token inputs and outputs (the
+    decoupled path also reads l_old). Implementation scratch (workspace) is not counted."""
+    per_valid = esize * V * (2 if bwd else 1) + PER_TOKEN_SCALAR_BYTES + (4 if decoupled else 0)
     per_invalid = (esize * V if bwd else 0) + 9
     return T_valid * per_valid + T_invalid * per_invalid
+
+
+OPS = {"cis": 0, "none": 1, "exact": 2, "tis": 3, "icepop": 4, "kpop": 5, "two_sided": 6,
+       "qfixed": 7, "seq_tis": 8, "seq_mis": 9}
+OP_BOUNDS = {"exact": (1e-6, 1e6), "tis": (0.0, 2.0), "icepop": (0.5, 5.0), "kpop": (0.0, 2.0),
+             "seq_tis": (0.0, 2.0), "seq_mis": (0.5, 2.0)}   # Table tab:baselines
 
 
 def hbm_traffic(mode: str, workload: str):
@@ -175,6 +190,10 @@ def main():
     ap.add_argument("--c", type=float, default=1.0)
     ap.add_argument("--mode", choices=("bwd", "fwd"), default="bwd")
     ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--op", choices=sorted(OPS), default=None,
+                    help="operator of the weight (cis_loss_*_ex); default: the base CIS path")
+    ap.add_argument("--decoupled", action="store_true",
+                    help="the decoupled PPO-clip objective with l_old at a theta_old snapshot")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-ceiling", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -203,10 +222,23 @@ def main():
         print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n}), flush=True)
         return
     b = make_batch(args.config, device="cuda", c=args.c)
-    torch.cuda.synchronize()
     bwd = args.mode == "bwd"
-    call = cis.LossCall(b.logits, b.ids, b.logp_infer, b.adv, b.mask, lam=b.lam, kappa=b.kappa,
-                        scale=b.scale, bwd=bwd)
+    ext = args.op is not None or args.decoupled
+    op = args.op or "cis"
+    if op in ("seq_tis", "seq_mis") and not args.decoupled:
+        ap.error("sequence operators need --decoupled")
+    if ext:
+        from workloads import old_logprobs, response_offsets
+        lo, hi = OP_BOUNDS.get(op, (0.0, math.inf))
+        prm = cis.params(OPS[op], lam=b.lam, kappa=b.kappa, lo=lo, hi=hi, scale=b.scale)
+        lold = old_logprobs(b, sd=0.3) if args.decoupled else None
+        offs = response_offsets(b.T, 256, 1536) if op.startswith("seq_") else None
+        call = cis.LossCall(b.logits, b.ids, b.logp_infer, b.adv, b.mask, bwd=bwd, params=prm,
+                            logp_old=lold, seq_offsets=offs)
+    else:
+        call = cis.LossCall(b.logits, b.ids, b.logp_infer, b.adv, b.mask, lam=b.lam,
+                            kappa=b.kappa, scale=b.scale, bwd=bwd)
+    torch.cuda.synchronize()
     for _ in range(args.warmup):
         call.run()
     torch.cuda.synchronize()
@@ -232,13 +264,20 @@ def main():
     n_valid = stats["n_valid"]
     T, V = b.T, b.V
     esize = b.logits.element_size()
-    alg = algorithmic_bytes(n_valid, T - n_valid, V, esize, bwd)
+    alg = algorithmic_bytes(n_valid, T - n_valid, V, esize, bwd, args.decoupled)
     achieved_gbs = alg / (avg_call_ms * 1e-3) / 1e9
     tokens_per_s = n_valid / (ms_per_step * 1e-3)
 
     workload = f"{b.meta['name']} T={T} V={V} {'bf16' if esize == 2 else 'fp32'} c={args.c:g} " \
                f"kappa={b.kappa:g} {'fused fwd+bwd' if bwd else 'forward only'}"
-    traffic = hbm_traffic(args.mode, f"cfg{args.config}")
+    if ext:
+        workload += f" op={op}" + (" decoupled PPO-clip (0.2, 0.28)" if args.decoupled else "")
+    if not ext:
+        traffic = hbm_traffic(args.mode, f"cfg{args.config}")
+    elif op == "cis" and args.decoupled:
+        traffic = hbm_traffic(args.mode, f"cfg{args.config}_decoupled")
+    else:
+        traffic = None
     line = {
         "metric": METRIC if bwd else METRIC.replace("fwd+bwd", "fwd"),
         "value": tokens_per_s,
@@ -272,7 +311,11 @@ def main():
         line["roofline"]["measured_ceiling_gbs"] = ceil
         line["roofline"]["frac_of_measured_copy"] = achieved_gbs / ceil["copy"] if bwd else \
             achieved_gbs / ceil["read"]
-    if not args.no_cpu_baseline:
+    if ext:
+        line["config"]["op"] = op
+        line["config"]["decoupled"] = bool(args.decoupled)
+        line["diagnostics"] = {k: stats[k] for k in ("n_trunc", "max_abs_logk", "trunc_excess")}
+    if not args.no_cpu_baseline and not ext:
         line["cpu_baseline"] = cpu_baseline(b, V)
     print(json.dumps(line), flush=True)
 

@@ -245,31 +245,51 @@ class LossCall:
     """One loss call with every output, the gradient and the workspace allocated up front;
     run() only launches (what a training step or a benchmark repeats)."""
 
-    def __init__(self, logits, ids, logp_infer, adv, mask=None, *, lam, kappa=5e-3, scale=1.0,
-                 bwd=True, V=None, want=_ALL):
+    def __init__(self, logits, ids, logp_infer, adv, mask=None, *, lam=2.3, kappa=5e-3,
+                 scale=1.0, bwd=True, V=None, want=_ALL, params: Optional[Params] = None,
+                 logp_old=None, seq_offsets=None):
+        """With `params` the call goes through cis_loss_{fwd,bwd}_ex (any operator; with
+        logp_old, the decoupled path) and the "trunc" output is the acted-on flag."""
         dtype, T, V, ld = _logits_args(logits, V)
         dev = logits.device
         _check_vec("ids", ids, T, torch.int64, dev)
         _check_vec("logp_infer", logp_infer, T, torch.float32, dev)
         _check_vec("adv", adv, T, torch.float32, dev)
+        _check_vec("logp_old", logp_old, T, torch.float32, dev, optional=True)
         mask = _check_vec("mask", _mask_u8(mask), T, torch.uint8, dev, optional=True)
+        ext = params is not None
+        if not ext and (logp_old is not None or seq_offsets is not None):
+            raise ValueError("logp_old and seq_offsets need params")
+        offs, n_seq = _offsets(seq_offsets, T, dev)
         self.dev, self.bwd, self.T, self.V = dev, bwd, T, V
         self.out = _outputs(T, dev, want)
-        self.workspace = torch.empty(workspace_bytes(T), dtype=torch.uint8, device=dev)
-        self._keep = (logits, ids, logp_infer, adv, mask)
-        common = (_ptr(logits), dtype, T, V, ld, _ptr(ids), _ptr(logp_infer), _ptr(adv),
-                  _ptr(mask), float(lam), float(kappa), float(scale))
-        tail = (_ptr(self.out.get("logp_train")), _ptr(self.out.get("w")),
-                _ptr(self.out.get("trunc")), _ptr(self.out.get("terms")), _ptr(self.out["loss"]),
-                _ptr(self.workspace), self.workspace.numel())
+        nws = workspace_bytes_ex(T, n_seq) if ext else workspace_bytes(T)
+        self.workspace = torch.empty(nws, dtype=torch.uint8, device=dev)
+        self._prm = params
+        self._keep = (logits, ids, logp_infer, adv, mask, logp_old, offs)
         lib = load_library()
+        if ext:
+            common = (_ptr(logits), dtype, T, V, ld, _ptr(ids), _ptr(logp_infer),
+                      _ptr(logp_old), _ptr(adv), _ptr(mask), _ptr(offs), n_seq,
+                      ctypes.byref(self._prm))
+            tail = (_ptr(self.out.get("logp_train")), _ptr(self.out.get("w")),
+                    _ptr(self.out.get("trunc")), _ptr(self.out.get("terms")), None,
+                    _ptr(self.out["loss"]), _ptr(self.workspace), self.workspace.numel())
+            fns = (lib.cis_loss_bwd_ex, "cis_loss_bwd_ex", lib.cis_loss_fwd_ex, "cis_loss_fwd_ex")
+        else:
+            common = (_ptr(logits), dtype, T, V, ld, _ptr(ids), _ptr(logp_infer), _ptr(adv),
+                      _ptr(mask), float(lam), float(kappa), float(scale))
+            tail = (_ptr(self.out.get("logp_train")), _ptr(self.out.get("w")),
+                    _ptr(self.out.get("trunc")), _ptr(self.out.get("terms")),
+                    _ptr(self.out["loss"]), _ptr(self.workspace), self.workspace.numel())
+            fns = (lib.cis_loss_bwd, "cis_loss_bwd", lib.cis_loss_fwd, "cis_loss_fwd")
         if bwd:
             self.dlogits = _new_grad(T, V, logits)
-            self._fn, self._name = lib.cis_loss_bwd, "cis_loss_bwd"
+            self._fn, self._name = fns[0], fns[1]
             self._args = common + (_ptr(self.dlogits), self.dlogits.stride(0)) + tail
             self.out["dlogits"] = self.dlogits
         else:
-            self._fn, self._name = lib.cis_loss_fwd, "cis_loss_fwd"
+            self._fn, self._name = fns[2], fns[3]
             self._args = common + tail
         self.out["workspace"] = self.workspace
 
