@@ -149,19 +149,29 @@ def test_threshold_and_floor_settings(kappa, c):
         assert np.allclose(w, np.minimum(k, 1.0), rtol=1e-5)
 
 
-def test_in_place_gradient():
-    b = make_random_batch(40, 9001, torch.bfloat16, DEV, seed=9, ld=9008)
-    ref_out = cis.loss_bwd(b.logits, b.ids, b.logp_infer, b.adv, b.mask, lam=b.lam,
-                           kappa=b.kappa, scale=b.scale, V=b.V)
+@pytest.mark.parametrize("V,ld", [(9001, 9008), (151936, 151936), (200003, 200016)])
+def test_in_place_gradient(V, ld):
+    # The gradient overwrites the logits row by row (each element is read before the same
+    # thread writes it). Checked against the oracle on the original logits, and bit for bit
+    # against a separate output buffer.
+    b = make_random_batch(40, V, torch.bfloat16, DEV, seed=9, ld=ld)
+    store = torch.empty(2, 40, ld, dtype=torch.bfloat16, device=DEV)
+    store[0, :, :V] = b.logits
+    buf = store[0, :, :V]
+    sep = store[1, :, :V]
+    ref_out = cis.loss_bwd(buf, b.ids, b.logp_infer, b.adv, b.mask, lam=b.lam, kappa=b.kappa,
+                           scale=b.scale, V=V, dlogits=sep)
     torch.cuda.synchronize()
-    g_sep = ref_out["dlogits"].clone()
-    store = torch.empty(40, 9008, dtype=torch.bfloat16, device=DEV)
-    store[:, :b.V] = b.logits
-    buf = store[:, :b.V]            # same row stride as the logits (ld = 9008)
+    ref = P.oracle_for_batch(b, with_grad=False, grad=ref_out["dlogits"])
     out = cis.loss_bwd(buf, b.ids, b.logp_infer, b.adv, b.mask, lam=b.lam, kappa=b.kappa,
-                       scale=b.scale, V=b.V, dlogits=buf)
+                       scale=b.scale, V=V, dlogits=buf)
     torch.cuda.synchronize()
-    assert torch.equal(buf.view(torch.int16), g_sep.view(torch.int16))
+    rep = {}
+    P.check_grad_stats(ref["grad_stats"], rep)
+    ref_ip = P.oracle_for_batch(b, with_grad=False, grad=buf)
+    P.check_grad_stats(ref_ip["grad_stats"], rep)
+    P.compare_scalars(out, ref_ip, b, rep)
+    assert torch.equal(buf.view(torch.int16), sep.view(torch.int16))
     assert torch.equal(out["w"], ref_out["w"])
 
 
