@@ -17,6 +17,12 @@ cores.
 
 --op / --decoupled time the operator family and the decoupled PPO-clip path (the _ex entry
 points; the decoupled call includes its weight pre-pass) on the same workload.
+
+--lmhead times the loss behind the LM head instead (cis_lmhead_loss_bwd / _fwd): hidden states
+[T, H] and a head weight [V, H] in bf16 (workloads/lmhead.py; H = 2048 by default), the logits
+formed chunk by chunk on the matrix cores and never materialised for the whole batch. Its
+`roofline` is the matrix-core bound: the three products' FLOPs (2 T V H each; one for the
+forward) per call over the call time, against the bf16 dense peak.
 """
 
 from __future__ import annotations
@@ -34,15 +40,17 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 METRIC = "tokens/sec and achieved HBM GB/s, CIS loss fwd+bwd, V=151936, 1 MI355X"
 PER_TOKEN_SCALAR_BYTES = 30   # ids 8 + mask 1 + l_infer 4 + A 4 in; l_train 4 + w 4 + trunc 1 + term 4 out
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(extra=()) -> str:
     h = hashlib.sha256()
     for f in ("paper_2609_32444_amd/csrc/cis_row.h", "paper_2609_32444_amd/csrc/cis_kernels.hip",
               "paper_2609_32444_amd/csrc/cis_kernels_ext.hip",
-              "paper_2609_32444_amd/csrc/cis_api.cpp", "paper_2609_32444_amd/csrc/cis_internal.h"):
+              "paper_2609_32444_amd/csrc/cis_api.cpp", "paper_2609_32444_amd/csrc/cis_internal.h",
+              *extra):
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -184,6 +192,138 @@ def _baseline_worker(idx):
     return len(idx)
 
 
+def cpu_baseline_lmhead(b, prm_ref, target_s: float = 15.0):
+    """oracle.lmhead as it stands (float64: logits, loss, dL/dh and dL/dW of the sampled rows) on
+    a sample of rows, one process whose matrix products use the host's BLAS threads."""
+    import numpy as np
+
+    from oracle import lmhead as L
+
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    W = b.weight.float().cpu().double().numpy()
+    h = b.hidden.float().cpu().double().numpy()
+    ids = b.ids.cpu().numpy()
+    linf = b.logp_infer.cpu().double().numpy()
+    adv = b.adv.cpu().double().numpy()
+    mask = b.mask.cpu().numpy()
+
+    def run(rows):
+        L.lmhead_cis_loss(h[rows], W, ids[rows], linf[rows], adv[rows], mask[rows], prm_ref,
+                          with_grad=True, chunk=1024)
+
+    rng = np.random.default_rng(0)
+    run(np.arange(4))                       # warm-up: BLAS threads, page-in
+    t0 = time.perf_counter()
+    run(np.arange(4, 68))
+    per_row = (time.perf_counter() - t0) / 64
+    n = int(max(64, min(b.T, 8192, target_s / max(per_row, 1e-6))))
+    rows = np.sort(rng.choice(b.T, size=n, replace=False))
+    t0 = time.perf_counter()
+    run(rows)
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n} random rows of the same batch through oracle.lmhead (float64 logits, "
+                      f"loss, dL/dh and dL/dW of those rows), one process, BLAS on {cores} "
+                      f"threads, {dt:.1f} s wall"}
+
+
+def bench_lmhead(args, torch, cis):
+    """The loss behind the LM head (see the module docstring)."""
+    import numpy as np
+
+    from oracle import ops as X
+    from workloads import make_lmhead_batch
+
+    spec = {2: (16384, 151936)}.get(args.config)
+    if spec is None:
+        raise SystemExit("--lmhead runs the MoE-rollout shape (--config 2)")
+    T, V = spec
+    H, chunk = args.hidden, args.chunk
+    b = make_lmhead_batch(T, V, H, device="cuda", seed=2, c=args.c)
+    bwd = args.mode == "bwd"
+    prm = cis.params(cis.OP_CIS, lam=b.lam, kappa=b.kappa, scale=b.scale)
+    ws = torch.empty(cis.lmhead_workspace_bytes(T, V, H, chunk, 0, bwd), dtype=torch.uint8,
+                     device="cuda")
+    dh = torch.empty(T, H, dtype=torch.float32, device="cuda") if bwd else None
+    dw = torch.empty(V, H, dtype=torch.float32, device="cuda") if bwd else None
+    want = ("logp_train", "w", "acted", "terms")
+    if bwd:
+        def step():
+            return cis.lmhead_loss_bwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
+                                       params=prm, chunk=chunk, dhidden=dh, dweight=dw,
+                                       want=want, workspace=ws)
+    else:
+        def step():
+            return cis.lmhead_loss_fwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
+                                       params=prm, chunk=chunk, want=want, workspace=ws)
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    t_all0 = torch.cuda.Event(enable_timing=True)
+    t_all1 = torch.cuda.Event(enable_timing=True)
+    t_all0.record()
+    for i in range(args.steps):
+        starts[i].record()
+        step()
+        ends[i].record()
+    t_all1.record()
+    torch.cuda.synchronize()
+    ms_per_step = t_all0.elapsed_time(t_all1) / args.steps
+    per_call = sorted(s.elapsed_time(e) for s, e in zip(starts, ends))
+    avg_call_ms = sum(per_call) / len(per_call)
+    stats = cis.read_stats(ws)
+    n_valid = stats["n_valid"]
+    flops = (3 if bwd else 1) * 2.0 * T * V * H
+    tflops = flops / (avg_call_ms * 1e-3) / 1e12
+    line = {
+        "metric": f"tokens/sec, CIS loss {'fwd+bwd' if bwd else 'fwd'} through the LM head "
+                  f"(H={H} -> V={V}), 1 MI355X",
+        "value": n_valid / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"moe-rollout LM head T={T} V={V} H={H} bf16 chunk={chunk} "
+                               f"c={args.c:g} {'fused fwd+bwd' if bwd else 'forward only'}",
+                   "T": T, "V": V, "H": H, "chunk": chunk, "valid_tokens": n_valid,
+                   "lambda": b.lam, "kappa": b.kappa, "seed": b.meta["seed"]},
+        "roofline": {
+            "bound": "mfma",
+            "achieved": tflops,
+            "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": tflops / MFMA_BF16_PEAK_TFLOPS,
+            "traffic": None,
+            "algorithmic_flops_per_call": flops,
+            "avg_call_ms": avg_call_ms,
+            "min_call_ms": per_call[0],
+            "scope": "whole call (every kernel of the chunked pipeline) against the matrix-core "
+                     "peak of its three products",
+            "kernel_source": kernel_source_hash(("paper_2609_32444_amd/csrc/cis_gemm.hip",
+                                                 "paper_2609_32444_amd/csrc/cis_gemm.h")),
+        },
+    }
+    if not args.no_cpu_baseline:
+        f32 = lambda x: float(np.float32(x))  # noqa: E731
+        prm_ref = X.OpParams(op=X.OP_CIS, lam=f32(b.lam), kappa=f32(b.kappa), lo=0.0,
+                             hi=math.inf, clip_low=f32(0.2), clip_high=f32(0.28),
+                             scale=f32(b.scale))
+        line["cpu_baseline"] = cpu_baseline_lmhead(b, prm_ref)
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -196,6 +336,10 @@ def main():
                     help="operator of the weight (cis_loss_*_ex); default: the base CIS path")
     ap.add_argument("--decoupled", action="store_true",
                     help="the decoupled PPO-clip objective with l_old at a theta_old snapshot")
+    ap.add_argument("--lmhead", action="store_true",
+                    help="the loss behind the LM head (hidden [T, H] x weight [V, H], bf16)")
+    ap.add_argument("--hidden", type=int, default=2048, help="--lmhead: hidden size H")
+    ap.add_argument("--chunk", type=int, default=4096, help="--lmhead: rows per chunk")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-ceiling", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -222,6 +366,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n}), flush=True)
+        return
+    if args.lmhead:
+        bench_lmhead(args, torch, cis)
         return
     b = make_batch(args.config, device="cuda", c=args.c)
     bwd = args.mode == "bwd"

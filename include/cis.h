@@ -280,6 +280,73 @@ int cis_loss_bwd_ex(const void* logits, int dtype, int64_t T, int64_t V, int64_t
                     float* loss_terms_out, float* eps_out, float* loss_out,
                     void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* =========================================================================================
+ * The loss behind the language-model head: the logits are z_t = W h_t, the output of the
+ * policy's final projection (the training engine's logits of Sec. 3.1; App. C.1 trains in
+ * bf16), and are never materialised for the whole batch. Rows are processed `chunk` at a time:
+ * the chunk's logits are formed in float32 by a matrix-core product, the loss of
+ * cis_loss_fwd_ex / cis_loss_bwd_ex is evaluated on them, and the backward forms
+ *
+ *   dL/dh = G W        and        dL/dW = G^T h,        G = dL/dz  (chunk by chunk),
+ *
+ * with G rounded to bf16 as the operand of those two products (float32 accumulation).
+ * ========================================================================================= */
+
+/* Workspace bytes for cis_lmhead_loss_fwd (with_grad = 0) or _bwd (with_grad != 0): the loss
+ * workspace of cis_workspace_bytes_ex plus the chunk's float32 logits (min(T, chunk) x V) and,
+ * with gradients, W^T and two transposed chunk operands (about 2*V*H + 2*(V + H)*chunk bytes).
+ * Returns 0 for T < 0, V outside [1, 2^28], H outside [1, 2^16], chunk outside [1, 2^16] or
+ * n_seq < 0. */
+size_t cis_lmhead_workspace_bytes(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_t n_seq,
+                                  int with_grad);
+
+/*
+ * cis_lmhead_loss_fwd — the loss (any operator; the decoupled path with logp_old) on the logits
+ * hidden * weight^T.
+ *
+ *   hidden [T, ld_h] bf16   last hidden state of each token row; ld_h >= H, a multiple of 8,
+ *                           base 16-byte aligned
+ *   weight [V, ld_w] bf16   head weight (row v produces logit v); ld_w >= H, a multiple of 8,
+ *                           base 16-byte aligned
+ *   chunk                   rows per chunk (1 <= chunk <= 2^16); the workspace holds one
+ *                           chunk of float32 logits. Results do not depend on chunk.
+ *   ids, logp_infer, logp_old, adv, mask, seq_offsets, n_seq, params and the per-row outputs
+ *                           as for cis_loss_fwd_ex
+ *   workspace               >= cis_lmhead_workspace_bytes(T, V, H, chunk, n_seq, 0), 256-byte
+ *                           aligned; receives the cis_stats_t
+ * Errors: as for cis_loss_fwd_ex; CIS_ERR_SHAPE also for H or ld_* out of range, CIS_ERR_ALIGN
+ * for hidden / weight alignment.
+ */
+int cis_lmhead_loss_fwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
+                        const void* weight, int64_t V, int64_t ld_w,
+                        const int64_t* ids, const float* logp_infer, const float* logp_old,
+                        const float* adv, const uint8_t* mask, const int64_t* seq_offsets,
+                        int64_t n_seq, const cis_params_t* params, int64_t chunk,
+                        float* logp_train_out, float* w_out, uint8_t* acted_out,
+                        float* loss_terms_out, float* eps_out, float* loss_out,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * cis_lmhead_loss_bwd — everything cis_lmhead_loss_fwd produces, plus the gradients of
+ * sum_t term_t with respect to the hidden states and the head weight.
+ *
+ *   dhidden [T, ld_dh] float32   dL/dh (overwritten; rows of invalid tokens are 0); ld_dh >= H
+ *   dweight [V, ld_dw] float32   dL/dW; ld_dw >= H. accumulate_dweight = 0 overwrites it (zeros
+ *                                when T = 0), nonzero adds the gradient to its contents.
+ *   workspace                    >= cis_lmhead_workspace_bytes(T, V, H, chunk, n_seq, 1)
+ * dhidden and dweight must not overlap each other, the inputs or the workspace.
+ */
+int cis_lmhead_loss_bwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
+                        const void* weight, int64_t V, int64_t ld_w,
+                        const int64_t* ids, const float* logp_infer, const float* logp_old,
+                        const float* adv, const uint8_t* mask, const int64_t* seq_offsets,
+                        int64_t n_seq, const cis_params_t* params, int64_t chunk,
+                        float* dhidden, int64_t ld_dh, float* dweight, int64_t ld_dw,
+                        int accumulate_dweight,
+                        float* logp_train_out, float* w_out, uint8_t* acted_out,
+                        float* loss_terms_out, float* eps_out, float* loss_out,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

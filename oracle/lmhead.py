@@ -50,23 +50,31 @@ class LmHeadResult:
     acted: np.ndarray         # [T] bool
     term: np.ndarray          # [T]
     flags: np.ndarray         # [T] uint8
+    logk: np.ndarray          # [T] log k of the operator's weight (oracle.ops)
+    eps: np.ndarray           # [T] displacement
+    gate: np.ndarray          # [T] bool, the PPO gradient flows (decoupled path)
+    rho: np.ndarray           # [T] update ratio (1 on the rate-1 path)
     loss: float
     dhidden: np.ndarray | None  # [T, H] float64
     dW: np.ndarray | None       # [V, H] float64
+    grad: np.ndarray | None = None  # [T, V] dL/dz (keep_grad only)
 
 
 def lmhead_cis_loss(hidden, W, ids, logp_infer, adv, mask, prm: "X.OpParams",
                     logp_old=None, offsets=None, with_grad: bool = True,
-                    chunk: int = 1024) -> LmHeadResult:
+                    chunk: int = 1024, keep_grad: bool = False) -> LmHeadResult:
     """The CIS loss (or any operator of oracle.ops; the decoupled path with logp_old) on the
-    logits hidden @ W^T, and its gradients with respect to hidden and W, in float64."""
+    logits hidden @ W^T, and its gradients with respect to hidden and W, in float64.
+    keep_grad also returns dL/dz itself (small problems)."""
     hidden = np.asarray(hidden, dtype=np.float64)
     W = np.asarray(W, dtype=np.float64)
     T, H = hidden.shape
     V = W.shape[0]
-    out = {k: [] for k in ("logp_train", "w", "acted", "term", "flags")}
+    out = {k: [] for k in ("logp_train", "w", "acted", "term", "flags", "logk", "eps", "gate",
+                           "rho")}
     dhidden = np.zeros((T, H)) if with_grad else None
     dW = np.zeros((V, H)) if with_grad else None
+    grads = [] if (with_grad and keep_grad) else None
     for t0 in range(0, T, chunk):
         t1 = min(T, t0 + chunk)
         z = lmhead_logits(hidden[t0:t1], W)
@@ -83,13 +91,16 @@ def lmhead_cis_loss(hidden, W, ids, logp_infer, adv, mask, prm: "X.OpParams",
             out[k].append(getattr(r, k))
         if with_grad:
             G = r.grad
+            if grads is not None:
+                grads.append(G)
             dhidden[t0:t1] = G @ W
             dW += G.T @ hidden[t0:t1]
     res = {k: np.concatenate(v) for k, v in out.items()}
     term = res["term"]
     loss = math.fsum(term.tolist()) if np.all(np.isfinite(term)) else float(np.sum(term))
-    return LmHeadResult(res["logp_train"], res["w"], res["acted"], term, res["flags"], loss,
-                        dhidden, dW)
+    return LmHeadResult(res["logp_train"], res["w"], res["acted"], term, res["flags"],
+                        res["logk"], res["eps"], res["gate"], res["rho"], loss, dhidden, dW,
+                        np.concatenate(grads) if grads else None)
 
 
 class _Rows:

@@ -90,6 +90,17 @@ def load_library() -> ctypes.CDLL:
                                     _i64, ctypes.POINTER(Params), _vp, _i64, _vp, _vp, _vp, _vp,
                                     _vp, _vp, _vp, _size, _vp]
     lib.cis_loss_bwd_ex.restype = _int
+    lib.cis_lmhead_workspace_bytes.argtypes = [_i64, _i64, _i64, _i64, _i64, _int]
+    lib.cis_lmhead_workspace_bytes.restype = _size
+    lib.cis_lmhead_loss_fwd.argtypes = [_vp, _i64, _i64, _i64, _vp, _i64, _i64, _vp, _vp, _vp,
+                                        _vp, _vp, _vp, _i64, ctypes.POINTER(Params), _i64,
+                                        _vp, _vp, _vp, _vp, _vp, _vp, _vp, _size, _vp]
+    lib.cis_lmhead_loss_fwd.restype = _int
+    lib.cis_lmhead_loss_bwd.argtypes = [_vp, _i64, _i64, _i64, _vp, _i64, _i64, _vp, _vp, _vp,
+                                        _vp, _vp, _vp, _i64, ctypes.POINTER(Params), _i64,
+                                        _vp, _i64, _vp, _i64, _int,
+                                        _vp, _vp, _vp, _vp, _vp, _vp, _vp, _size, _vp]
+    lib.cis_lmhead_loss_bwd.restype = _int
     _LIB = lib
     return lib
 
@@ -104,6 +115,12 @@ def workspace_bytes(T: int) -> int:
 
 def workspace_bytes_ex(T: int, n_seq: int = 0) -> int:
     return int(load_library().cis_workspace_bytes_ex(int(T), int(n_seq)))
+
+
+def lmhead_workspace_bytes(T: int, V: int, H: int, chunk: int, n_seq: int = 0,
+                           with_grad: bool = True) -> int:
+    return int(load_library().cis_lmhead_workspace_bytes(int(T), int(V), int(H), int(chunk),
+                                                         int(n_seq), int(bool(with_grad))))
 
 
 def lambda_from_logodds(c: float) -> float:
@@ -436,3 +453,86 @@ def loss_bwd_ex(logits, ids, logp_infer, adv, mask=None, *, params: Params, logp
     plus "dlogits"."""
     return _loss_ex(True, logits, ids, logp_infer, adv, mask, params, logp_old, seq_offsets, V,
                     dlogits, want, workspace)
+
+
+LMHEAD_CHUNK = 4096
+
+
+def _bf16_matrix(name, t, rows, dev):
+    if t.device != dev or t.dtype != torch.bfloat16 or t.dim() != 2 or t.stride(1) != 1 \
+            or t.shape[0] != rows:
+        raise ValueError(f"{name} must be a bf16 [{rows}, H] tensor on {dev} with unit column "
+                         "stride")
+    return t
+
+
+def _lmhead(bwd, hidden, weight, ids, logp_infer, adv, mask, prm, logp_old, seq_offsets, chunk,
+            dhidden, dweight, accumulate, want, workspace):
+    dev = hidden.device
+    T, H = hidden.shape
+    V = weight.shape[0]
+    _bf16_matrix("hidden", hidden, T, dev)
+    _bf16_matrix("weight", weight, V, dev)
+    if weight.shape[1] != H:
+        raise ValueError(f"weight must be [V, {H}], got {tuple(weight.shape)}")
+    _check_vec("ids", ids, T, torch.int64, dev)
+    _check_vec("logp_infer", logp_infer, T, torch.float32, dev)
+    _check_vec("adv", adv, T, torch.float32, dev)
+    _check_vec("logp_old", logp_old, T, torch.float32, dev, optional=True)
+    mask = _check_vec("mask", _mask_u8(mask), T, torch.uint8, dev, optional=True)
+    offs, n_seq = _offsets(seq_offsets, T, dev)
+    workspace = _workspace(workspace, lmhead_workspace_bytes(T, V, H, chunk, n_seq, bwd), dev)
+    out = {}
+    for k in want:
+        out[k] = torch.empty(T, dtype=torch.uint8 if k == "acted" else torch.float32, device=dev)
+    out["loss"] = torch.empty(1, dtype=torch.float32, device=dev)
+    lib = load_library()
+    with torch.cuda.device(dev):
+        head = (_ptr(hidden), T, H, hidden.stride(0), _ptr(weight), V, weight.stride(0),
+                _ptr(ids), _ptr(logp_infer), _ptr(logp_old), _ptr(adv), _ptr(mask), _ptr(offs),
+                n_seq, ctypes.byref(prm), int(chunk))
+        tail = (_ptr(out.get("logp_train")), _ptr(out.get("w")), _ptr(out.get("acted")),
+                _ptr(out.get("terms")), _ptr(out.get("eps")), _ptr(out["loss"]),
+                _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(dev))
+        if bwd:
+            if dhidden is None:
+                dhidden = torch.empty(T, H, dtype=torch.float32, device=dev)
+            if dweight is None:
+                dweight = torch.empty(V, H, dtype=torch.float32, device=dev)
+            for name, g, rows in (("dhidden", dhidden, T), ("dweight", dweight, V)):
+                if g.device != dev or g.dtype != torch.float32 or g.dim() != 2 \
+                        or g.shape[0] != rows or g.shape[1] < H or g.stride(1) != 1:
+                    raise ValueError(f"{name} must be a float32 [{rows}, >={H}] tensor on {dev}")
+            rc = lib.cis_lmhead_loss_bwd(*head, _ptr(dhidden), dhidden.stride(0), _ptr(dweight),
+                                         dweight.stride(0), int(bool(accumulate)), *tail)
+            fn = "cis_lmhead_loss_bwd"
+        else:
+            rc = lib.cis_lmhead_loss_fwd(*head, *tail)
+            fn = "cis_lmhead_loss_fwd"
+    if rc != 0:
+        raise CisError(fn, rc)
+    out["workspace"] = workspace
+    if bwd:
+        out["dhidden"] = dhidden
+        out["dweight"] = dweight
+    return out
+
+
+def lmhead_loss_fwd(hidden, weight, ids, logp_infer, adv, mask=None, *, params: Params,
+                    logp_old=None, seq_offsets=None, chunk=LMHEAD_CHUNK, want=_ALL_EX,
+                    workspace=None):
+    """The loss on the logits hidden @ weight^T without materialising them for the whole batch
+    (cis_lmhead_loss_fwd). hidden [T, H] and weight [V, H] are bf16. Keys as for
+    loss_fwd_ex."""
+    return _lmhead(False, hidden, weight, ids, logp_infer, adv, mask, params, logp_old,
+                   seq_offsets, chunk, None, None, False, want, workspace)
+
+
+def lmhead_loss_bwd(hidden, weight, ids, logp_infer, adv, mask=None, *, params: Params,
+                    logp_old=None, seq_offsets=None, chunk=LMHEAD_CHUNK, dhidden=None,
+                    dweight=None, accumulate=False, want=_ALL_EX, workspace=None):
+    """Forward and backward through the head (cis_lmhead_loss_bwd): lmhead_loss_fwd's keys plus
+    "dhidden" [T, H] and "dweight" [V, H], float32 (dweight accumulated into when
+    accumulate=True)."""
+    return _lmhead(True, hidden, weight, ids, logp_infer, adv, mask, params, logp_old,
+                   seq_offsets, chunk, dhidden, dweight, accumulate, want, workspace)

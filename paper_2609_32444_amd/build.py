@@ -14,12 +14,12 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB_PATH = os.path.join(HERE, "libcis.so")
 SOURCES = [os.path.join(HERE, "csrc", f) for f in
-           ("cis_kernels.hip", "cis_kernels_ext.hip", "cis_api.cpp")]
+           ("cis_kernels.hip", "cis_kernels_ext.hip", "cis_gemm.hip", "cis_api.cpp")]
 # bandwidth probes for the roofline (a separate library; not part of the loss)
 PROBE_PATH = os.path.join(HERE, "libcis_probe.so")
 PROBE_SOURCES = [os.path.join(HERE, "csrc", "bw_probe.hip")]
 HEADERS = [os.path.join(ROOT, "include", "cis.h"), os.path.join(HERE, "csrc", "cis_internal.h"),
-           os.path.join(HERE, "csrc", "cis_row.h")]
+           os.path.join(HERE, "csrc", "cis_row.h"), os.path.join(HERE, "csrc", "cis_gemm.h")]
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in device code (the compiler's host pass warns
 # that it does not know the feature; that warning is expected).

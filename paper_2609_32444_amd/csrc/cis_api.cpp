@@ -7,6 +7,7 @@
 
 #include <mutex>
 
+#include "cis_gemm.h"
 #include "cis_internal.h"
 
 namespace {
@@ -163,29 +164,120 @@ struct LossCall {
   size_t workspace_bytes;
 };
 
+// Parameter checks shared by every loss entry point.
+int check_loss_params(const LossCall& c) {
+  const bool decoupled = c.logp_old != nullptr;
+  if (c.ext) {
+    if (int rc = check_op_params(&c.prm, decoupled)) return rc;
+    if (is_seq_op(c.prm.op) && !decoupled) return CIS_ERR_PARAM;
+    if (is_seq_op(c.prm.op) && c.T > 0 && c.n_seq < 1) return CIS_ERR_SHAPE;
+  } else if (int rc = check_params(c.prm.lambda, c.prm.kappa, c.prm.scale)) {
+    return rc;
+  }
+  return CIS_OK;
+}
+
+int64_t seq_count(const LossCall& c) { return c.ext && is_seq_op(c.prm.op) ? c.n_seq : 0; }
+
+// Decoupled path: the weight depends only on (l_old, l_infer), so it is computed for all T rows
+// before any logits row is read.
+int launch_prepass(const LossCall& c, const Ws& ws, const DeviceInfo& info, hipStream_t stream) {
+  const int64_t n_seq = seq_count(c);
+  if (n_seq > 0) {
+    if (int rc = launch_seq_sum(c.logp_old, c.logp_infer, c.mask, c.ids, c.V, c.offsets, n_seq,
+                                c.T, ws, stream))
+      return rc;
+  }
+  cis::PrepassArgs pa{};
+  pa.logp_p = c.logp_old;
+  pa.logp_q = c.logp_infer;
+  pa.mask = c.mask;
+  pa.ids = c.ids;
+  pa.offsets = c.offsets;
+  pa.logK = reinterpret_cast<const double*>(ws.base + ws.L.logK);
+  pa.ops = op_args(c.prm);
+  pa.T = c.T;
+  pa.n_seq = n_seq;
+  pa.V = (int32_t)c.V;
+  pa.w_out = c.w_out;
+  pa.acted_out = c.acted_out;
+  pa.eps_out = c.eps_out;
+  pa.wpre_ws = ws.f(ws.L.wpre);
+  pa.pflags_ws = ws.b(ws.L.pflags);
+  pa.logk_ws = ws.f(ws.L.logk);
+  pa.excess_ws = ws.f(ws.L.excess);
+  return launch_grid_stride(cis::prepass_kernel(), c.T, cis::kWeightsBlock, info, &pa, stream);
+}
+
+template <class P>
+P* at(P* p, int64_t t0) { return p ? p + t0 : nullptr; }
+
+// The row kernel over rows [t0, t0 + rows) of the call: `logits` / `dlogits` point at the first
+// of those rows (row strides ld, ld_g elements of c.dtype); per-row arrays are indexed from t0.
+int launch_rows(const LossCall& c, const Ws& ws, const void* logits, void* dlogits, int64_t ld,
+                int64_t ld_g, int64_t t0, int64_t rows, int dev, const DeviceInfo& info,
+                hipStream_t stream) {
+  if (rows <= 0) return CIS_OK;
+  const int esize = c.dtype == CIS_BF16 ? 2 : 4;
+  const int32_t nvec = (int32_t)((c.V + 16 / esize - 1) / (16 / esize));
+  const cis::RowVariant& var = c.ext ? cis::select_row_variant_ext(c.dtype, c.bwd, nvec)
+                                     : cis::select_row_variant(c.dtype, c.bwd, nvec);
+  cis::RowArgs ra{};
+  ra.logits = logits;
+  ra.dlogits = dlogits;
+  ra.row_bytes = ld * esize;
+  ra.grow_bytes = c.bwd ? ld_g * esize : 0;
+  ra.ids = c.ids + t0;
+  ra.logp_infer = c.logp_infer + t0;
+  ra.adv = c.adv + t0;
+  ra.mask = at(c.mask, t0);
+  ra.logp_train_out = at(c.logp_train_out, t0);
+  ra.w_out = at(c.w_out, t0);
+  ra.trunc_out = at(c.acted_out, t0);
+  ra.terms_user = at(c.terms_out, t0);
+  ra.terms_ws = ws.f(ws.L.terms) + t0;
+  ra.flags_ws = ws.b(ws.L.flags) + t0;
+  ra.logk_ws = ws.f(ws.L.logk) + t0;
+  ra.excess_ws = ws.f(ws.L.excess) + t0;
+  ra.T = rows;
+  ra.V = (int32_t)c.V;
+  ra.nvec = nvec;
+  ra.lam = c.prm.lambda;
+  ra.kappa = c.prm.kappa;
+  ra.scale = c.prm.scale;
+  ra.ops = op_args(c.prm);
+  ra.logp_old = at(c.logp_old, t0);
+  ra.wpre_ws = ws.f(ws.L.wpre) + t0;
+  ra.pflags_ws = ws.b(ws.L.pflags) + t0;
+  ra.eps_out = at(c.eps_out, t0);
+  ra.clip_low = c.prm.clip_low;
+  ra.clip_high = c.prm.clip_high;
+  const int per_cu = blocks_per_cu(var.fn, var.block, dev);
+  const int64_t resident = (int64_t)per_cu * info.num_cu;
+  const int grid = (int)(rows < resident ? rows : resident);
+  return launch(var.fn, grid, var.block, &ra, stream);
+}
+
+int launch_finalize(const Ws& ws, int64_t T, float* loss_out, hipStream_t stream) {
+  cis::FinalizeArgs fa{ws.f(ws.L.terms), ws.b(ws.L.flags), ws.f(ws.L.logk), ws.f(ws.L.excess), T,
+                       ws.stats(), loss_out};
+  return launch(cis::finalize_kernel(), 1, cis::kFinalizeBlock, &fa, stream);
+}
+
 int run_loss(const LossCall& c, hipStream_t stream) {
   const bool bwd = c.bwd;
   const int64_t T = c.T, V = c.V;
   if (c.dtype != CIS_BF16 && c.dtype != CIS_F32) return CIS_ERR_DTYPE;
   if (T < 0 || V < 1 || c.ld < V || (bwd && c.ld_g < V) || c.n_seq < 0) return CIS_ERR_SHAPE;
   const int esize = c.dtype == CIS_BF16 ? 2 : 4;
-  const int epv = 16 / esize;
   if (V > kMaxV) return CIS_ERR_SHAPE;  // row byte offsets stay within 32 bits
   if (c.ld > INT64_MAX / esize || (bwd && c.ld_g > INT64_MAX / esize)) return CIS_ERR_SHAPE;
-  const bool decoupled = c.logp_old != nullptr;
-  if (c.ext) {
-    if (int rc = check_op_params(&c.prm, decoupled)) return rc;
-    if (is_seq_op(c.prm.op) && !decoupled) return CIS_ERR_PARAM;
-    if (is_seq_op(c.prm.op) && T > 0 && c.n_seq < 1) return CIS_ERR_SHAPE;
-  } else if (int rc = check_params(c.prm.lambda, c.prm.kappa, c.prm.scale)) {
-    return rc;
-  }
-  const bool seq = c.ext && is_seq_op(c.prm.op);
-  const int64_t n_seq = seq ? c.n_seq : 0;
+  if (int rc = check_loss_params(c)) return rc;
+  const int64_t n_seq = seq_count(c);
   if (!c.workspace) return CIS_ERR_NULL;
   if (T > 0 && (!c.logits || !c.ids || !c.logp_infer || !c.adv || (bwd && !c.dlogits)))
     return CIS_ERR_NULL;
-  if (seq && T > 0 && !c.offsets) return CIS_ERR_NULL;
+  if (n_seq > 0 && T > 0 && !c.offsets) return CIS_ERR_NULL;
   if (!aligned(c.workspace, 256)) return CIS_ERR_ALIGN;
   const cis::WsLayout L = cis::ws_layout(T, n_seq);
   if (c.workspace_bytes < L.total) return CIS_ERR_WORKSPACE;
@@ -208,76 +300,103 @@ int run_loss(const LossCall& c, hipStream_t stream) {
 
   const Ws ws{static_cast<char*>(c.workspace), L};
   if (T > 0) {
-    if (decoupled) {
-      // the weight depends only on (l_old, l_infer): one pass before the rows
-      if (seq) {
-        if (int rc = launch_seq_sum(c.logp_old, c.logp_infer, c.mask, c.ids, V, c.offsets, n_seq,
-                                    T, ws, stream))
-          return rc;
-      }
-      cis::PrepassArgs pa{};
-      pa.logp_p = c.logp_old;
-      pa.logp_q = c.logp_infer;
-      pa.mask = c.mask;
-      pa.ids = c.ids;
-      pa.offsets = c.offsets;
-      pa.logK = reinterpret_cast<const double*>(ws.base + L.logK);
-      pa.ops = op_args(c.prm);
-      pa.T = T;
-      pa.n_seq = n_seq;
-      pa.V = (int32_t)V;
-      pa.w_out = c.w_out;
-      pa.acted_out = c.acted_out;
-      pa.eps_out = c.eps_out;
-      pa.wpre_ws = ws.f(L.wpre);
-      pa.pflags_ws = ws.b(L.pflags);
-      pa.logk_ws = ws.f(L.logk);
-      pa.excess_ws = ws.f(L.excess);
-      if (int rc = launch_grid_stride(cis::prepass_kernel(), T, cis::kWeightsBlock, info, &pa,
-                                      stream))
-        return rc;
+    if (c.logp_old) {
+      if (int rc = launch_prepass(c, ws, info, stream)) return rc;
     }
-    const int32_t nvec = (int32_t)((V + epv - 1) / epv);
-    const cis::RowVariant& var = c.ext ? cis::select_row_variant_ext(c.dtype, bwd, nvec)
-                                       : cis::select_row_variant(c.dtype, bwd, nvec);
-    cis::RowArgs ra{};
-    ra.logits = c.logits;
-    ra.dlogits = c.dlogits;
-    ra.row_bytes = c.ld * esize;
-    ra.grow_bytes = bwd ? c.ld_g * esize : 0;
-    ra.ids = c.ids;
-    ra.logp_infer = c.logp_infer;
-    ra.adv = c.adv;
-    ra.mask = c.mask;
-    ra.logp_train_out = c.logp_train_out;
-    ra.w_out = c.w_out;
-    ra.trunc_out = c.acted_out;
-    ra.terms_user = c.terms_out;
-    ra.terms_ws = ws.f(L.terms);
-    ra.flags_ws = ws.b(L.flags);
-    ra.logk_ws = ws.f(L.logk);
-    ra.excess_ws = ws.f(L.excess);
-    ra.T = T;
-    ra.V = (int32_t)V;
-    ra.nvec = nvec;
-    ra.lam = c.prm.lambda;
-    ra.kappa = c.prm.kappa;
-    ra.scale = c.prm.scale;
-    ra.ops = op_args(c.prm);
-    ra.logp_old = c.logp_old;
-    ra.wpre_ws = ws.f(L.wpre);
-    ra.pflags_ws = ws.b(L.pflags);
-    ra.eps_out = c.eps_out;
-    ra.clip_low = c.prm.clip_low;
-    ra.clip_high = c.prm.clip_high;
-    const int per_cu = blocks_per_cu(var.fn, var.block, dev);
-    const int64_t resident = (int64_t)per_cu * info.num_cu;
-    const int grid = (int)(T < resident ? T : resident);
-    if (int rc = launch(var.fn, grid, var.block, &ra, stream)) return rc;
+    if (int rc = launch_rows(c, ws, c.logits, c.dlogits, c.ld, c.ld_g, 0, T, dev, info, stream))
+      return rc;
   }
-  cis::FinalizeArgs fa{ws.f(L.terms), ws.b(L.flags), ws.f(L.logk), ws.f(L.excess), T,
-                       ws.stats(), c.loss_out};
-  return launch(cis::finalize_kernel(), 1, cis::kFinalizeBlock, &fa, stream);
+  return launch_finalize(ws, T, c.loss_out, stream);
+}
+
+// The loss on the logits hidden * W^T, a chunk of rows at a time (cis_lmhead_loss_fwd/_bwd).
+struct LmHeadCall {
+  LossCall loss;            // logits / dlogits / ld unused; dtype is the chunk's (float32)
+  const void* hidden;       // [T, ld_h] bf16
+  const void* weight;       // [V, ld_w] bf16
+  int64_t H, ld_h, ld_w, chunk;
+  float* dhidden;           // [T, ld_dh] float32
+  float* dweight;           // [V, ld_dw] float32
+  int64_t ld_dh, ld_dw;
+  bool accumulate;
+};
+
+int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
+  const LossCall& c = m.loss;
+  const bool bwd = c.bwd;
+  const int64_t T = c.T, V = c.V, H = m.H;
+  if (T < 0 || V < 1 || V > kMaxV || H < 1 || c.n_seq < 0 || m.chunk < 1) return CIS_ERR_SHAPE;
+  if (m.ld_h < H || m.ld_w < H || (bwd && (m.ld_dh < H || m.ld_dw < H))) return CIS_ERR_SHAPE;
+  if (H > cis::kLmMaxH || m.chunk > cis::kLmMaxChunk) return CIS_ERR_SHAPE;
+  if (int rc = check_loss_params(c)) return rc;
+  const int64_t n_seq = seq_count(c);
+  if (!c.workspace || !m.weight) return CIS_ERR_NULL;
+  if (T > 0 && (!m.hidden || !c.ids || !c.logp_infer || !c.adv)) return CIS_ERR_NULL;
+  if (bwd && (!m.dweight || (T > 0 && !m.dhidden))) return CIS_ERR_NULL;
+  if (n_seq > 0 && T > 0 && !c.offsets) return CIS_ERR_NULL;
+  if (!aligned(c.workspace, 256)) return CIS_ERR_ALIGN;
+  if (!aligned(m.weight, 16) || m.ld_w % 8 != 0) return CIS_ERR_ALIGN;
+  if (T > 0 && (!aligned(m.hidden, 16) || m.ld_h % 8 != 0)) return CIS_ERR_ALIGN;
+  const cis::LmLayout LM = cis::lm_layout(T, V, H, m.chunk, n_seq, bwd);
+  if (c.workspace_bytes < LM.total) return CIS_ERR_WORKSPACE;
+  DeviceInfo info;
+  const int dev = current_device(&info);
+  if (dev < 0) return dev;
+
+  char* base = static_cast<char*>(c.workspace);
+  const Ws ws{base, LM.loss};
+  float* Z = reinterpret_cast<float*>(base + LM.z);
+  __bf16* Wt = reinterpret_cast<__bf16*>(base + LM.wt);
+  __bf16* Gt = reinterpret_cast<__bf16*>(base + LM.gt);
+  __bf16* Ht = reinterpret_cast<__bf16*>(base + LM.ht);
+  auto ok = [](hipError_t e) { return e == hipSuccess ? CIS_OK : CIS_ERR_LAUNCH; };
+  const __bf16* hid = static_cast<const __bf16*>(m.hidden);
+
+  if (bwd && T > 0) {  // W^T once: the operand of dL/dh = G W with V as the contracted axis
+    if (int rc = ok(cis::launch_transpose(
+            cis::TransposeArgs{m.weight, Wt, V, H, m.ld_w, LM.ldv}, false, stream)))
+      return rc;
+  }
+  if (T > 0 && c.logp_old) {
+    if (int rc = launch_prepass(c, ws, info, stream)) return rc;
+  }
+  for (int64_t t0 = 0; t0 < T; t0 += m.chunk) {
+    const int64_t tc = T - t0 < m.chunk ? T - t0 : m.chunk;
+    const __bf16* hc = hid + t0 * m.ld_h;
+    // Z = h_c W^T (float32 logits of the chunk)
+    if (int rc = ok(cis::launch_gemm_nt(
+            cis::GemmArgs{hc, m.weight, Z, tc, V, H, m.ld_h, m.ld_w, LM.ldz, 1.f, false}, false,
+            false, stream)))
+      return rc;
+    // loss rows; the backward overwrites Z with G = dL/dz in place
+    if (int rc = launch_rows(c, ws, Z, bwd ? Z : nullptr, LM.ldz, LM.ldz, t0, tc, dev, info,
+                             stream))
+      return rc;
+    if (!bwd) continue;
+    // dL/dh_c = G W = G (W^T)^T
+    if (int rc = ok(cis::launch_gemm_nt(cis::GemmArgs{Z, Wt, m.dhidden + t0 * m.ld_dh, tc, H, V,
+                                                      LM.ldz, LM.ldv, m.ld_dh, 1.f, false},
+                                        true, false, stream)))
+      return rc;
+    // dL/dW (+)= G^T h_c, contracted over the chunk's rows
+    if (int rc = ok(cis::launch_transpose(cis::TransposeArgs{Z, Gt, tc, V, LM.ldz, LM.ldc}, true,
+                                          stream)))
+      return rc;
+    if (int rc = ok(cis::launch_transpose(cis::TransposeArgs{hc, Ht, tc, H, m.ld_h, LM.ldc},
+                                          false, stream)))
+      return rc;
+    if (int rc = ok(cis::launch_gemm_nt(
+            cis::GemmArgs{Gt, Ht, m.dweight, V, H, tc, LM.ldc, LM.ldc, m.ld_dw, 1.f, false},
+            false, m.accumulate || t0 > 0, stream)))
+      return rc;
+  }
+  if (bwd && T == 0 && !m.accumulate) {  // no rows: dL/dW = 0 (an empty contraction)
+    if (int rc = ok(cis::launch_gemm_nt(
+            cis::GemmArgs{Wt, Wt, m.dweight, V, H, 0, 8, 8, m.ld_dw, 1.f, false}, false, false,
+            stream)))
+      return rc;
+  }
+  return launch_finalize(ws, T, c.loss_out, stream);
 }
 
 LossCall base_call(bool bwd, const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
@@ -329,9 +448,76 @@ LossCall ext_call(bool bwd, const void* logits, int dtype, int64_t T, int64_t V,
   return c;
 }
 
+LmHeadCall lm_call(bool bwd, const void* hidden, int64_t T, int64_t H, int64_t ld_h,
+                   const void* weight, int64_t V, int64_t ld_w, const int64_t* ids,
+                   const float* logp_infer, const float* logp_old, const float* adv,
+                   const uint8_t* mask, const int64_t* offsets, int64_t n_seq,
+                   const cis_params_t* params, int64_t chunk, float* dhidden, int64_t ld_dh,
+                   float* dweight, int64_t ld_dw, int accumulate, float* logp_train_out,
+                   float* w_out, uint8_t* acted_out, float* terms_out, float* eps_out,
+                   float* loss_out, void* workspace, size_t workspace_bytes) {
+  LmHeadCall m{};
+  m.loss = ext_call(bwd, nullptr, CIS_F32, T, V, 0, ids, logp_infer, logp_old, adv, mask, offsets,
+                    n_seq, params, nullptr, 0, logp_train_out, w_out, acted_out, terms_out,
+                    eps_out, loss_out, workspace, workspace_bytes);
+  m.hidden = hidden;
+  m.weight = weight;
+  m.H = H;
+  m.ld_h = ld_h;
+  m.ld_w = ld_w;
+  m.chunk = chunk;
+  m.dhidden = dhidden;
+  m.dweight = dweight;
+  m.ld_dh = ld_dh;
+  m.ld_dw = ld_dw;
+  m.accumulate = accumulate != 0;
+  return m;
+}
+
 }  // namespace
 
 extern "C" {
+
+size_t cis_lmhead_workspace_bytes(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_t n_seq,
+                                  int with_grad) {
+  if (T < 0 || V < 1 || H < 1 || chunk < 1 || n_seq < 0) return 0;
+  if (V > kMaxV || H > cis::kLmMaxH || chunk > cis::kLmMaxChunk) return 0;
+  return cis::lm_layout(T, V, H, chunk, n_seq, with_grad != 0).total;
+}
+
+int cis_lmhead_loss_fwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
+                        const void* weight, int64_t V, int64_t ld_w, const int64_t* ids,
+                        const float* logp_infer, const float* logp_old, const float* adv,
+                        const uint8_t* mask, const int64_t* seq_offsets, int64_t n_seq,
+                        const cis_params_t* params, int64_t chunk, float* logp_train_out,
+                        float* w_out, uint8_t* acted_out, float* loss_terms_out, float* eps_out,
+                        float* loss_out, void* workspace, size_t workspace_bytes,
+                        hipStream_t stream) {
+  if (!params) return CIS_ERR_NULL;
+  return run_lmhead(lm_call(false, hidden, T, H, ld_h, weight, V, ld_w, ids, logp_infer,
+                            logp_old, adv, mask, seq_offsets, n_seq, params, chunk, nullptr, 0,
+                            nullptr, 0, 0, logp_train_out, w_out, acted_out, loss_terms_out,
+                            eps_out, loss_out, workspace, workspace_bytes),
+                    stream);
+}
+
+int cis_lmhead_loss_bwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
+                        const void* weight, int64_t V, int64_t ld_w, const int64_t* ids,
+                        const float* logp_infer, const float* logp_old, const float* adv,
+                        const uint8_t* mask, const int64_t* seq_offsets, int64_t n_seq,
+                        const cis_params_t* params, int64_t chunk, float* dhidden,
+                        int64_t ld_dh, float* dweight, int64_t ld_dw, int accumulate_dweight,
+                        float* logp_train_out, float* w_out, uint8_t* acted_out,
+                        float* loss_terms_out, float* eps_out, float* loss_out, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+  if (!params) return CIS_ERR_NULL;
+  return run_lmhead(lm_call(true, hidden, T, H, ld_h, weight, V, ld_w, ids, logp_infer,
+                            logp_old, adv, mask, seq_offsets, n_seq, params, chunk, dhidden,
+                            ld_dh, dweight, ld_dw, accumulate_dweight, logp_train_out, w_out,
+                            acted_out, loss_terms_out, eps_out, loss_out, workspace,
+                            workspace_bytes),
+                    stream);
+}
 
 size_t cis_workspace_bytes(int64_t T) { return T < 0 ? 0 : cis::ws_bytes(T); }
 

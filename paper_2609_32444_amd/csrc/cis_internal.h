@@ -38,6 +38,41 @@ inline WsLayout ws_layout(int64_t T, int64_t n_seq) {
 }
 inline size_t ws_bytes(int64_t T) { return ws_layout(T, 0).total; }
 
+// LM-head workspace: the loss workspace above, then (256-byte aligned)
+//   Z   float[rows, ldz]   the chunk's logits; the backward overwrites them with dL/dz
+//   Wt  bf16[H, ldv]       W^T (backward)
+//   Gt  bf16[V, ldc]       (dL/dz)^T of the chunk (backward)
+//   Ht  bf16[H, ldc]       the chunk's hidden states transposed (backward)
+// with rows = min(T, chunk) and row strides rounded up to 8 elements.
+constexpr int64_t kLmMaxH = int64_t(1) << 16;
+constexpr int64_t kLmMaxChunk = int64_t(1) << 16;
+struct LmLayout {
+  WsLayout loss;
+  int64_t ldz, ldv, ldc;
+  size_t z, wt, gt, ht, total;
+};
+inline LmLayout lm_layout(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_t n_seq,
+                          bool bwd) {
+  LmLayout M;
+  M.loss = ws_layout(T, n_seq);
+  const int64_t rows = T < chunk ? T : chunk;
+  M.ldz = (V + 7) / 8 * 8;
+  M.ldv = M.ldz;
+  M.ldc = ((rows > 0 ? rows : 1) + 7) / 8 * 8;
+  M.z = align_up(M.loss.total, 256);
+  size_t end = M.z + align_up((size_t)rows * (size_t)M.ldz * 4, 256);
+  M.wt = M.gt = M.ht = end;
+  if (bwd) {
+    end += align_up((size_t)H * (size_t)M.ldv * 2, 256);
+    M.gt = end;
+    end += align_up((size_t)V * (size_t)M.ldc * 2, 256);
+    M.ht = end;
+    end += align_up((size_t)H * (size_t)M.ldc * 2, 256);
+  }
+  M.total = end;
+  return M;
+}
+
 // Per-row status bits (workspace flags[T]; kFlagTrunc = the operator acted on the row).
 enum : uint8_t { kFlagValid = 1, kFlagBadId = 2, kFlagNonFinite = 4, kFlagTrunc = 8 };
 

@@ -31,7 +31,8 @@ def test_library_exports_every_declared_symbol():
     names = declared_functions()
     assert set(names) == {"cis_workspace_bytes", "cis_workspace_bytes_ex", "cis_status_string",
                           "cis_weights", "cis_weights_ex", "cis_loss_fwd", "cis_loss_bwd",
-                          "cis_loss_fwd_ex", "cis_loss_bwd_ex"}
+                          "cis_loss_fwd_ex", "cis_loss_bwd_ex", "cis_lmhead_workspace_bytes",
+                          "cis_lmhead_loss_fwd", "cis_lmhead_loss_bwd"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -193,3 +194,64 @@ def test_weights_ex_argument_errors():
     assert call(_prm(), ws=FAKE + 8) == -5
     assert call(_prm(), wsb=16) == -7
     assert call(_prm()) == -9
+
+
+def test_lmhead_workspace_bytes():
+    f = cis.lmhead_workspace_bytes
+    T, V, H = 16384, 151936, 2048
+    fwd, bwd = f(T, V, H, 4096, 0, False), f(T, V, H, 4096, 0, True)
+    loss = cis.workspace_bytes_ex(T, 0)
+    # the loss workspace plus one float32 chunk of logits; the backward adds W^T and the two
+    # transposed chunk operands
+    assert fwd >= loss + 4 * 4096 * V and fwd % 256 == 0
+    assert bwd >= fwd + 2 * V * H + 2 * (V + H) * 4096
+    # a chunk larger than the batch only needs the batch's rows
+    assert f(100, 1000, 64, 4096, 0, True) == f(100, 1000, 64, 100, 0, True)
+    assert f(T, V, H, 4096, 10, True) >= bwd
+    for bad in ((-1, V, H, 1), (T, 0, H, 1), (T, V, 0, 1), (T, V, H, 0), (T, 1 << 29, H, 1),
+                (T, V, 1 << 17, 1), (T, V, H, 1 << 17)):
+        assert f(*bad, 0, True) == 0, bad
+    assert f(T, V, H, 64, -1, True) == 0
+
+
+def _lm(bwd=True, **kw):
+    a = dict(hidden=FAKE, T=4, H=64, ld_h=64, weight=FAKE, V=1000, ld_w=64, ids=FAKE, linf=FAKE,
+             lold=NULL, adv=FAKE, mask=NULL, offs=NULL, nseq=0, prm=_prm(), chunk=4096,
+             dh=FAKE, ld_dh=64, dw=FAKE, ld_dw=64, ws=FAKE, wsb=1 << 30)
+    a.update(kw)
+    pp = ctypes.byref(a["prm"]) if a["prm"] is not None else None
+    lib = cis.load_library()
+    head = (a["hidden"], a["T"], a["H"], a["ld_h"], a["weight"], a["V"], a["ld_w"], a["ids"],
+            a["linf"], a["lold"], a["adv"], a["mask"], a["offs"], a["nseq"], pp, a["chunk"])
+    tail = (NULL, NULL, NULL, NULL, NULL, NULL, a["ws"], a["wsb"], NULL)
+    if bwd:
+        return lib.cis_lmhead_loss_bwd(*head, a["dh"], a["ld_dh"], a["dw"], a["ld_dw"], 0, *tail)
+    return lib.cis_lmhead_loss_fwd(*head, *tail)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(prm=None), -1), (dict(hidden=NULL), -1), (dict(weight=NULL), -1), (dict(ids=NULL), -1),
+    (dict(dh=NULL), -1), (dict(dw=NULL), -1), (dict(ws=NULL), -1),
+    (dict(T=-1), -2), (dict(V=0), -2), (dict(H=0), -2), (dict(ld_h=32), -2),
+    (dict(ld_w=32), -2), (dict(ld_dh=32), -2), (dict(ld_dw=32), -2), (dict(chunk=0), -2),
+    (dict(chunk=1 << 17), -2), (dict(H=1 << 17, ld_h=1 << 17, ld_w=1 << 17), -2),
+    (dict(ld_h=68, H=60), -5), (dict(ld_w=68, H=60), -5), (dict(hidden=FAKE + 8), -5),
+    (dict(weight=FAKE + 8), -5), (dict(ws=FAKE + 16), -5), (dict(wsb=1000), -7),
+    (dict(prm=None), -1), (dict(lold=FAKE, prm=None), -1),
+])
+def test_lmhead_argument_errors(kw, code):
+    assert _lm(True, **kw) == code
+
+
+def test_lmhead_fwd_needs_no_gradient_buffers():
+    # the forward ignores dhidden / dweight; valid arguments reach the device check
+    assert _lm(False, dh=NULL, dw=NULL) == -9
+    assert _lm(True) == -9
+    # no rows: hidden and the per-row arrays may be NULL, dweight is still written
+    assert _lm(True, T=0, hidden=NULL, ids=NULL, linf=NULL, adv=NULL, dh=NULL) == -9
+    assert _lm(True, T=0, dw=NULL) == -1
+    # H not a multiple of 8 with a padded row stride is fine
+    assert _lm(True, H=60, ld_h=64, ld_w=64) == -9
+    # a sequence operator needs logp_old and responses
+    assert _lm(True, prm=_prm(op=8, hi=2.0)) == -4
+    assert _lm(True, prm=_prm(op=8, hi=2.0), lold=FAKE, nseq=2, offs=FAKE) == -9

@@ -1,0 +1,317 @@
+"""The loss behind the LM head on the GPU (cis_lmhead_loss_fwd / _bwd) against oracle.lmhead.
+
+Inputs come from workloads.make_lmhead_batch, whose hidden states and head weight make every
+float32 partial sum of h W^T exact: the chunk's float32 logits equal the oracle's float64 ones,
+so the per-row outputs, the loss and the diagnostics take the tolerances of tests/parity.py and
+tests/parity_ops.py unchanged.
+
+Gradients. The kernel rounds G = dL/dz (float32, within 2e-5 |G| + 2^-126 of the float64 G) to
+bf16 as the operand of dL/dh = G W and dL/dW = G^T h, and accumulates in float32. Per element
+of dL/dh (dL/dW likewise with |G|^T |h|):
+
+    |gpu - ref| <= (2^-8 + 4e-5 + (8 sqrt(K) + n_add) 2^-24) (|G| |W|) + 1e-30
+
+2^-8 is the unit roundoff of bf16 (8-bit significand, round to nearest even), 4e-5 covers the
+float32 G, K is the contracted length (V for dL/dh, the chunk's rows for dL/dW) and n_add the
+float32 additions of whole partial results (1 for dL/dh; the number of chunks for dL/dW, which
+is accumulated chunk by chunk). The accumulation term is the probabilistic bound of blocked
+float32 summation (sqrt(K) u with a factor of 8) rather than the worst case K u, which at
+K = 151936 would allow 0.9% and test nothing.
+"""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_32444_amd as cis
+from oracle import lmhead as L
+from oracle import ops as X
+from tests import parity as P
+from tests import parity_ops as PO
+from workloads import make_lmhead_batch
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+OUT = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "gpurun_out")
+U32 = 2.0 ** -24
+U16 = 2.0 ** -8
+
+
+def f32(x):
+    return float(np.float32(x))
+
+
+def make_params(op, kw, scale, clip=(0.2, 0.28)):
+    base = dict(lam=2.3, kappa=5e-3, lo=0.0, hi=math.inf)
+    base.update(kw)
+    dev = cis.params(op, lam=base["lam"], kappa=base["kappa"], lo=base["lo"], hi=base["hi"],
+                     clip_low=clip[0], clip_high=clip[1], scale=scale)
+    ref = X.OpParams(op=op, lam=f32(base["lam"]), kappa=f32(base["kappa"]), lo=f32(base["lo"]),
+                     hi=f32(base["hi"]), clip_low=f32(clip[0]), clip_high=f32(clip[1]),
+                     scale=f32(scale))
+    return dev, ref
+
+
+def host(b):
+    return (b.hidden.float().cpu().double().numpy(), b.weight.float().cpu().double().numpy())
+
+
+def _dump(name, rep):
+    os.makedirs(OUT, exist_ok=True)
+    with open(os.path.join(OUT, f"parity_lmhead_{name}.json"), "w") as f:
+        json.dump({k: v for k, v in rep.items() if not k.startswith("_")}, f, default=str)
+
+
+def grad_bound(Gabs_B, K, n_add):
+    return (U16 + 4e-5 + (8.0 * math.sqrt(max(K, 1)) + n_add) * U32) * Gabs_B + 1e-30
+
+
+def check_grad(name, gpu, ref, bound, rows_ok=None):
+    err = np.abs(gpu - ref)
+    if rows_ok is not None:
+        err, ref, bound = err[rows_ok], ref[rows_ok], bound[rows_ok]
+    bad = err > bound
+    rel = np.linalg.norm(err) / max(np.linalg.norm(ref), 1e-300)
+    if bad.any():
+        i = np.unravel_index(int(np.argmax(err - bound)), err.shape)
+        raise AssertionError(f"{name}: {int(bad.sum())} elements out of tolerance; worst at {i}: "
+                             f"err {err[i]:.3g} bound {bound[i]:.3g} ref {ref[i]:.3g}")
+    return {"max_err_over_bound": float(np.max(err / bound)) if err.size else 0.0,
+            "rel_fro": float(rel)}
+
+
+def ref_dict(res):
+    return {"rows": np.arange(len(res.w)), "flags": res.flags, "logp_train": res.logp_train,
+            "w": res.w, "term": res.term, "eps": res.eps, "logk": res.logk, "acted": res.acted,
+            "rho": res.rho, "gate": res.gate}
+
+
+def run_case(name, b, op=X.OP_CIS, kw=None, chunk=4096, decoupled=False, seq=False, bwd=True):
+    kw = dict(lam=b.lam, kappa=b.kappa) if kw is None and op == X.OP_CIS else (kw or {})
+    prm_dev, prm_ref = make_params(op, kw, b.scale)
+    lold = b.logp_old if decoupled else None
+    offs = b.offsets if seq else None
+    fn = cis.lmhead_loss_bwd if bwd else cis.lmhead_loss_fwd
+    out = fn(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask, params=prm_dev,
+             logp_old=lold, seq_offsets=offs, chunk=chunk)
+    torch.cuda.synchronize()
+    h, W = host(b)
+    res = L.lmhead_cis_loss(h, W, b.ids.cpu().numpy(), b.logp_infer.cpu().double().numpy(),
+                            b.adv.cpu().double().numpy(), b.mask.cpu().numpy(), prm_ref,
+                            logp_old=None if lold is None else lold.cpu().double().numpy(),
+                            offsets=None if offs is None else offs.cpu().numpy(),
+                            with_grad=bwd, keep_grad=bwd)
+    rep = {"case": name, "T": b.T, "V": b.V, "H": b.H, "chunk": chunk}
+    ref = ref_dict(res)
+    PO.compare_ops(out, ref, b, prm_ref, rep, logp_old=lold, offsets=offs)
+    differ = rep.pop("_differ")
+    stats = cis.read_stats(out["workspace"])
+    PO.check_diagnostics(stats, ref, differ, rep)
+    assert stats["n_valid"] == int(np.sum((res.flags & 1) > 0))
+    if bwd:
+        # rows whose acted flag or PPO gate may legitimately differ leave the gradient checks
+        assert not differ.any(), "margin rows in a gradient case: pick another seed"
+        if lold is not None:
+            hi_c, lo_c = 1.0 + prm_ref.clip_high, 1.0 - prm_ref.clip_low
+            near = (np.abs(res.rho - hi_c) <= 1e-5 * hi_c) | (np.abs(res.rho - lo_c) <= 1e-5 * lo_c)
+            assert not near[(res.flags & 1) > 0].any(), "rows at the PPO clip edge: other seed"
+        G = np.abs(res.grad)
+        nch = (b.T + chunk - 1) // chunk
+        dh = out["dhidden"].cpu().double().numpy()
+        dW = out["dweight"].cpu().double().numpy()
+        rep["dhidden"] = check_grad("dhidden", dh, res.dhidden, grad_bound(G @ np.abs(W), b.V, 1))
+        rep["dweight"] = check_grad("dweight", dW, res.dW,
+                                    grad_bound(G.T @ np.abs(h), min(chunk, b.T), nch))
+        inval = (res.flags & 1) == 0
+        assert np.all(dh[inval] == 0), "dhidden rows of invalid tokens must be zero"
+    _dump(name, rep)
+    return out, res
+
+
+SMALL = [
+    # name, T, V, H, chunk, extra generator arguments
+    ("one_chunk", 64, 1000, 64, 4096, {}),
+    ("chunks_ragged", 300, 9001, 136, 128, {}),
+    ("padded_H100", 200, 2053, 100, 64, dict(ld_h=104, ld_w=112)),
+    ("masked", 257, 4099, 72, 128, dict(mask_p=0.7)),
+    ("one_row", 1, 517, 2048, 4096, {}),
+    ("vocab_1", 5, 1, 8, 4096, {}),
+]
+
+
+@pytest.mark.parametrize("name,T,V,H,chunk,gen", SMALL, ids=[c[0] for c in SMALL])
+def test_lmhead_parity_small(name, T, V, H, chunk, gen):
+    b = make_lmhead_batch(T, V, H, device=DEV, seed=11, min_len=16, max_len=96, **gen)
+    run_case(name, b, chunk=chunk)
+
+
+def test_lmhead_forward_matches_backward_and_chunking():
+    b = make_lmhead_batch(300, 9001, 136, device=DEV, seed=5, min_len=16, max_len=96)
+    prm, _ = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
+    args = (b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask)
+    a = cis.lmhead_loss_bwd(*args, params=prm, chunk=128)
+    c = cis.lmhead_loss_bwd(*args, params=prm, chunk=4096)
+    f = cis.lmhead_loss_fwd(*args, params=prm, chunk=256)
+    torch.cuda.synchronize()
+    # chunks that are multiples of the 128-row tile give the same logits and per-row results
+    for k in ("logp_train", "w", "acted", "terms", "eps", "loss"):
+        assert torch.equal(a[k], c[k]), k
+    assert torch.equal(a["dhidden"], c["dhidden"])
+    # the forward-only kernel may sum a row in another order: float32 rounding apart
+    for k in ("logp_train", "w", "terms"):
+        assert torch.allclose(a[k], f[k], rtol=1e-5, atol=2e-6), k
+    assert torch.equal(a["acted"], f["acted"])
+    # dL/dW is summed chunk by chunk: equal up to float32 rounding of the partial sums
+    rel = (a["dweight"] - c["dweight"]).abs().max() / c["dweight"].abs().max()
+    assert rel.item() < 1e-5
+
+
+TOKEN_OPS = [("icepop", X.OP_ICEPOP, dict(lo=0.5, hi=5.0)), ("tis", X.OP_TIS, dict(hi=2.0)),
+             ("kpop", X.OP_KPOP, dict(hi=2.0)), ("two_sided", X.OP_TWO_SIDED, {})]
+
+
+@pytest.mark.parametrize("name,op,kw", TOKEN_OPS, ids=[o[0] for o in TOKEN_OPS])
+def test_lmhead_operators(name, op, kw):
+    b = make_lmhead_batch(200, 3001, 64, device=DEV, seed=21, min_len=16, max_len=96,
+                          delta_sd=0.5)
+    run_case(f"op_{name}", b, op=op, kw=kw, chunk=128)
+
+
+@pytest.mark.parametrize("name,op,kw,seq", [
+    ("ppo_cis", X.OP_CIS, dict(lam=math.e - 1, kappa=5e-3), False),
+    ("ppo_icepop", X.OP_ICEPOP, dict(lo=0.5, hi=5.0), False),
+    ("ppo_seq_tis", X.OP_SEQ_TIS, dict(hi=2.0), True),
+])
+def test_lmhead_decoupled(name, op, kw, seq):
+    b = make_lmhead_batch(300, 2001, 64, device=DEV, seed=31, min_len=16, max_len=80,
+                          delta_sd=0.3, old_sd=0.2)
+    run_case(name, b, op=op, kw=kw, chunk=128, decoupled=True, seq=seq)
+
+
+def test_lmhead_forward_only_parity():
+    b = make_lmhead_batch(150, 5003, 96, device=DEV, seed=41, min_len=16, max_len=96)
+    run_case("fwd_only", b, chunk=64, bwd=False)
+
+
+def test_lmhead_empty_batch_and_accumulation():
+    b = make_lmhead_batch(96, 1000, 64, device=DEV, seed=51, min_len=16, max_len=48)
+    prm, _ = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
+    e = torch.empty(0, device=DEV)
+    ei = torch.empty(0, dtype=torch.int64, device=DEV)
+    h0 = b.hidden[:0]
+    dW = torch.full((1000, 64), 3.0, device=DEV)
+    out = cis.lmhead_loss_bwd(h0, b.weight, ei, e, e, None, params=prm, dweight=dW,
+                              accumulate=True)
+    torch.cuda.synchronize()
+    assert torch.all(out["dweight"] == 3.0)
+    out = cis.lmhead_loss_bwd(h0, b.weight, ei, e, e, None, params=prm, dweight=dW)
+    torch.cuda.synchronize()
+    assert torch.all(out["dweight"] == 0.0) and float(out["loss"].item()) == 0.0
+    # accumulate: dW0 + the gradient, summed onto dW0 chunk by chunk (3 chunks)
+    args = (b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask)
+    dW0 = torch.randn(1000, 64, device=DEV) * 1e-3
+    acc = cis.lmhead_loss_bwd(*args, params=prm, chunk=32, dweight=dW0.clone(),
+                              accumulate=True)["dweight"]
+    torch.cuda.synchronize()
+    _, prm_ref = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
+    h, W = host(b)
+    res = L.lmhead_cis_loss(h, W, b.ids.cpu().numpy(), b.logp_infer.cpu().double().numpy(),
+                            b.adv.cpu().double().numpy(), b.mask.cpu().numpy(), prm_ref,
+                            keep_grad=True)
+    d0 = dW0.cpu().double().numpy()
+    bound = grad_bound(np.abs(res.grad).T @ np.abs(h), 32, 3) + 4 * U32 * np.abs(d0)
+    check_grad("dweight_accumulated", acc.cpu().double().numpy(), d0 + res.dW, bound)
+
+
+# ------------------------------------------------------------------------------------------
+# the full LM-head workload in the configuration the benchmark times
+# ------------------------------------------------------------------------------------------
+FULL_T, FULL_V, FULL_H, FULL_CHUNK = 16384, 151936, 2048, cis.LMHEAD_CHUNK
+
+
+def test_lmhead_full_size_sampled():
+    """T = 16384, V = 151936, H = 2048 in chunks of 4096 rows: sampled rows against the oracle
+    (per-row outputs and dL/dh rows), and for dL/dW the properties that hold at any size:
+    <dW, W> = sum_t <dh_t, h_t> (both are sum_t <G_t, z_t> for the same bf16 G), and each
+    column of dW sums to sum_t (sum_v G_tv) h_t with sum_v G_tv = 0 up to G's bf16 rounding."""
+    b = make_lmhead_batch(FULL_T, FULL_V, FULL_H, device=DEV, seed=2, c=1.0)
+    prm_dev, prm_ref = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
+    out = cis.lmhead_loss_bwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
+                              params=prm_dev, chunk=FULL_CHUNK)
+    torch.cuda.synchronize()
+    stats = cis.read_stats(out["workspace"])
+    assert stats["n_valid"] == FULL_T and stats["n_bad_id"] == 0 and stats["n_nonfinite"] == 0
+    terms = out["terms"].double()
+    assert abs(stats["loss"] - float(terms.sum())) <= 1e-9 * float(terms.abs().sum())
+    g = torch.Generator().manual_seed(3)
+    rows = sorted(set(torch.randint(0, FULL_T, (6,), generator=g).tolist()) | {0, FULL_T - 1})
+    h, W = host(b)
+    res = L.lmhead_cis_loss(h[rows], W, b.ids.cpu().numpy()[rows],
+                            b.logp_infer.cpu().double().numpy()[rows],
+                            b.adv.cpu().double().numpy()[rows], b.mask.cpu().numpy()[rows],
+                            prm_ref, keep_grad=True)
+    rep = {"case": "full_size", "rows": rows}
+    for k, kk in (("logp_train", "logp_train"), ("w", "w"), ("terms", "term")):
+        dev = out[k].cpu().double().numpy()[rows]
+        ref = getattr(res, kk)
+        assert np.all(np.abs(dev - ref) <= 1e-5 * np.abs(ref) + 2e-6), (k, dev, ref)
+    dh = out["dhidden"].cpu().double().numpy()
+    rep["dhidden_rows"] = check_grad("dhidden", dh[rows], res.dhidden,
+                                     grad_bound(np.abs(res.grad) @ np.abs(W), FULL_V, 1))
+    # dW properties; |G_tv| <= |c_t| (1{v = y} + p_tv) bounds sum_v |G_tv| S_tv by
+    # 2 |c_t| max_v S_tv <= 2 |c_t| ||h_t||_1 max|W|
+    dW = out["dweight"].double()
+    hd = b.hidden.double()
+    Wd = b.weight.double()
+    c = (b.scale * out["w"].double() * b.adv.double()).abs()
+    lhs = float((dW * Wd).sum())
+    rhs = float((out["dhidden"].double() * hd).sum())
+    nch = FULL_T // FULL_CHUNK
+    gam = (8 * math.sqrt(FULL_V) + 8 * math.sqrt(FULL_CHUNK) + nch + 2) * U32
+    bound = gam * 2 * float((c * hd.abs().sum(1)).sum()) * float(Wd.abs().max())
+    assert abs(lhs - rhs) <= bound, (lhs, rhs, bound)
+    col = dW.sum(0)
+    cbound = (2 * U16 + gam) * 2 * (c[:, None] * hd.abs()).sum(0) + 1e-30
+    assert torch.all(col.abs() <= cbound)
+    rep.update(trace_lhs=lhs, trace_rhs=rhs, trace_bound=bound,
+               colsum_max_over_bound=float((col.abs() / cbound).max()))
+    _dump("full_size", rep)
+
+
+def test_lmhead_full_size_few_valid_rows_dweight():
+    """The same configuration with only a few valid rows: dL/dW is then a sum over those rows,
+    which the oracle forms exactly; compared on sampled vocabulary rows (the sampled ids
+    included)."""
+    b = make_lmhead_batch(FULL_T, FULL_V, FULL_H, device=DEV, seed=4, c=1.0)
+    keep = torch.tensor([3, 5000, 9001, FULL_T - 2], device=DEV)
+    b.mask.zero_()
+    b.mask[keep] = 1
+    b.scale = -1.0 / 4
+    prm_dev, prm_ref = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
+    out = cis.lmhead_loss_bwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
+                              params=prm_dev, chunk=FULL_CHUNK)
+    torch.cuda.synchronize()
+    rows = keep.cpu().numpy()
+    h, W = host(b)
+    res = L.lmhead_cis_loss(h[rows], W, b.ids.cpu().numpy()[rows],
+                            b.logp_infer.cpu().double().numpy()[rows],
+                            b.adv.cpu().double().numpy()[rows], None, prm_ref, keep_grad=True)
+    g = torch.Generator().manual_seed(9)
+    vs = sorted(set(torch.randint(0, FULL_V, (60,), generator=g).tolist())
+                | set(b.ids.cpu().numpy()[rows].tolist()) | {0, FULL_V - 1})
+    dW = out["dweight"][vs].cpu().double().numpy()
+    G = np.abs(res.grad)
+    bound = grad_bound(G[:, vs].T @ np.abs(h[rows]), FULL_CHUNK, FULL_T // FULL_CHUNK)
+    rep = {"case": "full_size_few_valid", "dweight_rows": check_grad("dweight", dW, res.dW[vs],
+                                                                      bound)}
+    dh = out["dhidden"].cpu().double().numpy()
+    others = np.ones(FULL_T, dtype=bool)
+    others[rows] = False
+    assert np.all(dh[others] == 0)
+    rep["dhidden_rows"] = check_grad("dhidden", dh[rows], res.dhidden,
+                                     grad_bound(G @ np.abs(W), FULL_V, 1))
+    _dump("full_size_few_valid", rep)
