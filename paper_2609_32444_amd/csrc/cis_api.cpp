@@ -349,12 +349,15 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
   __bf16* Wt = reinterpret_cast<__bf16*>(base + LM.wt);
   __bf16* Gt = reinterpret_cast<__bf16*>(base + LM.gt);
   __bf16* Ht = reinterpret_cast<__bf16*>(base + LM.ht);
+  __bf16* Gb = reinterpret_cast<__bf16*>(base + LM.gb);
+  float* part = reinterpret_cast<float*>(base + LM.part);
   auto ok = [](hipError_t e) { return e == hipSuccess ? CIS_OK : CIS_ERR_LAUNCH; };
   const __bf16* hid = static_cast<const __bf16*>(m.hidden);
+  const int ncu = info.num_cu;
 
   if (bwd && T > 0) {  // W^T once: the operand of dL/dh = G W with V as the contracted axis
     if (int rc = ok(cis::launch_transpose(
-            cis::TransposeArgs{m.weight, Wt, V, H, m.ld_w, LM.ldv}, false, stream)))
+            cis::TransposeArgs{m.weight, Wt, nullptr, V, H, m.ld_w, LM.ldv, 0}, false, stream)))
       return rc;
   }
   if (T > 0 && c.logp_old) {
@@ -365,34 +368,35 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
     const __bf16* hc = hid + t0 * m.ld_h;
     // Z = h_c W^T (float32 logits of the chunk)
     if (int rc = ok(cis::launch_gemm_nt(
-            cis::GemmArgs{hc, m.weight, Z, tc, V, H, m.ld_h, m.ld_w, LM.ldz, 1.f, false}, false,
-            false, stream)))
+            cis::gemm_args(hc, m.weight, Z, tc, V, H, m.ld_h, m.ld_w, LM.ldz), false, nullptr,
+            ncu, stream)))
       return rc;
     // loss rows; the backward overwrites Z with G = dL/dz in place
     if (int rc = launch_rows(c, ws, Z, bwd ? Z : nullptr, LM.ldz, LM.ldz, t0, tc, dev, info,
                              stream))
       return rc;
     if (!bwd) continue;
+    // G in bf16, row-major (operand of dL/dh) and transposed (operand of dL/dW); h_c^T
+    if (int rc = ok(cis::launch_transpose(
+            cis::TransposeArgs{Z, Gt, Gb, tc, V, LM.ldz, LM.ldc, LM.ldv}, true, stream)))
+      return rc;
+    if (int rc = ok(cis::launch_transpose(
+            cis::TransposeArgs{hc, Ht, nullptr, tc, H, m.ld_h, LM.ldc, 0}, false, stream)))
+      return rc;
     // dL/dh_c = G W = G (W^T)^T
-    if (int rc = ok(cis::launch_gemm_nt(cis::GemmArgs{Z, Wt, m.dhidden + t0 * m.ld_dh, tc, H, V,
-                                                      LM.ldz, LM.ldv, m.ld_dh, 1.f, false},
-                                        true, false, stream)))
+    if (int rc = ok(cis::launch_gemm_nt(
+            cis::gemm_args(Gb, Wt, m.dhidden + t0 * m.ld_dh, tc, H, V, LM.ldv, LM.ldv, m.ld_dh),
+            false, part, ncu, stream)))
       return rc;
     // dL/dW (+)= G^T h_c, contracted over the chunk's rows
-    if (int rc = ok(cis::launch_transpose(cis::TransposeArgs{Z, Gt, tc, V, LM.ldz, LM.ldc}, true,
-                                          stream)))
-      return rc;
-    if (int rc = ok(cis::launch_transpose(cis::TransposeArgs{hc, Ht, tc, H, m.ld_h, LM.ldc},
-                                          false, stream)))
-      return rc;
     if (int rc = ok(cis::launch_gemm_nt(
-            cis::GemmArgs{Gt, Ht, m.dweight, V, H, tc, LM.ldc, LM.ldc, m.ld_dw, 1.f, false},
-            false, m.accumulate || t0 > 0, stream)))
+            cis::gemm_args(Gt, Ht, m.dweight, V, H, tc, LM.ldc, LM.ldc, m.ld_dw),
+            m.accumulate || t0 > 0, nullptr, ncu, stream)))
       return rc;
   }
   if (bwd && T == 0 && !m.accumulate) {  // no rows: dL/dW = 0 (an empty contraction)
     if (int rc = ok(cis::launch_gemm_nt(
-            cis::GemmArgs{Wt, Wt, m.dweight, V, H, 0, 8, 8, m.ld_dw, 1.f, false}, false, false,
+            cis::gemm_args(Wt, Wt, m.dweight, V, H, 0, 8, 8, m.ld_dw), false, nullptr, ncu,
             stream)))
       return rc;
   }

@@ -7,31 +7,61 @@
 namespace cis {
 
 // C[M, N] (float32, row stride ldc) = alpha * A[M, K] * B[N, K]^T (+ C when accumulating).
-// A is float32 or bf16 (converted to bf16 on load, round to nearest even), B is bf16; both
-// row-major with K contiguous (row strides lda, ldb, multiples of 8 elements; bases 16-byte
-// aligned). Any M, N, K >= 0.
+// A and B are bf16, row-major with K contiguous (row strides lda, ldb: multiples of 8 elements,
+// bases 16-byte aligned). Any M, N, K >= 0. The last four fields are set by launch_gemm_nt.
 struct GemmArgs {
   const void* A;
   const void* B;
   float* C;
   int64_t M, N, K, lda, ldb, ldc;
   float alpha;
-  bool m_fastest;   // set by launch_gemm_nt
+  bool m_fastest;           // tile order: M tiles fastest
+  bool c_vec;               // C rows and base allow 16-byte stores
+  int64_t k_split;          // contraction length per split
+  int64_t c_split_stride;   // elements between the splits' partial outputs
 };
 
-// out[c][r] = bf16(in[r][c]), in R x C (float32 or bf16, row stride ldi), out C x R (ldo).
+inline GemmArgs gemm_args(const void* A, const void* B, float* C, int64_t M, int64_t N,
+                          int64_t K, int64_t lda, int64_t ldb, int64_t ldc) {
+  GemmArgs g{};
+  g.A = A;
+  g.B = B;
+  g.C = C;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.lda = lda;
+  g.ldb = ldb;
+  g.ldc = ldc;
+  g.alpha = 1.f;
+  return g;
+}
+
+// out[c][r] = bf16(in[r][c]), in R x C (float32 or bf16, row stride ldi), out C x R (ldo);
+// out_n (nullable) receives bf16(in) in the input's layout (row stride ldn). Row strides are
+// multiples of 4 elements and bases 16-byte aligned.
 struct TransposeArgs {
   const void* in;
   void* out;
-  int64_t R, C, ldi, ldo;
+  void* out_n;
+  int64_t R, C, ldi, ldo, ldn;
 };
 
-constexpr int kGemmTile = 128;   // C tile per workgroup (rows and columns)
-constexpr int kGemmThreads = 256;
+constexpr int kGemmTile = 256;      // C tile per workgroup (rows and columns)
+constexpr int kGemmBK = 64;         // contraction slab
+constexpr int kGemmWaveM = 128;     // C tile per wave: 128 rows x 64 columns (8 waves)
+constexpr int kGemmWaveN = 64;
+constexpr int kGemmMaxSplits = 8;   // split-K partial buffers
 constexpr int kTransposeTile = 64;
 
-// Launch on `stream`; `beta` adds the product to C instead of overwriting it.
-hipError_t launch_gemm_nt(GemmArgs g, bool a_f32, bool beta, hipStream_t stream);
+// Number of K splits launch_gemm_nt uses for an M x N x K product when given a partial buffer
+// (enough workgroups for every CU; 1 when the tiles already cover the chip).
+int64_t gemm_splitk_count(int64_t M, int64_t N, int64_t K, int num_cu);
+
+// Launch on `stream`; `beta` adds the product to C instead of overwriting it. With `partial`
+// (float32, >= gemm_splitk_count(...) * M * N elements, 16-byte aligned) small products are
+// split along K and the partials summed in a fixed order.
+hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int num_cu, hipStream_t stream);
 hipError_t launch_transpose(TransposeArgs t, bool in_f32, hipStream_t stream);
 
 }  // namespace cis

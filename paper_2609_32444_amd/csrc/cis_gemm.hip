@@ -1,197 +1,360 @@
 // Dense products of the LM-head form (gfx950 MFMA): C = alpha * A * B^T (+ C), both operands
-// K-contiguous, bf16 multiplies with float32 accumulation, and a tiled transpose that also
-// converts to bf16. Used for the logits of a row chunk (hidden * W^T), the gradient with respect
-// to the hidden states (G * W) and the gradient of the head weight (G^T * hidden).
+// bf16 and K-contiguous, float32 accumulation; and a tiled transpose that converts to bf16. Used
+// for the logits of a row chunk (hidden * W^T), the gradient with respect to the hidden states
+// (G * W) and the gradient of the head weight (G^T * hidden).
 //
-// Tiling: a 256-thread workgroup owns a 128 x 128 tile of C as 2 x 2 waves of 64 x 64, each
-// wave 2 x 2 v_mfma_f32_32x32x16_bf16 blocks. K advances 32 at a time through two LDS buffers
-// (the next slab's global loads are in flight while the current one is multiplied). LDS rows
-// hold 32 + 8 bf16 (80 bytes): a lane's 16-byte fragment read then hits a bank group of its own
-// among the 16 lanes the hardware serves together.
+// Tiling: a workgroup owns a BM x BN tile of C, split over (BM / WM) x (BN / WN) waves of
+// WM x WN, each a grid of v_mfma_f32_32x32x16_bf16 blocks. K advances BK at a time through two
+// LDS buffers: the next slab's global loads are issued before the current slab is multiplied
+// and written to the other buffer after it. LDS rows hold BK + 8 bf16, so that the 16-byte
+// fragment reads of a wave's lanes fall into distinct bank groups.
 //
-// MFMA operand layout (32x32x16): lane l holds A[m = l % 32][k = 8 (l / 32) + i] and
-// B[k = 8 (l / 32) + i][n = l % 32] for i = 0..7; accumulator register r of lane l is
-// C[m = r % 4 + 8 (r / 4) + 4 (l / 32)][n = l % 32].
+// MFMA operand layout (32x32x16): lane l supplies X[i = l % 32][k = 8 (l / 32) + j], j = 0..7,
+// for both operands, and accumulator register r of lane l is the product's element
+// (i = r % 4 + 8 (r / 4) + 4 (l / 32), i' = l % 32). The B fragment is passed as the first
+// operand, so a lane's registers r = 4q .. 4q + 3 hold four consecutive columns of one row of C
+// and the epilogue stores 16 bytes at a time.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "cis_gemm.h"
 
 namespace cis {
+namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4g __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kGemmBM = 128, kGemmBN = 128, kGemmBK = 32, kGemmLdsW = kGemmBK + 8;
+constexpr int kRsrcWord3 = 0x00020000;  // raw buffer, 32-bit data format
 
-// 8 consecutive K-elements of row `r` starting at column `k` (a multiple of 8), as bf16; zeros
-// outside the matrix. Rows start 16-byte aligned (ld a multiple of 8), so a whole vector is one
-// aligned load; the vector that straddles K is read element by element.
-__device__ __forceinline__ bf16x8 cvt8(const __bf16* q) {
-  return __builtin_bit_cast(bf16x8, *(const u32x4g*)q);
-}
-__device__ __forceinline__ bf16x8 cvt8(const float* q) {
-  const f32x4 a = ((const f32x4*)q)[0], b = ((const f32x4*)q)[1];
-  bf16x8 o;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    o[i] = (__bf16)a[i];  // round to nearest even
-    o[4 + i] = (__bf16)b[i];
-  }
-  return o;
-}
-template <class T>
-__device__ __forceinline__ bf16x8 load8(const T* p, int64_t r, int64_t k, int64_t R, int64_t K,
-                                        int64_t ld) {
-  bf16x8 o{};
-  if (r >= R || k >= K) return o;
-  const T* q = p + r * ld + k;
-  if (k + 8 <= K) return cvt8(q);
-  for (int i = 0; i < 8; ++i)
-    if (k + i < K) o[i] = (__bf16)q[i];
-  return o;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, kRsrcWord3);
 }
 
-// Workgroup -> C tile. Consecutive workgroup ids go to the 8 XCDs in turn and each XCD has an
-// L2 of its own, so the id is first remapped so that every XCD receives a contiguous run of the
-// logical order. Logically the smaller operand's tile index runs fastest: the larger operand's
-// panel is then shared by consecutive workgroups and streamed from HBM about once.
-__device__ __forceinline__ void tile_of(const GemmArgs& g, int64_t& tm, int64_t& tn) {
+// Bytes of an R x K row-major matrix (row stride ld elements of `es` bytes) from row r0 on,
+// clamped to the 32-bit range of a buffer resource (offsets used stay below it).
+__device__ __forceinline__ uint32_t span_bytes(int64_t R, int64_t r0, int64_t K, int64_t ld,
+                                               int es) {
+  if (r0 >= R) return 0;
+  const int64_t b = ((R - r0 - 1) * ld + K) * es;
+  return b > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)b;
+}
+
+// Workgroup -> (split, tile). Consecutive workgroup ids go to the 8 XCDs in turn and each XCD
+// has an L2 of its own, so the id is first remapped so that every XCD receives a contiguous run
+// of the logical order. Logically the smaller operand's tile index runs fastest: the larger
+// operand's panel is then shared by consecutive workgroups and streamed from HBM about once.
+template <int BM, int BN>
+__device__ __forceinline__ void tile_of(const GemmArgs& g, int64_t& tm, int64_t& tn,
+                                        int64_t& split) {
   const int64_t nwg = (int64_t)gridDim.x, id = blockIdx.x;
   const int64_t per = nwg / 8, rem = nwg % 8, x = id % 8, loc = id / 8;
   const int64_t lin = (x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per) + loc;
-  const int64_t mt = (g.M + kGemmBM - 1) / kGemmBM, nt = (g.N + kGemmBN - 1) / kGemmBN;
+  const int64_t mt = (g.M + BM - 1) / BM, nt = (g.N + BN - 1) / BN;
+  split = lin / (mt * nt);
+  const int64_t t = lin % (mt * nt);
   if (g.m_fastest) {
-    tm = lin % mt;
-    tn = lin / mt;
+    tm = t % mt;
+    tn = t / mt;
   } else {
-    tn = lin % nt;
-    tm = lin / nt;
+    tn = t % nt;
+    tm = t / nt;
   }
 }
 
-template <class TA, bool BETA>
-__global__ __launch_bounds__(256) void gemm_nt_kernel(const GemmArgs g) {
-  __shared__ __bf16 sA[2][kGemmBM * kGemmLdsW];
-  __shared__ __bf16 sB[2][kGemmBN * kGemmLdsW];
-  const TA* A = static_cast<const TA*>(g.A);
-  const __bf16* B = static_cast<const __bf16*>(g.B);
+template <int BM, int BN, int BK, int WM, int WN>
+struct Cfg {
+  static constexpr int kWavesN = BN / WN;
+  static constexpr int kThreads = (BM / WM) * (BN / WN) * 64;
+  static constexpr int kLdw = BK + 8;     // LDS row, elements
+  static constexpr int kKv = BK / 8;      // 16-byte vectors per tile row
+  static constexpr int kAv = BM * kKv / kThreads, kBv = BN * kKv / kThreads;
+  static constexpr int kTm = WM / 32, kTn = WN / 32;
+  static_assert(BM * kKv % kThreads == 0 && BN * kKv % kThreads == 0, "staging split");
+  static_assert(BK % 16 == 0 && WM % 32 == 0 && WN % 32 == 0, "MFMA blocks");
+};
+
+template <int BM, int BN, int BK, int WM, int WN, bool BETA>
+__global__ __launch_bounds__((Cfg<BM, BN, BK, WM, WN>::kThreads)) void gemm_bf16_kernel(
+    const GemmArgs g) {
+  using C = Cfg<BM, BN, BK, WM, WN>;
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2][(BM + BN) * C::kLdw];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  int64_t tm, tn;
-  tile_of(g, tm, tn);
-  const int64_t m0 = tm * kGemmBM, n0 = tn * kGemmBN;
-  // each thread stages rows lr and lr + 64, K-vector lc of both slabs
-  const int lr = tid >> 2, lc = (tid & 3) * 8;
-  f32x16 acc[2][2];
+  const int wm = wave / C::kWavesN, wn = wave % C::kWavesN;
+  int64_t tm, tn, split;
+  tile_of<BM, BN>(g, tm, tn, split);
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int64_t kbeg = split * g.k_split;
+  const int64_t kend = kbeg + g.k_split < g.K ? kbeg + g.k_split : g.K;
+  const __bf16* A = static_cast<const __bf16*>(g.A) + m0 * g.lda;
+  const __bf16* B = static_cast<const __bf16*>(g.B) + n0 * g.ldb;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, span_bytes(g.M, m0, g.K, g.lda, 2));
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(B, span_bytes(g.N, n0, g.K, g.ldb, 2));
+
+  // staging: vector v = tid + j * kThreads holds row v / kKv, K-chunk v % kKv of the slab
+  uint32_t aoff[C::kAv], boff[C::kBv];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int j = 0; j < C::kAv; ++j) {
+    const int v = tid + j * C::kThreads;
+    aoff[j] = (uint32_t)(((int64_t)(v / C::kKv) * g.lda + (v % C::kKv) * 8) * 2);
+  }
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-  bf16x8 ra[2], rb[2];
+  for (int j = 0; j < C::kBv; ++j) {
+    const int v = tid + j * C::kThreads;
+    boff[j] = (uint32_t)(((int64_t)(v / C::kKv) * g.ldb + (v % C::kKv) * 8) * 2);
+  }
+  u32x4 sa[C::kAv], sb[C::kBv];
   auto gload = [&](int64_t k0) {
+    const uint32_t ko = (uint32_t)(k0 * 2);
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      ra[h] = load8(A, m0 + lr + 64 * h, k0 + lc, g.M, g.K, g.lda);
-      rb[h] = load8(B, n0 + lr + 64 * h, k0 + lc, g.N, g.K, g.ldb);
+    for (int j = 0; j < C::kAv; ++j)
+      sa[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, aoff[j] + ko, 0, 0);
+#pragma unroll
+    for (int j = 0; j < C::kBv; ++j)
+      sb[j] = __builtin_amdgcn_raw_buffer_load_b128(rb, boff[j] + ko, 0, 0);
+    if (k0 + BK > kend) {
+      // the slab crosses the end of this split's K range: zero what lies past it. A vector that
+      // straddles the end is read again element by element (a 16-byte buffer load that is
+      // partly outside the resource returns zeros).
+      auto fix = [&](u32x4& x, int v, __amdgpu_buffer_rsrc_t rs, uint32_t off) {
+        const int64_t k = k0 + (v % C::kKv) * 8;
+        if (k + 8 <= kend) return;
+        bf16x8 e{};
+        for (int i = 0; i < 8; ++i)
+          if (k + i < kend)
+            e[i] = __builtin_bit_cast(
+                __bf16, (unsigned short)__builtin_amdgcn_raw_buffer_load_b16(rs, off + 2 * i, 0, 0));
+        x = __builtin_bit_cast(u32x4, e);
+      };
+#pragma unroll
+      for (int j = 0; j < C::kAv; ++j) fix(sa[j], tid + j * C::kThreads, ra, aoff[j] + ko);
+#pragma unroll
+      for (int j = 0; j < C::kBv; ++j) fix(sb[j], tid + j * C::kThreads, rb, boff[j] + ko);
     }
   };
   auto lstore = [&](int buf) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      *(bf16x8*)&sA[buf][(lr + 64 * h) * kGemmLdsW + lc] = ra[h];
-      *(bf16x8*)&sB[buf][(lr + 64 * h) * kGemmLdsW + lc] = rb[h];
+    for (int j = 0; j < C::kAv; ++j) {
+      const int v = tid + j * C::kThreads;
+      *(u32x4*)&lds[buf][(v / C::kKv) * C::kLdw + (v % C::kKv) * 8] = sa[j];
+    }
+#pragma unroll
+    for (int j = 0; j < C::kBv; ++j) {
+      const int v = tid + j * C::kThreads;
+      *(u32x4*)&lds[buf][(BM + v / C::kKv) * C::kLdw + (v % C::kKv) * 8] = sb[j];
     }
   };
-  const int64_t nk = (g.K + kGemmBK - 1) / kGemmBK;
-  gload(0);
-  lstore(0);
+
+  f32x16 acc[C::kTm][C::kTn];
+#pragma unroll
+  for (int i = 0; i < C::kTm; ++i)
+#pragma unroll
+    for (int j = 0; j < C::kTn; ++j) acc[i][j] = f32x16{};
+
+  const int64_t nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  if (nk > 0) {
+    gload(kbeg);
+    lstore(0);
+  }
   __syncthreads();
+  const int fr = lane & 31, fk = 8 * (lane >> 5);
   for (int64_t kt = 0; kt < nk; ++kt) {
     const int cur = (int)(kt & 1);
-    if (kt + 1 < nk) gload((kt + 1) * kGemmBK);
+    if (kt + 1 < nk) gload(kbeg + (kt + 1) * BK);
+    const __bf16* la = &lds[cur][(wm * WM + fr) * C::kLdw + fk];
+    const __bf16* lb = &lds[cur][(BM + wn * WN + fr) * C::kLdw + fk];
 #pragma unroll
-    for (int ks = 0; ks < kGemmBK / 16; ++ks) {
-      bf16x8 fa[2], fb[2];
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      bf16x8 fa[C::kTm], fb[C::kTn];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int kk = ks * 16 + 8 * (lane >> 5);
-        fa[i] = *(const bf16x8*)&sA[cur][(wm * 64 + i * 32 + (lane & 31)) * kGemmLdsW + kk];
-        fb[i] = *(const bf16x8*)&sB[cur][(wn * 64 + i * 32 + (lane & 31)) * kGemmLdsW + kk];
-      }
+      for (int i = 0; i < C::kTm; ++i) fa[i] = *(const bf16x8*)(la + i * 32 * C::kLdw + ks * 16);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int j = 0; j < C::kTn; ++j) fb[j] = *(const bf16x8*)(lb + j * 32 * C::kLdw + ks * 16);
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < C::kTm; ++i)
+#pragma unroll
+        for (int j = 0; j < C::kTn; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < nk) lstore(cur ^ 1);
     __syncthreads();
   }
-  float* C = g.C;
+
+  // epilogue: lane holds C[m][n .. n + 3] for m = row of lane, n = 8q + 4 (lane / 32)
+  float* Cp = g.C + split * g.c_split_stride;
+  const bool vec = g.c_vec;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < C::kTm; ++i) {
+    const int64_t m = m0 + wm * WM + i * 32 + fr;
+    if (m >= g.M) continue;
+    float* crow = Cp + m * g.ldc;
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < C::kTn; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t m = m0 + wm * 64 + i * 32 + (r % 4) + 8 * (r / 4) + 4 * (lane >> 5);
-        const int64_t n = n0 + wn * 64 + j * 32 + (lane & 31);
-        if (m < g.M && n < g.N) {
-          float v = g.alpha * acc[i][j][r];
-          if (BETA) v += C[m * g.ldc + n];
-          C[m * g.ldc + n] = v;
+      for (int q = 0; q < 4; ++q) {
+        const int64_t n = n0 + wn * WN + j * 32 + 8 * q + 4 * (lane >> 5);
+        f32x4 v = {acc[i][j][4 * q] * g.alpha, acc[i][j][4 * q + 1] * g.alpha,
+                   acc[i][j][4 * q + 2] * g.alpha, acc[i][j][4 * q + 3] * g.alpha};
+        if (vec && n + 3 < g.N) {
+          if (BETA) v += *(const f32x4*)(crow + n);
+          *(f32x4*)(crow + n) = v;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (n + e < g.N) crow[n + e] = BETA ? v[e] + crow[n + e] : v[e];
         }
       }
+  }
 }
 
-// out[c][r] = bf16(in[r][c]) for an R x C matrix (row strides ldi, ldo), 64 x 64 tiles through
-// LDS so that both the reads and the writes are row-contiguous.
+// C = alpha * sum_s P[s] (+ C): the split-K partials summed in split order.
+struct ReduceArgs {
+  const float* P;
+  float* C;
+  int64_t M, N, ldc, split_stride;
+  int32_t splits;
+  float alpha;
+  bool beta;
+};
+
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const ReduceArgs r) {
+  const int64_t total = r.M * r.N;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * 256) {
+    const int64_t m = i / r.N, n = i % r.N;
+    float s = 0.f;
+    for (int k = 0; k < r.splits; ++k) s += r.P[k * r.split_stride + m * r.N + n];
+    float* c = r.C + m * r.ldc + n;
+    *c = r.beta ? s * r.alpha + *c : s * r.alpha;
+  }
+}
+
+// out[c][r] = bf16(in[r][c]) for an R x C matrix (row strides ldi, ldo), and optionally
+// out_n[r][c] = bf16(in[r][c]) (row stride ldn): 64 x 64 tiles through LDS, every global access
+// row-contiguous (four elements per thread).
 template <class TI>
 __global__ __launch_bounds__(256) void transpose_kernel(const TransposeArgs t) {
   __shared__ float tile[64][65];
   const TI* in = static_cast<const TI*>(t.in);
   __bf16* out = static_cast<__bf16*>(t.out);
+  __bf16* outn = static_cast<__bf16*>(t.out_n);
   const int64_t ct = (t.C + 63) / 64;
   const int64_t r0 = (int64_t)(blockIdx.x / ct) * 64, c0 = (int64_t)(blockIdx.x % ct) * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int q = threadIdx.x & 15, p = threadIdx.x >> 4;  // 16 quads per row, 16 rows per pass
 #pragma unroll
-  for (int i = 0; i < 64; i += 4) {
-    const int64_t r = r0 + ty + i, c = c0 + tx;
-    tile[ty + i][tx] = (r < t.R && c < t.C) ? (float)in[r * t.ldi + c] : 0.f;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int lr = p + 16 * pass;
+    const int64_t r = r0 + lr, c = c0 + 4 * q;
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (r < t.R) {
+      const TI* src = in + r * t.ldi + c;
+      if (c + 4 <= t.C) {
+        if constexpr (sizeof(TI) == 4) {
+          const f32x4 x = *(const f32x4*)src;
+          v[0] = x[0], v[1] = x[1], v[2] = x[2], v[3] = x[3];
+        } else {
+          const bf16x4 x = *(const bf16x4*)src;
+          v[0] = (float)x[0], v[1] = (float)x[1], v[2] = (float)x[2], v[3] = (float)x[3];
+        }
+      } else {
+        for (int e = 0; e < 4; ++e)
+          if (c + e < t.C) v[e] = (float)src[e];
+      }
+      if (outn) {
+        __bf16* dst = outn + r * t.ldn + c;
+        if (c + 4 <= t.C) {
+          *(bf16x4*)dst = bf16x4{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+        } else {
+          for (int e = 0; e < 4; ++e)
+            if (c + e < t.C) dst[e] = (__bf16)v[e];
+        }
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) tile[lr][4 * q + e] = v[e];
   }
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < 64; i += 4) {
-    const int64_t c = c0 + ty + i, r = r0 + tx;
-    if (c < t.C && r < t.R) out[c * t.ldo + r] = (__bf16)tile[tx][ty + i];
+  for (int pass = 0; pass < 4; ++pass) {
+    const int lc = p + 16 * pass;
+    const int64_t c = c0 + lc, r = r0 + 4 * q;
+    if (c >= t.C) continue;
+    __bf16* dst = out + c * t.ldo + r;
+    const bf16x4 x = {(__bf16)tile[4 * q][lc], (__bf16)tile[4 * q + 1][lc],
+                      (__bf16)tile[4 * q + 2][lc], (__bf16)tile[4 * q + 3][lc]};
+    if (r + 4 <= t.R) {
+      *(bf16x4*)dst = x;
+    } else {
+      for (int e = 0; e < 4; ++e)
+        if (r + e < t.R) dst[e] = x[e];
+    }
   }
 }
 
-hipError_t launch_gemm_nt(GemmArgs g, bool a_f32, bool beta, hipStream_t stream) {
+template <int BM, int BN, int BK, int WM, int WN>
+hipError_t launch_cfg(GemmArgs g, bool beta, int splits, hipStream_t stream) {
+  const int64_t mt = (g.M + BM - 1) / BM, nt = (g.N + BN - 1) / BN;
+  const void* fn = beta ? (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, true>
+                        : (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, false>;
+  void* args[] = {&g};
+  return hipLaunchKernel(fn, dim3((unsigned)(mt * nt * splits)),
+                         dim3(Cfg<BM, BN, BK, WM, WN>::kThreads), args, 0, stream);
+}
+
+}  // namespace
+
+int64_t gemm_splitk_count(int64_t M, int64_t N, int64_t K, int num_cu) {
+  const int64_t tiles = ((M + kGemmTile - 1) / kGemmTile) * ((N + kGemmTile - 1) / kGemmTile);
+  int64_t s = 1;
+  // split the contraction until every CU has a tile, keeping >= 2048 of K per split
+  while (s < kGemmMaxSplits && tiles * s < num_cu && K / (2 * s) >= 2048) s *= 2;
+  return s;
+}
+
+hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int num_cu,
+                          hipStream_t stream) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
-  const int64_t mt = (g.M + kGemmBM - 1) / kGemmBM, nt = (g.N + kGemmBN - 1) / kGemmBN;
   // A is M x K, B is N x K: the smaller one's tiles run fastest
   g.m_fastest = g.M <= g.N;
-  const void* fn = a_f32 ? (beta ? (const void*)&gemm_nt_kernel<float, true>
-                                 : (const void*)&gemm_nt_kernel<float, false>)
-                         : (beta ? (const void*)&gemm_nt_kernel<__bf16, true>
-                                 : (const void*)&gemm_nt_kernel<__bf16, false>);
-  void* args[] = {&g};
-  return hipLaunchKernel(fn, dim3((unsigned)(mt * nt)), dim3(kGemmThreads), args, 0, stream);
+  const int64_t splits = partial ? gemm_splitk_count(g.M, g.N, g.K, num_cu) : 1;
+  const bool c_aligned = ((uintptr_t)g.C % 16 == 0) && g.ldc % 4 == 0;
+  if (splits <= 1) {
+    g.k_split = g.K > 0 ? g.K : 1;
+    g.c_split_stride = 0;
+    g.c_vec = c_aligned;
+    return launch_cfg<kGemmTile, kGemmTile, kGemmBK, kGemmWaveM, kGemmWaveN>(g, beta, 1, stream);
+  }
+  // split-K: partial products into `partial` [splits][M][N], then summed in split order
+  const int64_t kper = ((g.K + splits - 1) / splits + kGemmBK - 1) / kGemmBK * kGemmBK;
+  GemmArgs p = g;
+  p.C = partial;
+  p.ldc = g.N;
+  p.alpha = 1.f;
+  p.k_split = kper;
+  p.c_split_stride = g.M * g.N;
+  p.c_vec = ((uintptr_t)partial % 16 == 0) && g.N % 4 == 0;
+  if (hipError_t e = launch_cfg<kGemmTile, kGemmTile, kGemmBK, kGemmWaveM, kGemmWaveN>(
+          p, false, (int)splits, stream))
+    return e;
+  ReduceArgs r{partial, g.C, g.M, g.N, g.ldc, g.M * g.N, (int32_t)splits, g.alpha, beta};
+  const int64_t blocks = (g.M * g.N + 255) / 256;
+  void* args[] = {&r};
+  return hipLaunchKernel((const void*)&splitk_reduce_kernel,
+                         dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(256), args, 0,
+                         stream);
 }
 
 hipError_t launch_transpose(TransposeArgs t, bool in_f32, hipStream_t stream) {
   if (t.R <= 0 || t.C <= 0) return hipSuccess;
   const int64_t tiles = ((t.C + kTransposeTile - 1) / kTransposeTile) *
                         ((t.R + kTransposeTile - 1) / kTransposeTile);
-  const dim3 grid((unsigned)tiles);
   const void* fn =
       in_f32 ? (const void*)&transpose_kernel<float> : (const void*)&transpose_kernel<__bf16>;
   void* args[] = {&t};
-  return hipLaunchKernel(fn, grid, dim3(256), args, 0, stream);
+  return hipLaunchKernel(fn, dim3((unsigned)tiles), dim3(256), args, 0, stream);
 }
 
 }  // namespace cis

@@ -43,13 +43,16 @@ inline size_t ws_bytes(int64_t T) { return ws_layout(T, 0).total; }
 //   Wt  bf16[H, ldv]       W^T (backward)
 //   Gt  bf16[V, ldc]       (dL/dz)^T of the chunk (backward)
 //   Ht  bf16[H, ldc]       the chunk's hidden states transposed (backward)
+//   Gb  bf16[rows, ldv]    dL/dz of the chunk in bf16 (backward)
+//   P   float[kLmSplits, rows, H]  split-K partials of dL/dh (backward)
 // with rows = min(T, chunk) and row strides rounded up to 8 elements.
 constexpr int64_t kLmMaxH = int64_t(1) << 16;
 constexpr int64_t kLmMaxChunk = int64_t(1) << 16;
+constexpr int64_t kLmSplits = 8;
 struct LmLayout {
   WsLayout loss;
   int64_t ldz, ldv, ldc;
-  size_t z, wt, gt, ht, total;
+  size_t z, wt, gt, ht, gb, part, total;
 };
 inline LmLayout lm_layout(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_t n_seq,
                           bool bwd) {
@@ -61,13 +64,17 @@ inline LmLayout lm_layout(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_
   M.ldc = ((rows > 0 ? rows : 1) + 7) / 8 * 8;
   M.z = align_up(M.loss.total, 256);
   size_t end = M.z + align_up((size_t)rows * (size_t)M.ldz * 4, 256);
-  M.wt = M.gt = M.ht = end;
+  M.wt = M.gt = M.ht = M.gb = M.part = end;
   if (bwd) {
     end += align_up((size_t)H * (size_t)M.ldv * 2, 256);
     M.gt = end;
     end += align_up((size_t)V * (size_t)M.ldc * 2, 256);
     M.ht = end;
     end += align_up((size_t)H * (size_t)M.ldc * 2, 256);
+    M.gb = end;
+    end += align_up((size_t)rows * (size_t)M.ldv * 2, 256);
+    M.part = end;
+    end += align_up((size_t)kLmSplits * (size_t)rows * (size_t)H * 4, 256);
   }
   M.total = end;
   return M;
