@@ -51,7 +51,6 @@ constexpr int kGemmTile = 256;      // C tile per workgroup (rows and columns)
 constexpr int kGemmBK = 64;         // contraction slab
 constexpr int kGemmWaveM = 128;     // C tile per wave: 128 rows x 64 columns (8 waves)
 constexpr int kGemmWaveN = 64;
-constexpr int kGemmSched = 3;       // fragment reads one step ahead, behind scheduling fences
 constexpr int kGemmMaxSplits = 8;   // split-K partial buffers
 constexpr int kTransposeTile = 64;
 

@@ -6,7 +6,8 @@
 // Tiling: a workgroup owns a BM x BN tile of C, split over (BM / WM) x (BN / WN) waves of
 // WM x WN, each a grid of v_mfma_f32_32x32x16_bf16 blocks. K advances BK at a time through two
 // LDS buffers: the next slab's global loads are issued before the current slab is multiplied
-// and written to the other buffer after it. LDS rows hold BK + 8 bf16, so that the 16-byte
+// and written to the other buffer after it; within a slab the fragments of the next 16-step are
+// read while the current one is multiplied. LDS rows hold BK + 8 bf16, so that the 16-byte
 // fragment reads of a wave's lanes fall into distinct bank groups.
 //
 // MFMA operand layout (32x32x16): lane l supplies X[i = l % 32][k = 8 (l / 32) + j], j = 0..7,
@@ -66,11 +67,10 @@ __device__ __forceinline__ void tile_of(const GemmArgs& g, int64_t& tm, int64_t&
 }
 
 // One slab of MFMAs for a wave's TM x TN blocks over KS steps of 16. The fragments of step
-// ks + 1 are read from LDS while step ks is multiplied (two register sets), so LDS latency hides
-// behind the matrix cores. SCHED 2: the scheduler is asked to alternate one MFMA and one LDS
-// read; SCHED 3: scheduling fences keep each step's reads ahead of the previous step's MFMAs.
-// fa(i, ks) / fb(j, ks) give the LDS address of a fragment.
-template <int TM, int TN, int KS, int SCHED, class FA, class FB>
+// ks + 1 are read from LDS while step ks is multiplied (two register sets); scheduling fences
+// keep those reads ahead of the MFMAs, which the compiler would otherwise sink to just before
+// their use and wait on. fa(i, ks) / fb(j, ks) give the LDS address of a fragment.
+template <int TM, int TN, int KS, class FA, class FB>
 __device__ __forceinline__ void mfma_slab(f32x16 (&acc)[TM][TN], FA fa, FB fb) {
   bf16x8 a[2][TM], b[2][TN];
 #pragma unroll
@@ -86,22 +86,13 @@ __device__ __forceinline__ void mfma_slab(f32x16 (&acc)[TM][TN], FA fa, FB fb) {
 #pragma unroll
       for (int j = 0; j < TN; ++j) b[c ^ 1][j] = *(const bf16x8*)fb(j, ks + 1);
     }
-    if constexpr (SCHED == 3) __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[c][j], a[c][i], acc[i][j], 0, 0, 0);
-    if constexpr (SCHED == 3) __builtin_amdgcn_sched_barrier(0);
-    if constexpr (SCHED == 2) {
-      if (ks + 1 < KS) {
-#pragma unroll
-        for (int q = 0; q < TM * TN; ++q) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // one MFMA
-          if (q < TM + TN) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-        }
-      }
-    }
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -117,7 +108,7 @@ struct Cfg {
   static_assert(BK % 16 == 0 && WM % 32 == 0 && WN % 32 == 0, "MFMA blocks");
 };
 
-template <int BM, int BN, int BK, int WM, int WN, bool BETA, int SCHED>
+template <int BM, int BN, int BK, int WM, int WN, bool BETA>
 __global__ __launch_bounds__((Cfg<BM, BN, BK, WM, WN>::kThreads)) void gemm_bf16_kernel(
     const GemmArgs g) {
   using C = Cfg<BM, BN, BK, WM, WN>;
@@ -206,28 +197,9 @@ __global__ __launch_bounds__((Cfg<BM, BN, BK, WM, WN>::kThreads)) void gemm_bf16
     if (kt + 1 < nk) gload(kbeg + (kt + 1) * BK);
     const __bf16* la = &lds[cur][(wm * WM + fr) * C::kLdw + fk];
     const __bf16* lb = &lds[cur][(BM + wn * WN + fr) * C::kLdw + fk];
-    if constexpr (SCHED == 0) {
-#pragma unroll
-      for (int ks = 0; ks < BK / 16; ++ks) {
-        bf16x8 fa[C::kTm], fb[C::kTn];
-#pragma unroll
-        for (int i = 0; i < C::kTm; ++i)
-          fa[i] = *(const bf16x8*)(la + i * 32 * C::kLdw + ks * 16);
-#pragma unroll
-        for (int j = 0; j < C::kTn; ++j)
-          fb[j] = *(const bf16x8*)(lb + j * 32 * C::kLdw + ks * 16);
-#pragma unroll
-        for (int i = 0; i < C::kTm; ++i)
-#pragma unroll
-          for (int j = 0; j < C::kTn; ++j)
-            acc[i][j] =
-                __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
-      }
-    } else {
-      mfma_slab<C::kTm, C::kTn, BK / 16, SCHED>(
-          acc, [&](int i, int ks) { return la + i * 32 * C::kLdw + ks * 16; },
-          [&](int j, int ks) { return lb + j * 32 * C::kLdw + ks * 16; });
-    }
+    mfma_slab<C::kTm, C::kTn, BK / 16>(
+        acc, [&](int i, int ks) { return la + i * 32 * C::kLdw + ks * 16; },
+        [&](int j, int ks) { return lb + j * 32 * C::kLdw + ks * 16; });
     if (kt + 1 < nk) lstore(cur ^ 1);
     __syncthreads();
   }
@@ -257,196 +229,6 @@ __global__ __launch_bounds__((Cfg<BM, BN, BK, WM, WN>::kThreads)) void gemm_bf16
         }
       }
   }
-}
-
-// The same product with the operands moved global -> LDS by the buffer unit itself (16-byte
-// loads that write LDS, no VGPR staging) into a ring of S slabs of BK = 32, so that S - 1 slabs
-// are in flight while one is multiplied. LDS rows are unpadded (64 bytes); the 16-byte chunk c
-// of row r sits at chunk position c ^ swz(r), which spreads the rows that a fragment read
-// touches together over distinct bank groups. A slab that is cut by the end of the K range goes
-// through registers instead, where it is masked.
-__device__ __forceinline__ int swz4(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// 16-byte buffer load that writes LDS: lane l stores at lds_wave + 16 l (lds_wave is uniform
-// over the wave). Counted by vmcnt; the compiler does not order LDS reads after it.
-__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, __bf16* lds_wave,
-                                           uint32_t voff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_wave,
-                                           16, voff, 0, 0, 0);
-}
-
-// Workgroup barrier that waits for this wave's LDS operations only. __syncthreads() also counts
-// the buffer->LDS loads still in flight as LDS writes to be released and waits for all of them,
-// which would drain the ring; here each wave waits for its own slab with wait_vmcnt first. The
-// memory clobber keeps the compiler from moving LDS accesses across it.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-template <int BM, int BN, int WM, int WN, int S, bool BETA, int SCHED>
-__global__ __launch_bounds__(((BM / WM) * (BN / WN) * 64)) void gemm_bf16_dma_kernel(
-    const GemmArgs g) {
-  constexpr int BK = 32, KV = 4;
-  constexpr int NW = (BM / WM) * (BN / WN), NT = NW * 64, WAVES_N = BN / WN;
-  constexpr int STAGE = (BM + BN) * BK;          // elements per slab
-  constexpr int AL = BM * KV / NT, BL = BN * KV / NT;
-  constexpr int TM = WM / 32, TN = WN / 32;
-  static_assert(BM * KV % NT == 0 && BN * KV % NT == 0, "one 1 KiB block per wave and load");
-  static_assert(S >= 2 && S <= 4, "ring depth");
-  __shared__ __attribute__((aligned(16))) __bf16 lds[S * STAGE];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-  int64_t tm, tn, split;
-  tile_of<BM, BN>(g, tm, tn, split);
-  const int64_t m0 = tm * BM, n0 = tn * BN;
-  const int64_t kbeg = split * g.k_split;
-  const int64_t kend = kbeg + g.k_split < g.K ? kbeg + g.k_split : g.K;
-  const __bf16* A = static_cast<const __bf16*>(g.A) + m0 * g.lda;
-  const __bf16* B = static_cast<const __bf16*>(g.B) + n0 * g.ldb;
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, span_bytes(g.M, m0, g.K, g.lda, 2));
-  const __amdgpu_buffer_rsrc_t rb = make_rsrc(B, span_bytes(g.N, n0, g.K, g.ldb, 2));
-
-  // load j of this lane fills chunk position p = (j * NW + wave) * 64 + lane of the A (B)
-  // region: row p / 4, logical chunk (p % 4) ^ swz(row)
-  uint32_t aoff[AL], boff[BL];
-  int achunk[AL], bchunk[BL];
-#pragma unroll
-  for (int j = 0; j < AL; ++j) {
-    const int p = (j * NW + wave) * 64 + lane, r = p >> 2;
-    achunk[j] = (p & 3) ^ swz4(r);
-    aoff[j] = (uint32_t)(((int64_t)r * g.lda + achunk[j] * 8) * 2);
-  }
-#pragma unroll
-  for (int j = 0; j < BL; ++j) {
-    const int p = (j * NW + wave) * 64 + lane, r = p >> 2;
-    bchunk[j] = (p & 3) ^ swz4(r);
-    boff[j] = (uint32_t)(((int64_t)r * g.ldb + bchunk[j] * 8) * 2);
-  }
-  const int64_t nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
-
-  auto issue = [&](int64_t kt) {
-    __bf16* st = lds + (int)(kt % S) * STAGE;
-    const int64_t k0 = kbeg + kt * BK;
-    const uint32_t ko = (uint32_t)(k0 * 2);
-    if (k0 + BK <= kend) {
-#pragma unroll
-      for (int j = 0; j < AL; ++j) load_lds16(ra, st + (j * NW + wave) * 512, aoff[j] + ko);
-#pragma unroll
-      for (int j = 0; j < BL; ++j)
-        load_lds16(rb, st + BM * BK + (j * NW + wave) * 512, boff[j] + ko);
-    } else {
-      // the last slab of the range: through registers, zero past kend (a vector that
-      // straddles kend is read element by element)
-      auto fetch = [&](__amdgpu_buffer_rsrc_t rs, uint32_t off, int c) {
-        const int64_t k = k0 + c * 8;
-        bf16x8 e{};
-        if (k + 8 <= kend) {
-          e = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
-        } else if (k < kend) {
-          for (int i = 0; i < 8; ++i)
-            if (k + i < kend)
-              e[i] = __builtin_bit_cast(
-                  __bf16,
-                  (unsigned short)__builtin_amdgcn_raw_buffer_load_b16(rs, off + 2 * i, 0, 0));
-        }
-        return e;
-      };
-#pragma unroll
-      for (int j = 0; j < AL; ++j)
-        *(bf16x8*)(st + ((j * NW + wave) * 64 + lane) * 8) = fetch(ra, aoff[j] + ko, achunk[j]);
-#pragma unroll
-      for (int j = 0; j < BL; ++j)
-        *(bf16x8*)(st + BM * BK + ((j * NW + wave) * 64 + lane) * 8) =
-            fetch(rb, boff[j] + ko, bchunk[j]);
-    }
-  };
-
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
-
-  // fragment addressing: row r = wave base + 32 i + lane % 32 has swz(r) = swz(lane % 32)
-  const int fr = lane & 31, hi = lane >> 5, sw = swz4(fr);
-  const int aro = (wm * WM + fr) * BK, bro = BM * BK + (wn * WN + fr) * BK;
-#pragma unroll
-  for (int s = 0; s < S - 1; ++s)
-    if (s < nk) issue(s);
-  for (int64_t kt = 0; kt < nk; ++kt) {
-    // this wave's loads of slab kt have landed once at most the later slabs' are pending
-    const int64_t last = kt + S - 2 < nk - 1 ? kt + S - 2 : nk - 1;
-    const int pend = (int)(last - kt);
-    if (pend >= 2)
-      wait_vmcnt<2 * (AL + BL)>();
-    else if (pend == 1)
-      wait_vmcnt<AL + BL>();
-    else
-      wait_vmcnt<0>();
-    lds_barrier();
-    if (kt + S - 1 < nk) issue(kt + S - 1);  // into the slab read in the previous iteration
-    const __bf16* st = lds + (int)(kt % S) * STAGE;
-    auto fa = [&](int i, int ks) { return st + aro + i * 32 * BK + ((2 * ks + hi) ^ sw) * 8; };
-    auto fb = [&](int j, int ks) { return st + bro + j * 32 * BK + ((2 * ks + hi) ^ sw) * 8; };
-    if constexpr (SCHED == 0) {
-#pragma unroll
-      for (int ks = 0; ks < BK / 16; ++ks) {
-        bf16x8 xa[TM], xb[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i) xa[i] = *(const bf16x8*)fa(i, ks);
-#pragma unroll
-        for (int j = 0; j < TN; ++j) xb[j] = *(const bf16x8*)fb(j, ks);
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] =
-                __builtin_amdgcn_mfma_f32_32x32x16_bf16(xb[j], xa[i], acc[i][j], 0, 0, 0);
-      }
-    } else {
-      mfma_slab<TM, TN, BK / 16, SCHED>(acc, fa, fb);
-    }
-  }
-
-  float* Cp = g.C + split * g.c_split_stride;
-  const bool vec = g.c_vec;
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int64_t m = m0 + wm * WM + i * 32 + fr;
-    if (m >= g.M) continue;
-    float* crow = Cp + m * g.ldc;
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t n = n0 + wn * WN + j * 32 + 8 * q + 4 * hi;
-        f32x4 v = {acc[i][j][4 * q] * g.alpha, acc[i][j][4 * q + 1] * g.alpha,
-                   acc[i][j][4 * q + 2] * g.alpha, acc[i][j][4 * q + 3] * g.alpha};
-        if (vec && n + 3 < g.N) {
-          if (BETA) v += *(const f32x4*)(crow + n);
-          *(f32x4*)(crow + n) = v;
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (n + e < g.N) crow[n + e] = BETA ? v[e] + crow[n + e] : v[e];
-        }
-      }
-  }
-}
-
-template <int BM, int BN, int WM, int WN, int S, int SCHED = 0>
-hipError_t launch_dma_cfg(GemmArgs g, bool beta, int splits, hipStream_t stream) {
-  const int64_t mt = (g.M + BM - 1) / BM, nt = (g.N + BN - 1) / BN;
-  const void* fn = beta ? (const void*)&gemm_bf16_dma_kernel<BM, BN, WM, WN, S, true, SCHED>
-                        : (const void*)&gemm_bf16_dma_kernel<BM, BN, WM, WN, S, false, SCHED>;
-  void* args[] = {&g};
-  return hipLaunchKernel(fn, dim3((unsigned)(mt * nt * splits)),
-                         dim3((BM / WM) * (BN / WN) * 64), args, 0, stream);
 }
 
 // C = alpha * sum_s P[s] (+ C): the split-K partials summed in split order.
@@ -533,11 +315,11 @@ __global__ __launch_bounds__(256) void transpose_kernel(const TransposeArgs t) {
   }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int SCHED = 0>
+template <int BM, int BN, int BK, int WM, int WN>
 hipError_t launch_cfg(GemmArgs g, bool beta, int splits, hipStream_t stream) {
   const int64_t mt = (g.M + BM - 1) / BM, nt = (g.N + BN - 1) / BN;
-  const void* fn = beta ? (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, true, SCHED>
-                        : (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, false, SCHED>;
+  const void* fn = beta ? (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, true>
+                        : (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, false>;
   void* args[] = {&g};
   return hipLaunchKernel(fn, dim3((unsigned)(mt * nt * splits)),
                          dim3(Cfg<BM, BN, BK, WM, WN>::kThreads), args, 0, stream);
@@ -564,7 +346,7 @@ hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int num_cu,
     g.k_split = g.K > 0 ? g.K : 1;
     g.c_split_stride = 0;
     g.c_vec = c_aligned;
-    return launch_cfg<kGemmTile, kGemmTile, kGemmBK, kGemmWaveM, kGemmWaveN, kGemmSched>(g, beta, 1, stream);
+    return launch_cfg<kGemmTile, kGemmTile, kGemmBK, kGemmWaveM, kGemmWaveN>(g, beta, 1, stream);
   }
   // split-K: partial products into `partial` [splits][M][N], then summed in split order
   const int64_t kper = ((g.K + splits - 1) / splits + kGemmBK - 1) / kGemmBK * kGemmBK;
@@ -575,7 +357,7 @@ hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int num_cu,
   p.k_split = kper;
   p.c_split_stride = g.M * g.N;
   p.c_vec = ((uintptr_t)partial % 16 == 0) && g.N % 4 == 0;
-  if (hipError_t e = launch_cfg<kGemmTile, kGemmTile, kGemmBK, kGemmWaveM, kGemmWaveN, kGemmSched>(
+  if (hipError_t e = launch_cfg<kGemmTile, kGemmTile, kGemmBK, kGemmWaveM, kGemmWaveN>(
           p, false, (int)splits, stream))
     return e;
   ReduceArgs r{partial, g.C, g.M, g.N, g.ldc, g.M * g.N, (int32_t)splits, g.alpha, beta};
