@@ -144,6 +144,7 @@ int launch_seq_sum(const float* lp, const float* lq, const uint8_t* mask, const 
 // family / decoupled path); the base entry points pass the CIS operator with ext = false.
 struct LossCall {
   bool bwd, ext;
+  bool bf16_grad;           // float32 logits, bf16 gradient (LM-head path)
   const void* logits;
   int dtype;
   int64_t T, V, ld;
@@ -219,14 +220,16 @@ int launch_rows(const LossCall& c, const Ws& ws, const void* logits, void* dlogi
                 hipStream_t stream) {
   if (rows <= 0) return CIS_OK;
   const int esize = c.dtype == CIS_BF16 ? 2 : 4;
+  const int gsize = c.bf16_grad ? 2 : esize;
   const int32_t nvec = (int32_t)((c.V + 16 / esize - 1) / (16 / esize));
-  const cis::RowVariant& var = c.ext ? cis::select_row_variant_ext(c.dtype, c.bwd, nvec)
-                                     : cis::select_row_variant(c.dtype, c.bwd, nvec);
+  const cis::RowVariant& var = c.ext
+                                   ? cis::select_row_variant_ext(c.dtype, c.bwd, nvec, c.bf16_grad)
+                                   : cis::select_row_variant(c.dtype, c.bwd, nvec);
   cis::RowArgs ra{};
   ra.logits = logits;
   ra.dlogits = dlogits;
   ra.row_bytes = ld * esize;
-  ra.grow_bytes = c.bwd ? ld_g * esize : 0;
+  ra.grow_bytes = c.bwd ? ld_g * gsize : 0;
   ra.ids = c.ids + t0;
   ra.logp_infer = c.logp_infer + t0;
   ra.adv = c.adv + t0;
@@ -371,14 +374,14 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
             cis::gemm_args(hc, m.weight, Z, tc, V, H, m.ld_h, m.ld_w, LM.ldz), false, nullptr,
             ncu, stream)))
       return rc;
-    // loss rows; the backward overwrites Z with G = dL/dz in place
-    if (int rc = launch_rows(c, ws, Z, bwd ? Z : nullptr, LM.ldz, LM.ldz, t0, tc, dev, info,
+    // loss rows; the backward writes G = dL/dz in bf16 (the operand of dL/dh)
+    if (int rc = launch_rows(c, ws, Z, bwd ? Gb : nullptr, LM.ldz, LM.ldv, t0, tc, dev, info,
                              stream))
       return rc;
     if (!bwd) continue;
-    // G in bf16, row-major (operand of dL/dh) and transposed (operand of dL/dW); h_c^T
+    // G^T (operand of dL/dW) and h_c^T
     if (int rc = ok(cis::launch_transpose(
-            cis::TransposeArgs{Z, Gt, Gb, tc, V, LM.ldz, LM.ldc, LM.ldv}, true, stream)))
+            cis::TransposeArgs{Gb, Gt, nullptr, tc, V, LM.ldv, LM.ldc, 0}, false, stream)))
       return rc;
     if (int rc = ok(cis::launch_transpose(
             cis::TransposeArgs{hc, Ht, nullptr, tc, H, m.ld_h, LM.ldc, 0}, false, stream)))
@@ -464,6 +467,7 @@ LmHeadCall lm_call(bool bwd, const void* hidden, int64_t T, int64_t H, int64_t l
   m.loss = ext_call(bwd, nullptr, CIS_F32, T, V, 0, ids, logp_infer, logp_old, adv, mask, offsets,
                     n_seq, params, nullptr, 0, logp_train_out, w_out, acted_out, terms_out,
                     eps_out, loss_out, workspace, workspace_bytes);
+  m.loss.bf16_grad = true;
   m.hidden = hidden;
   m.weight = weight;
   m.H = H;

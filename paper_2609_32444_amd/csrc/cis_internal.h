@@ -39,11 +39,11 @@ inline WsLayout ws_layout(int64_t T, int64_t n_seq) {
 inline size_t ws_bytes(int64_t T) { return ws_layout(T, 0).total; }
 
 // LM-head workspace: the loss workspace above, then (256-byte aligned)
-//   Z   float[rows, ldz]   the chunk's logits; the backward overwrites them with dL/dz
+//   Z   float[rows, ldz]   the chunk's logits
 //   Wt  bf16[H, ldv]       W^T (backward)
 //   Gt  bf16[V, ldc]       (dL/dz)^T of the chunk (backward)
 //   Ht  bf16[H, ldc]       the chunk's hidden states transposed (backward)
-//   Gb  bf16[rows, ldv]    dL/dz of the chunk in bf16 (backward)
+//   Gb  bf16[rows, ldv]    dL/dz of the chunk in bf16, written by the loss rows (backward)
 //   P   float[kLmSplits, rows, H]  split-K partials of dL/dh (backward)
 // with rows = min(T, chunk) and row strides rounded up to 8 elements.
 constexpr int64_t kLmMaxH = int64_t(1) << 16;
@@ -92,9 +92,9 @@ struct OpArgs {
 // Arguments of the row kernels, passed by value.
 struct RowArgs {
   const void* logits;       // [T, ld] elements
-  void* dlogits;            // [T, ldg] elements (bwd only)
-  int64_t row_bytes;        // ld  * sizeof(elem)
-  int64_t grow_bytes;       // ldg * sizeof(elem)
+  void* dlogits;            // [T, ldg] gradient elements (bwd only)
+  int64_t row_bytes;        // ld  * sizeof(logit element)
+  int64_t grow_bytes;       // ldg * sizeof(gradient element)
   const int64_t* ids;
   const float* logp_infer;
   const float* adv;
@@ -185,9 +185,11 @@ struct RowVariant {
 };
 
 // Picks the variant for `nvec` 16-byte vectors per row; dtype is CIS_BF16 or CIS_F32. The
-// extended variants carry the operator family and the decoupled path in their epilogue.
+// extended variants carry the operator family and the decoupled path in their epilogue;
+// bf16_grad selects, for float32 logits, a fused pass that writes the gradient in bf16.
 const RowVariant& select_row_variant(int dtype, bool bwd, int32_t nvec);
-const RowVariant& select_row_variant_ext(int dtype, bool bwd, int32_t nvec);
+const RowVariant& select_row_variant_ext(int dtype, bool bwd, int32_t nvec,
+                                         bool bf16_grad = false);
 
 const void* finalize_kernel();
 const void* weights_kernel();

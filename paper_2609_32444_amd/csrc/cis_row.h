@@ -41,6 +41,7 @@ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLog2e = 1.44269504088896340736f;
@@ -232,6 +233,11 @@ __device__ __forceinline__ uint32_t after(u32x4 x) {
   asm volatile("v_mov_b32 %0, 0" : "=v"(z) : "v"(x));
   return z;
 }
+__device__ __forceinline__ uint32_t after(u32x2 x) {
+  uint32_t z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z) : "v"(x));
+  return z;
+}
 __device__ __forceinline__ uint32_t after(float a, float b, float c, float d) {
   uint32_t z;
   asm volatile("v_mov_b32 %0, 0" : "=v"(z) : "v"(a), "v"(b), "v"(c), "v"(d));
@@ -264,12 +270,6 @@ __device__ __forceinline__ uint32_t rp_off(int BLOCK, const RowGeom& g, uint32_t
   return (g.has_rp && g.rp_mine) ? voff + (uint32_t)(g.L * BLOCK * 16) : kOutOfRange;
 }
 
-// Writes elements [0, n) of gradient vector v one by one (the partial last vector).
-template <class E>
-__device__ __forceinline__ void store_partial(void* grow, int v, u32x4 val, int n) {
-  for (int e = 0; e < n; ++e) E::store_elem(grow, v * E::kPerVec + e, E::elem_bits(val, e));
-}
-
 // Gradient of one 16-byte vector of logits: exp2(z*log2e - b2) rounded to the storage format,
 // with the sign applied as an xor of the sign bits (sgn = 0 or the format's sign mask).
 template <class E>
@@ -280,6 +280,48 @@ __device__ __forceinline__ u32x4 grad_vec(u32x4 zv, float b2, uint32_t sgn) {
   for (int e = 0; e < E::kPerVec; ++e) f[e] = fast_exp2(__builtin_fmaf(f[e], kLog2e, -b2));
   return E::pack(f) ^ u32x4{sgn, sgn, sgn, sgn};
 }
+
+// Gradient output of one 16-byte vector of logits. By default it has the logits' format and
+// position. GradOut<F32, Bf16> (float32 logits, bf16 gradient: the LM-head path) packs the four
+// values into 8 bytes at half the byte offset, in a separate gradient buffer.
+template <class E, class EO>
+struct GradOut {
+  static_assert(__is_same(E, EO), "bf16 gradients of fp32 logits: GradOut<F32, Bf16>");
+  typedef u32x4 vec;
+  static constexpr int kShift = 0;  // output byte offset = input byte offset >> kShift
+  static constexpr uint32_t kSign = E::kSignMask;
+  __device__ static __forceinline__ vec zero() { return u32x4{0u, 0u, 0u, 0u}; }
+  __device__ static __forceinline__ vec make(u32x4 zv, float b2, uint32_t sgn) {
+    return grad_vec<E>(zv, b2, sgn);
+  }
+  __device__ static __forceinline__ void store(vec v, __amdgpu_buffer_rsrc_t r, uint32_t o) {
+    bstore(v, r, o, 0u);
+  }
+  __device__ static __forceinline__ uint32_t elem(vec v, int e) { return E::elem_bits(v, e); }
+};
+template <class E>
+struct GradOutNarrow {
+  typedef u32x2 vec;
+  static constexpr int kShift = 1;
+  static constexpr uint32_t kSign = Bf16::kSignMask;
+  __device__ static __forceinline__ vec zero() { return u32x2{0u, 0u}; }
+  __device__ static __forceinline__ vec make(u32x4 zv, float b2, uint32_t sgn) {
+    float f[4];
+    F32::unpack(zv, f);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) f[e] = fast_exp2(__builtin_fmaf(f[e], kLog2e, -b2));
+    const bf16x2 lo = {(__bf16)f[0], (__bf16)f[1]}, hi = {(__bf16)f[2], (__bf16)f[3]};
+    return u32x2{__builtin_bit_cast(uint32_t, lo) ^ sgn, __builtin_bit_cast(uint32_t, hi) ^ sgn};
+  }
+  __device__ static __forceinline__ void store(vec v, __amdgpu_buffer_rsrc_t r, uint32_t o) {
+    __builtin_amdgcn_raw_buffer_store_b64(v, r, o >> 1, 0u, kAuxNT);
+  }
+  __device__ static __forceinline__ uint32_t elem(vec v, int e) {
+    return (v[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+  }
+};
+template <>
+struct GradOut<F32, Bf16> : GradOutNarrow<F32> {};
 
 // Exp-sum of one vector relative to mb = max*log2e, optionally leaving out element `skip`.
 template <class E>
@@ -481,9 +523,10 @@ __device__ __forceinline__ float displacement(float lp, float lq, float one_m_p)
 //   EXT: the epilogue also carries the operator family (rate-1 path, any token operator) and
 //        the decoupled PPO-clip path (weight from the pre-pass, clipped update ratio). The base
 //        kernels compute the CIS weight only, which keeps their registers for the row.
-template <class E, int BLOCK, int NV, int NL, bool BWD, bool PF, bool EXT>
+template <class E, int BLOCK, int NV, int NL, bool BWD, bool PF, bool EXT, class EO = E>
 __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
   static_assert(NL == 0 || (BWD && !PF), "LDS slots are for the fused pass");
+  using GO = GradOut<E, EO>;
   constexpr int EPV = E::kPerVec;
   constexpr int NW = BLOCK / 64;
   __shared__ float sh_m[2][NW];
@@ -566,8 +609,8 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     const __amdgpu_buffer_rsrc_t rs = row_rsrc(row, valid, g);
     void* grow = BWD ? (void*)((char*)a.dlogits + row * a.grow_bytes) : nullptr;
     // write descriptor: complete vectors only
-    const __amdgpu_buffer_rsrc_t ws =
-        make_rsrc(grow, BWD ? (uint32_t)(g.nvec - (g.ragged ? 1 : 0)) * 16u : 0u);
+    const __amdgpu_buffer_rsrc_t ws = make_rsrc(
+        grow, BWD ? ((uint32_t)(g.nvec - (g.ragged ? 1 : 0)) * 16u) >> GO::kShift : 0u);
     // the next row of this workgroup (prefetched during this row's last sweep)
     const bool nvalid = PF && cur.valid(V);
     const __amdgpu_buffer_rsrc_t nrs = row_rsrc(nrow, nvalid, g);
@@ -765,29 +808,29 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     // finally the sampled element is overwritten with coef*(1-p) by the thread that stored its
     // vector (same-thread program order). Invalid rows store zeros.
     if (BWD) {
-      const uint32_t sgn = coef > 0.f ? E::kSignMask : 0u;
+      const uint32_t sgn = coef > 0.f ? GO::kSign : 0u;
       static_for<NV>([&](auto I) {
         constexpr int i = I;
         const uint32_t o = slot_off<BLOCK>(i, g, voff);
-        u32x4 out = {0u, 0u, 0u, 0u};
-        if (valid) out = grad_vec<E>(r[i], b2, sgn);
+        typename GO::vec out = GO::zero();
+        if (valid) out = GO::make(r[i], b2, sgn);
         if (PF) r[i] = bload(nrs, o + after(out), 0u);
-        bstore(out, ws, o, 0u);
+        GO::store(out, ws, o);
         slot_fence();
       });
       {
         const uint32_t o = rp_off(BLOCK, g, voff);
-        u32x4 out = {0u, 0u, 0u, 0u};
-        if (valid) out = grad_vec<E>(rp, b2, sgn);
+        typename GO::vec out = GO::zero();
+        if (valid) out = GO::make(rp, b2, sgn);
         if (PF) rp = bload(nrs, o + after(out), 0u);
-        bstore(out, ws, o, 0u);
+        GO::store(out, ws, o);
       }
       static_for<NL>([&](auto K) {
         constexpr int k = K;
         if (k < g.nlds) {
-          u32x4 out = {0u, 0u, 0u, 0u};
-          if (valid) out = grad_vec<E>(lds_row[k * BLOCK + tid], b2, sgn);
-          bstore(out, ws, voff + (uint32_t)((NV + k) * BLOCK * 16), 0u);
+          typename GO::vec out = GO::zero();
+          if (valid) out = GO::make(lds_row[k * BLOCK + tid], b2, sgn);
+          GO::store(out, ws, voff + (uint32_t)((NV + k) * BLOCK * 16));
         }
       });
       if (!g.has_rp) {
@@ -797,18 +840,19 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
         u32x4 cur = bload(rs, o < end ? o : kOutOfRange, 0u);
         for (; o < end; o += step) {
           const u32x4 nxt = bload(rs, o + step < end ? o + step : kOutOfRange, 0u);
-          u32x4 out = {0u, 0u, 0u, 0u};
-          if (valid) out = grad_vec<E>(cur, b2, sgn);
-          bstore(out, ws, o, 0u);
+          typename GO::vec out = GO::zero();
+          if (valid) out = GO::make(cur, b2, sgn);
+          GO::store(out, ws, o);
           cur = nxt;
         }
       }
       if (g.ragged && g.last_mine) {
-        u32x4 out = {0u, 0u, 0u, 0u};
-        if (valid) out = grad_vec<E>(bload(rs, (uint32_t)(g.nvec - 1) * 16u, 0u), b2, sgn);
-        store_partial<E>(grow, g.nvec - 1, out, g.tail);
+        typename GO::vec out = GO::zero();
+        if (valid) out = GO::make(bload(rs, (uint32_t)(g.nvec - 1) * 16u, 0u), b2, sgn);
+        for (int e = 0; e < g.tail; ++e)
+          EO::store_elem(grow, (g.nvec - 1) * EPV + e, GO::elem(out, e));
       }
-      if (valid && y_mine) E::store_elem(grow, y, E::bits_of(coef * one_m_p));
+      if (valid && y_mine) EO::store_elem(grow, y, EO::bits_of(coef * one_m_p));
     }
   }
 }
@@ -818,6 +862,9 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 // ------------------------------------------------------------------------------------------
 #define CIS_V(E, B, N, L, BWD, PF) \
   RowVariant{B, N, L, (const void*)&cis_row_kernel<E, B, N, L, BWD, PF, CIS_EXT>}
+// fused-pass variant with a gradient format other than the logits' (GradOut<E, EO>)
+#define CIS_VO(E, EO, B, N, L, PF) \
+  RowVariant{B, N, L, (const void*)&cis_row_kernel<E, B, N, L, true, PF, CIS_EXT, EO>}
 
 // Row capacity of a variant: block*(nv+1) vectors (block*(nv+nl) with LDS slots); a row goes
 // to the first variant that holds it. The ladders were chosen by timing every (block, nv)
@@ -827,13 +874,14 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 // sweep only on short rows (on long ones it costs more than it hides), and adds 9 LDS slots
 // (144 KiB) for rows beyond its registers. The fp32 forward kernel stops at 15 slots (18
 // would spill the prefetched row to scratch).
-#define CIS_BWD_TABLE(E)                                                                    \
-  {CIS_V(E, 64, 1, 0, true, true),     CIS_V(E, 64, 3, 0, true, true),                      \
-   CIS_V(E, 64, 7, 0, true, true),     CIS_V(E, 64, 15, 0, true, true),                     \
-   CIS_V(E, 512, 3, 0, true, false),   CIS_V(E, 256, 15, 0, true, true),                    \
-   CIS_V(E, 1024, 7, 0, true, false),  CIS_V(E, 1024, 11, 0, true, false),                  \
-   CIS_V(E, 1024, 15, 0, true, false), CIS_V(E, 1024, 18, 0, true, false),                  \
-   CIS_V(E, 1024, 18, 9, true, false)}
+#define CIS_BWD_TABLE_OUT(E, EO)                                                            \
+  {CIS_VO(E, EO, 64, 1, 0, true),     CIS_VO(E, EO, 64, 3, 0, true),                        \
+   CIS_VO(E, EO, 64, 7, 0, true),     CIS_VO(E, EO, 64, 15, 0, true),                       \
+   CIS_VO(E, EO, 512, 3, 0, false),   CIS_VO(E, EO, 256, 15, 0, true),                      \
+   CIS_VO(E, EO, 1024, 7, 0, false),  CIS_VO(E, EO, 1024, 11, 0, false),                    \
+   CIS_VO(E, EO, 1024, 15, 0, false), CIS_VO(E, EO, 1024, 18, 0, false),                    \
+   CIS_VO(E, EO, 1024, 18, 9, false)}
+#define CIS_BWD_TABLE(E) CIS_BWD_TABLE_OUT(E, E)
 #define CIS_FWD_TABLE(E, LAST)                                                              \
   {CIS_V(E, 64, 1, 0, false, true),    CIS_V(E, 64, 3, 0, false, true),                     \
    CIS_V(E, 64, 7, 0, false, true),    CIS_V(E, 64, 15, 0, false, true),                    \
