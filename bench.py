@@ -88,6 +88,22 @@ def hbm_traffic(mode: str, workload: str):
         return None
 
 
+def lmhead_traffic():
+    """HBM bytes per LM-head call (all of its kernels) from the committed counter passes, if
+    they were taken on the current source (else None)."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_lmhead.json")
+    try:
+        rec = json.load(open(path))
+        if rec.get("source_hash") != kernel_source_hash(LMHEAD_SOURCES):
+            return None
+        return int(rec["bytes_per_call"])
+    except Exception:
+        return None
+
+
+LMHEAD_SOURCES = ("paper_2609_32444_amd/csrc/cis_gemm.hip", "paper_2609_32444_amd/csrc/cis_gemm.h")
+
+
 def bandwidth_ceilings(rows: int, row_bytes: int, torch) -> dict:
     """Measured ceilings on this device (libcis_probe.so), in GB/s: the row kernel's access
     pattern as copy (equal read and write), read only and write only of rows x row_bytes, and
@@ -307,14 +323,14 @@ def bench_lmhead(args, torch, cis):
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": tflops / MFMA_BF16_PEAK_TFLOPS,
-            "traffic": None,
+            "traffic": lmhead_traffic() if bwd and chunk == 4096 and H == 2048 else None,
+            "traffic_scope": "HBM bytes per call, every kernel of the call (rocprofv3 counters)",
             "algorithmic_flops_per_call": flops,
             "avg_call_ms": avg_call_ms,
             "min_call_ms": per_call[0],
             "scope": "whole call (every kernel of the chunked pipeline) against the matrix-core "
                      "peak of its three products",
-            "kernel_source": kernel_source_hash(("paper_2609_32444_amd/csrc/cis_gemm.hip",
-                                                 "paper_2609_32444_amd/csrc/cis_gemm.h")),
+            "kernel_source": kernel_source_hash(LMHEAD_SOURCES),
         },
     }
     if not args.no_cpu_baseline:
