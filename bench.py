@@ -327,6 +327,7 @@ def bench_lmhead(args, torch, cis):
             "traffic_scope": "HBM bytes per call, every kernel of the call (rocprofv3 counters)",
             "algorithmic_flops_per_call": flops,
             "avg_call_ms": avg_call_ms,
+            "median_call_ms": per_call[len(per_call) // 2],
             "min_call_ms": per_call[0],
             "scope": "whole call (every kernel of the chunked pipeline) against the matrix-core "
                      "peak of its three products",
@@ -469,6 +470,7 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": alg,
             "avg_call_ms": avg_call_ms,
+            "median_call_ms": per_call[len(per_call) // 2],
             "min_call_ms": per_call[0],
             "kernel_source": kernel_source_hash(),
         },
