@@ -295,7 +295,7 @@ int cis_loss_bwd_ex(const void* logits, int dtype, int64_t T, int64_t V, int64_t
 /* Workspace bytes for cis_lmhead_loss_fwd (with_grad = 0) or _bwd (with_grad != 0): the loss
  * workspace of cis_workspace_bytes_ex plus the chunk's float32 logits (min(T, chunk) x V) and,
  * with gradients, W^T and two transposed chunk operands (about 2*V*H + 2*(V + H)*chunk bytes).
- * Returns 0 for T < 0, V outside [1, 2^28], H outside [1, 2^16], chunk outside [1, 2^16] or
+ * Returns 0 for T < 0, V outside [1, 2^22], H outside [1, 2^16], chunk outside [1, 2^16] or
  * n_seq < 0. */
 size_t cis_lmhead_workspace_bytes(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_t n_seq,
                                   int with_grad);
@@ -304,10 +304,10 @@ size_t cis_lmhead_workspace_bytes(int64_t T, int64_t V, int64_t H, int64_t chunk
  * cis_lmhead_loss_fwd — the loss (any operator; the decoupled path with logp_old) on the logits
  * hidden * weight^T.
  *
- *   hidden [T, ld_h] bf16   last hidden state of each token row; ld_h >= H, a multiple of 8,
- *                           base 16-byte aligned
- *   weight [V, ld_w] bf16   head weight (row v produces logit v); ld_w >= H, a multiple of 8,
- *                           base 16-byte aligned
+ *   hidden [T, ld_h] bf16   last hidden state of each token row; H <= ld_h <= 2^22, a multiple
+ *                           of 8, base 16-byte aligned
+ *   weight [V, ld_w] bf16   head weight (row v produces logit v), 1 <= V <= 2^22; H <= ld_w <=
+ *                           2^22, a multiple of 8, base 16-byte aligned
  *   chunk                   rows per chunk (1 <= chunk <= 2^16); the workspace holds one
  *                           chunk of float32 logits. Results do not depend on chunk.
  *   ids, logp_infer, logp_old, adv, mask, seq_offsets, n_seq, params and the per-row outputs

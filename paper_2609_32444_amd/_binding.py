@@ -498,6 +498,8 @@ def _lmhead(bwd, hidden, weight, ids, logp_infer, adv, mask, prm, logp_old, seq_
             if dhidden is None:
                 dhidden = torch.empty(T, H, dtype=torch.float32, device=dev)
             if dweight is None:
+                if accumulate:
+                    raise ValueError("accumulate=True needs the dweight to accumulate into")
                 dweight = torch.empty(V, H, dtype=torch.float32, device=dev)
             for name, g, rows in (("dhidden", dhidden, T), ("dweight", dweight, V)):
                 if g.device != dev or g.dtype != torch.float32 or g.dim() != 2 \

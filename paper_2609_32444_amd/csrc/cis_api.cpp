@@ -330,7 +330,8 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
   const int64_t T = c.T, V = c.V, H = m.H;
   if (T < 0 || V < 1 || V > kMaxV || H < 1 || c.n_seq < 0 || m.chunk < 1) return CIS_ERR_SHAPE;
   if (m.ld_h < H || m.ld_w < H || (bwd && (m.ld_dh < H || m.ld_dw < H))) return CIS_ERR_SHAPE;
-  if (H > cis::kLmMaxH || m.chunk > cis::kLmMaxChunk) return CIS_ERR_SHAPE;
+  if (H > cis::kLmMaxH || m.chunk > cis::kLmMaxChunk || V > cis::kLmMaxV) return CIS_ERR_SHAPE;
+  if (m.ld_h > cis::kLmMaxLd || m.ld_w > cis::kLmMaxLd) return CIS_ERR_SHAPE;
   if (int rc = check_loss_params(c)) return rc;
   const int64_t n_seq = seq_count(c);
   if (!c.workspace || !m.weight) return CIS_ERR_NULL;
@@ -489,7 +490,7 @@ extern "C" {
 size_t cis_lmhead_workspace_bytes(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_t n_seq,
                                   int with_grad) {
   if (T < 0 || V < 1 || H < 1 || chunk < 1 || n_seq < 0) return 0;
-  if (V > kMaxV || H > cis::kLmMaxH || chunk > cis::kLmMaxChunk) return 0;
+  if (V > cis::kLmMaxV || H > cis::kLmMaxH || chunk > cis::kLmMaxChunk) return 0;
   return cis::lm_layout(T, V, H, chunk, n_seq, with_grad != 0).total;
 }
 

@@ -48,6 +48,10 @@ inline size_t ws_bytes(int64_t T) { return ws_layout(T, 0).total; }
 // with rows = min(T, chunk) and row strides rounded up to 8 elements.
 constexpr int64_t kLmMaxH = int64_t(1) << 16;
 constexpr int64_t kLmMaxChunk = int64_t(1) << 16;
+// The products address a 256-row operand tile with 32-bit byte offsets, so operand row strides
+// stay below 2^23 elements: V (the contracted length of dL/dh) and ld_h, ld_w up to 2^22.
+constexpr int64_t kLmMaxV = int64_t(1) << 22;
+constexpr int64_t kLmMaxLd = int64_t(1) << 22;
 constexpr int64_t kLmSplits = 8;
 struct LmLayout {
   WsLayout loss;

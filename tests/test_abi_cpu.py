@@ -208,7 +208,7 @@ def test_lmhead_workspace_bytes():
     # a chunk larger than the batch only needs the batch's rows
     assert f(100, 1000, 64, 4096, 0, True) == f(100, 1000, 64, 100, 0, True)
     assert f(T, V, H, 4096, 10, True) >= bwd
-    for bad in ((-1, V, H, 1), (T, 0, H, 1), (T, V, 0, 1), (T, V, H, 0), (T, 1 << 29, H, 1),
+    for bad in ((-1, V, H, 1), (T, 0, H, 1), (T, V, 0, 1), (T, V, H, 0), (T, (1 << 22) + 1, H, 1),
                 (T, V, 1 << 17, 1), (T, V, H, 1 << 17)):
         assert f(*bad, 0, True) == 0, bad
     assert f(T, V, H, 64, -1, True) == 0
@@ -235,6 +235,7 @@ def _lm(bwd=True, **kw):
     (dict(T=-1), -2), (dict(V=0), -2), (dict(H=0), -2), (dict(ld_h=32), -2),
     (dict(ld_w=32), -2), (dict(ld_dh=32), -2), (dict(ld_dw=32), -2), (dict(chunk=0), -2),
     (dict(chunk=1 << 17), -2), (dict(H=1 << 17, ld_h=1 << 17, ld_w=1 << 17), -2),
+    (dict(V=(1 << 22) + 1), -2), (dict(ld_h=(1 << 22) + 8), -2), (dict(ld_w=(1 << 22) + 8), -2),
     (dict(ld_h=68, H=60), -5), (dict(ld_w=68, H=60), -5), (dict(hidden=FAKE + 8), -5),
     (dict(weight=FAKE + 8), -5), (dict(ws=FAKE + 16), -5), (dict(wsb=1000), -7),
     (dict(prm=None), -1), (dict(lold=FAKE, prm=None), -1),
@@ -255,3 +256,12 @@ def test_lmhead_fwd_needs_no_gradient_buffers():
     # a sequence operator needs logp_old and responses
     assert _lm(True, prm=_prm(op=8, hi=2.0)) == -4
     assert _lm(True, prm=_prm(op=8, hi=2.0), lold=FAKE, nseq=2, offs=FAKE) == -9
+
+
+def test_lmhead_binding_rejects_accumulating_into_nothing():
+    import torch
+    h = torch.zeros(4, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        cis.lmhead_loss_bwd(h, torch.zeros(10, 64, dtype=torch.bfloat16),
+                            torch.zeros(4, dtype=torch.int64), torch.zeros(4), torch.zeros(4),
+                            params=cis.params(), accumulate=True)
