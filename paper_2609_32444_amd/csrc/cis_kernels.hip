@@ -19,18 +19,34 @@ __global__ __launch_bounds__(kFinalizeBlock) void cis_finalize_kernel(const Fina
   double acc = 0.0, exc = 0.0;
   float mx = 0.f;
   long long nv = 0, nb = 0, nf = 0, nt = 0;
-  for (int64_t t = tid; t < a.T; t += kFinalizeBlock) {
-    acc += (double)a.terms_ws[t];
-    const uint8_t f = a.flags_ws[t];
+  auto take = [&](float term, uint8_t f, float lk, float ex) {
+    acc += (double)term;
     nv += (f & kFlagValid) ? 1 : 0;
     nb += (f & kFlagBadId) ? 1 : 0;
     nf += (f & kFlagNonFinite) ? 1 : 0;
     nt += (f & kFlagTrunc) ? 1 : 0;
     if (f & kFlagValid) {
-      mx = fmaxf(mx, fabsf(a.logk_ws[t]));  // fmaxf ignores NaN
-      exc += (double)a.excess_ws[t];
+      mx = fmaxf(mx, fabsf(lk));  // fmaxf ignores NaN
+      exc += (double)ex;
     }
+  };
+  // four rows per thread and step, with 16-byte (4-byte for the flags) loads of the 256-byte
+  // aligned workspace arrays; the loop is unrolled so that several steps' loads are in flight
+  typedef float f4 __attribute__((ext_vector_type(4)));
+  const int64_t T4 = a.T / 4;
+  const f4* terms4 = reinterpret_cast<const f4*>(a.terms_ws);
+  const f4* logk4 = reinterpret_cast<const f4*>(a.logk_ws);
+  const f4* exc4 = reinterpret_cast<const f4*>(a.excess_ws);
+  const uint32_t* flags4 = reinterpret_cast<const uint32_t*>(a.flags_ws);
+#pragma unroll 4
+  for (int64_t q = tid; q < T4; q += kFinalizeBlock) {
+    const f4 tv = terms4[q], lv = logk4[q], ev = exc4[q];
+    const uint32_t fv = flags4[q];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) take(tv[e], (uint8_t)(fv >> (8 * e)), lv[e], ev[e]);
   }
+  for (int64_t t = T4 * 4 + tid; t < a.T; t += kFinalizeBlock)
+    take(a.terms_ws[t], a.flags_ws[t], a.logk_ws[t], a.excess_ws[t]);
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     acc += __shfl_down(acc, off, 64);
