@@ -260,10 +260,19 @@ def bench_lmhead(args, torch, cis):
         raise SystemExit("--lmhead runs the MoE-rollout shape (--config 2)")
     T, V = spec
     H, chunk = args.hidden, args.chunk
-    b = make_lmhead_batch(T, V, H, device="cuda", seed=2, c=args.c)
+    ext = args.op is not None or args.decoupled
+    op = args.op or "cis"
+    if op in ("seq_tis", "seq_mis") and not args.decoupled:
+        raise SystemExit("sequence operators need --decoupled")
+    b = make_lmhead_batch(T, V, H, device="cuda", seed=2, c=args.c,
+                          old_sd=0.3 if args.decoupled else None)
     bwd = args.mode == "bwd"
-    prm = cis.params(cis.OP_CIS, lam=b.lam, kappa=b.kappa, scale=b.scale)
-    ws = torch.empty(cis.lmhead_workspace_bytes(T, V, H, chunk, 0, bwd), dtype=torch.uint8,
+    lo, hi = OP_BOUNDS.get(op, (0.0, math.inf))
+    prm = cis.params(OPS[op], lam=b.lam, kappa=b.kappa, lo=lo, hi=hi, scale=b.scale)
+    lold = b.logp_old if args.decoupled else None
+    offs = b.offsets if op.startswith("seq_") else None
+    n_seq = 0 if offs is None else offs.numel() - 1
+    ws = torch.empty(cis.lmhead_workspace_bytes(T, V, H, chunk, n_seq, bwd), dtype=torch.uint8,
                      device="cuda")
     dh = torch.empty(T, H, dtype=torch.float32, device="cuda") if bwd else None
     dw = torch.empty(V, H, dtype=torch.float32, device="cuda") if bwd else None
@@ -271,12 +280,13 @@ def bench_lmhead(args, torch, cis):
     if bwd:
         def step():
             return cis.lmhead_loss_bwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
-                                       params=prm, chunk=chunk, dhidden=dh, dweight=dw,
-                                       want=want, workspace=ws)
+                                       params=prm, logp_old=lold, seq_offsets=offs, chunk=chunk,
+                                       dhidden=dh, dweight=dw, want=want, workspace=ws)
     else:
         def step():
             return cis.lmhead_loss_fwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
-                                       params=prm, chunk=chunk, want=want, workspace=ws)
+                                       params=prm, logp_old=lold, seq_offsets=offs, chunk=chunk,
+                                       want=want, workspace=ws)
     torch.cuda.synchronize()
     for _ in range(args.warmup):
         step()
@@ -314,7 +324,9 @@ def bench_lmhead(args, torch, cis):
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"moe-rollout LM head T={T} V={V} H={H} bf16 chunk={chunk} "
-                               f"c={args.c:g} {'fused fwd+bwd' if bwd else 'forward only'}",
+                               f"c={args.c:g} {'fused fwd+bwd' if bwd else 'forward only'}"
+                               + (f" op={op}" if ext else "")
+                               + (" decoupled PPO-clip (0.2, 0.28)" if args.decoupled else ""),
                    "T": T, "V": V, "H": H, "chunk": chunk, "valid_tokens": n_valid,
                    "lambda": b.lam, "kappa": b.kappa, "seed": b.meta["seed"]},
         "roofline": {
@@ -323,7 +335,8 @@ def bench_lmhead(args, torch, cis):
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": tflops / MFMA_BF16_PEAK_TFLOPS,
-            "traffic": lmhead_traffic() if bwd and chunk == 4096 and H == 2048 else None,
+            "traffic": lmhead_traffic() if bwd and chunk == 4096 and H == 2048 and not ext
+            else None,
             "traffic_scope": "HBM bytes per call, every kernel of the call (rocprofv3 counters)",
             "algorithmic_flops_per_call": flops,
             "avg_call_ms": avg_call_ms,
@@ -334,7 +347,11 @@ def bench_lmhead(args, torch, cis):
             "kernel_source": kernel_source_hash(LMHEAD_SOURCES),
         },
     }
-    if not args.no_cpu_baseline:
+    if ext:
+        line["config"]["op"] = op
+        line["config"]["decoupled"] = bool(args.decoupled)
+        line["diagnostics"] = {k: stats[k] for k in ("n_trunc", "max_abs_logk", "trunc_excess")}
+    if not args.no_cpu_baseline and not ext:
         f32 = lambda x: float(np.float32(x))  # noqa: E731
         prm_ref = X.OpParams(op=X.OP_CIS, lam=f32(b.lam), kappa=f32(b.kappa), lo=0.0,
                              hi=math.inf, clip_low=f32(0.2), clip_high=f32(0.28),

@@ -32,6 +32,21 @@ from tests import parity as P
 _SHARED = {}
 
 
+def make_params(op, kw, scale, clip=(0.2, 0.28)):
+    """The same operator parameters for the device (cis_params_t) and the oracle (OpParams): the
+    float32 values the kernels use. kw overrides the defaults lam 2.3, kappa 5e-3, lo 0,
+    hi inf."""
+    import paper_2609_32444_amd as cis
+    base = dict(lam=2.3, kappa=5e-3, lo=0.0, hi=math.inf)
+    base.update(kw)
+    dev = cis.params(op, lam=base["lam"], kappa=base["kappa"], lo=base["lo"], hi=base["hi"],
+                     clip_low=clip[0], clip_high=clip[1], scale=scale)
+    ref = X.OpParams(op=op, lam=P.f32(base["lam"]), kappa=P.f32(base["kappa"]),
+                     lo=P.f32(base["lo"]), hi=P.f32(base["hi"]), clip_low=P.f32(clip[0]),
+                     clip_high=P.f32(clip[1]), scale=P.f32(scale))
+    return dev, ref
+
+
 def margin_tol(op: int) -> float:
     """Width of the band around an operator's boundary where either acted flag is correct."""
     return 1e-4 if op == X.OP_KPOP else (1e-9 if op in X.SEQ_OPS else 1e-5)

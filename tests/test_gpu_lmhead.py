@@ -32,6 +32,7 @@ from oracle import lmhead as L
 from oracle import ops as X
 from tests import parity as P
 from tests import parity_ops as PO
+from tests.parity_ops import make_params
 from workloads import make_lmhead_batch
 
 pytestmark = pytest.mark.gpu
@@ -43,17 +44,6 @@ U16 = 2.0 ** -8
 
 def f32(x):
     return float(np.float32(x))
-
-
-def make_params(op, kw, scale, clip=(0.2, 0.28)):
-    base = dict(lam=2.3, kappa=5e-3, lo=0.0, hi=math.inf)
-    base.update(kw)
-    dev = cis.params(op, lam=base["lam"], kappa=base["kappa"], lo=base["lo"], hi=base["hi"],
-                     clip_low=clip[0], clip_high=clip[1], scale=scale)
-    ref = X.OpParams(op=op, lam=f32(base["lam"]), kappa=f32(base["kappa"]), lo=f32(base["lo"]),
-                     hi=f32(base["hi"]), clip_low=f32(clip[0]), clip_high=f32(clip[1]),
-                     scale=f32(scale))
-    return dev, ref
 
 
 def host(b):

@@ -17,6 +17,7 @@ from oracle import cis as O
 from oracle import ops as X
 from tests import parity as P
 from tests import parity_ops as PO
+from tests.parity_ops import make_params
 from workloads import make_batch, make_random_batch, old_logprobs, response_offsets
 
 pytestmark = pytest.mark.gpu
@@ -48,18 +49,6 @@ SEQ_OPS = [
 
 def f32(x):
     return float(np.float32(x))
-
-
-def make_params(op, kw, scale, clip=(0.2, 0.28)):
-    """The same parameters for both sides: float32 values (what the kernels use)."""
-    base = dict(lam=2.3, kappa=5e-3, lo=0.0, hi=math.inf)
-    base.update(kw)
-    dev = cis.params(op, lam=base["lam"], kappa=base["kappa"], lo=base["lo"], hi=base["hi"],
-                     clip_low=clip[0], clip_high=clip[1], scale=scale)
-    ref = X.OpParams(op=op, lam=f32(base["lam"]), kappa=f32(base["kappa"]), lo=f32(base["lo"]),
-                     hi=f32(base["hi"]), clip_low=f32(clip[0]), clip_high=f32(clip[1]),
-                     scale=f32(scale))
-    return dev, ref
 
 
 def _dump(name, rep):
