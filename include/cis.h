@@ -65,7 +65,8 @@ enum {
                           /* workspace not 256-byte aligned                                   */
   CIS_ERR_LAUNCH = -6,    /* the HIP runtime rejected a kernel launch                         */
   CIS_ERR_WORKSPACE = -7, /* workspace smaller than cis_workspace_bytes(T)                    */
-  CIS_ERR_ALIAS = -8,     /* dlogits == logits with ld_g != ld, or a partial overlap          */
+  CIS_ERR_ALIAS = -8,     /* dlogits == logits with ld_g != ld, a partial overlap, or an
+                             LM-head gradient overlapping an operand or the workspace        */
   CIS_ERR_DEVICE = -9     /* the current device is not a gfx950 GPU, or no device            */
 };
 
@@ -334,7 +335,8 @@ int cis_lmhead_loss_fwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
  *   dweight [V, ld_dw] float32   dL/dW; ld_dw >= H. accumulate_dweight = 0 overwrites it (zeros
  *                                when T = 0), nonzero adds the gradient to its contents.
  *   workspace                    >= cis_lmhead_workspace_bytes(T, V, H, chunk, n_seq, 1)
- * dhidden and dweight must not overlap each other, the inputs or the workspace.
+ * dhidden and dweight must not overlap each other, hidden, weight or the used part of the
+ * workspace (CIS_ERR_ALIAS otherwise).
  */
 int cis_lmhead_loss_bwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
                         const void* weight, int64_t V, int64_t ld_w,

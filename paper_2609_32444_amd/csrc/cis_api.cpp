@@ -312,6 +312,22 @@ int run_loss(const LossCall& c, hipStream_t stream) {
   return launch_finalize(ws, T, c.loss_out, stream);
 }
 
+// Byte range [lo, hi) of a rows x cols matrix with a row stride of ld elements of es bytes
+// (empty for a null pointer or no rows); hi saturates at the top of the address space.
+struct Span {
+  uintptr_t lo, hi;
+};
+
+Span span_of(const void* p, int64_t rows, int64_t cols, int64_t ld, int es) {
+  if (!p || rows <= 0 || cols <= 0) return Span{0, 0};
+  const unsigned __int128 n = ((unsigned __int128)(rows - 1) * (uint64_t)ld + (uint64_t)cols) *
+                              (unsigned)es;
+  const uintptr_t lo = (uintptr_t)p;
+  return Span{lo, n > (unsigned __int128)(UINTPTR_MAX - lo) ? UINTPTR_MAX : lo + (uintptr_t)n};
+}
+
+bool overlaps(Span a, Span b) { return a.lo < b.hi && b.lo < a.hi; }
+
 // The loss on the logits hidden * W^T, a chunk of rows at a time (cis_lmhead_loss_fwd/_bwd).
 struct LmHeadCall {
   LossCall loss;            // logits / dlogits / ld unused; dtype is the chunk's (float32)
@@ -343,6 +359,14 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
   if (T > 0 && (!aligned(m.hidden, 16) || m.ld_h % 8 != 0)) return CIS_ERR_ALIGN;
   const cis::LmLayout LM = cis::lm_layout(T, V, H, m.chunk, n_seq, bwd);
   if (c.workspace_bytes < LM.total) return CIS_ERR_WORKSPACE;
+  if (bwd) {  // the gradients may not overlap each other, the operands or the workspace
+    const Span dh = span_of(m.dhidden, T, H, m.ld_dh, 4), dw = span_of(m.dweight, V, H, m.ld_dw, 4);
+    const Span ins[] = {span_of(m.hidden, T, H, m.ld_h, 2), span_of(m.weight, V, H, m.ld_w, 2),
+                        Span{(uintptr_t)c.workspace, (uintptr_t)c.workspace + LM.total}};
+    for (const Span& s : ins)
+      if (overlaps(dh, s) || overlaps(dw, s)) return CIS_ERR_ALIAS;
+    if (overlaps(dh, dw)) return CIS_ERR_ALIAS;
+  }
   DeviceInfo info;
   const int dev = current_device(&info);
   if (dev < 0) return dev;

@@ -214,10 +214,14 @@ def test_lmhead_workspace_bytes():
     assert f(T, V, H, 64, -1, True) == 0
 
 
+# distinct fake buffers for the LM-head calls, 4 GiB apart (never dereferenced)
+LM_H, LM_W, LM_DH, LM_DW, LM_WS = (k << 32 for k in range(1, 6))
+
+
 def _lm(bwd=True, **kw):
-    a = dict(hidden=FAKE, T=4, H=64, ld_h=64, weight=FAKE, V=1000, ld_w=64, ids=FAKE, linf=FAKE,
+    a = dict(hidden=LM_H, T=4, H=64, ld_h=64, weight=LM_W, V=1000, ld_w=64, ids=FAKE, linf=FAKE,
              lold=NULL, adv=FAKE, mask=NULL, offs=NULL, nseq=0, prm=_prm(), chunk=4096,
-             dh=FAKE, ld_dh=64, dw=FAKE, ld_dw=64, ws=FAKE, wsb=1 << 30)
+             dh=LM_DH, ld_dh=64, dw=LM_DW, ld_dw=64, ws=LM_WS, wsb=1 << 30)
     a.update(kw)
     pp = ctypes.byref(a["prm"]) if a["prm"] is not None else None
     lib = cis.load_library()
@@ -236,8 +240,8 @@ def _lm(bwd=True, **kw):
     (dict(ld_w=32), -2), (dict(ld_dh=32), -2), (dict(ld_dw=32), -2), (dict(chunk=0), -2),
     (dict(chunk=1 << 17), -2), (dict(H=1 << 17, ld_h=1 << 17, ld_w=1 << 17), -2),
     (dict(V=(1 << 22) + 1), -2), (dict(ld_h=(1 << 22) + 8), -2), (dict(ld_w=(1 << 22) + 8), -2),
-    (dict(ld_h=68, H=60), -5), (dict(ld_w=68, H=60), -5), (dict(hidden=FAKE + 8), -5),
-    (dict(weight=FAKE + 8), -5), (dict(ws=FAKE + 16), -5), (dict(wsb=1000), -7),
+    (dict(ld_h=68, H=60), -5), (dict(ld_w=68, H=60), -5), (dict(hidden=LM_H + 8), -5),
+    (dict(weight=LM_W + 8), -5), (dict(ws=LM_WS + 16), -5), (dict(wsb=1000), -7),
     (dict(prm=None), -1), (dict(lold=FAKE, prm=None), -1),
 ])
 def test_lmhead_argument_errors(kw, code):
@@ -256,6 +260,22 @@ def test_lmhead_fwd_needs_no_gradient_buffers():
     # a sequence operator needs logp_old and responses
     assert _lm(True, prm=_prm(op=8, hi=2.0)) == -4
     assert _lm(True, prm=_prm(op=8, hi=2.0), lold=FAKE, nseq=2, offs=FAKE) == -9
+
+
+def test_lmhead_gradient_overlaps():
+    V, ld = 1000, 64
+    w_end = LM_W + V * ld * 2                       # one past weight's last byte
+    assert _lm(True, dh=LM_H) == -8                 # dL/dh over hidden
+    assert _lm(True, dw=LM_W) == -8                 # dL/dW over weight
+    assert _lm(True, dw=w_end - 16) == -8           # dL/dW starting in weight's last row
+    assert _lm(True, dw=LM_WS + 4096) == -8         # inside the workspace
+    assert _lm(True, dh=LM_DW + 1024) == -8         # the two gradients overlap
+    assert _lm(True, dh=LM_DW - 16) == -8           # dL/dh runs into dL/dW
+    assert _lm(True, dw=w_end) == -9                # adjacent is fine
+    assert _lm(True, dw=LM_H - V * ld * 4) == -9    # ends right where hidden starts
+    # no rows: dL/dh is not written, so it may sit anywhere; the forward writes neither
+    assert _lm(True, T=0, hidden=NULL, ids=NULL, linf=NULL, adv=NULL, dh=LM_W) == -9
+    assert _lm(False, dh=LM_H, dw=LM_W) == -9
 
 
 def test_lmhead_binding_rejects_accumulating_into_nothing():
