@@ -379,6 +379,7 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
   __bf16* Ht = reinterpret_cast<__bf16*>(base + LM.ht);
   __bf16* Gb = reinterpret_cast<__bf16*>(base + LM.gb);
   float* part = reinterpret_cast<float*>(base + LM.part);
+  int* queue = reinterpret_cast<int*>(base + LM.queue);
   auto ok = [](hipError_t e) { return e == hipSuccess ? CIS_OK : CIS_ERR_LAUNCH; };
   const __bf16* hid = static_cast<const __bf16*>(m.hidden);
   const int ncu = info.num_cu;
@@ -397,7 +398,7 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
     // Z = h_c W^T (float32 logits of the chunk)
     if (int rc = ok(cis::launch_gemm_nt(
             cis::gemm_args(hc, m.weight, Z, tc, V, H, m.ld_h, m.ld_w, LM.ldz), false, nullptr,
-            ncu, stream)))
+            queue, ncu, stream)))
       return rc;
     // loss rows; the backward writes G = dL/dz in bf16 (the operand of dL/dh)
     if (int rc = launch_rows(c, ws, Z, bwd ? Gb : nullptr, LM.ldz, LM.ldv, t0, tc, dev, info,
@@ -414,18 +415,18 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
     // dL/dh_c = G W = G (W^T)^T
     if (int rc = ok(cis::launch_gemm_nt(
             cis::gemm_args(Gb, Wt, m.dhidden + t0 * m.ld_dh, tc, H, V, LM.ldv, LM.ldv, m.ld_dh),
-            false, part, ncu, stream)))
+            false, part, queue, ncu, stream)))
       return rc;
     // dL/dW (+)= G^T h_c, contracted over the chunk's rows
     if (int rc = ok(cis::launch_gemm_nt(
             cis::gemm_args(Gt, Ht, m.dweight, V, H, tc, LM.ldc, LM.ldc, m.ld_dw),
-            m.accumulate || t0 > 0, nullptr, ncu, stream)))
+            m.accumulate || t0 > 0, nullptr, queue, ncu, stream)))
       return rc;
   }
   if (bwd && T == 0 && !m.accumulate) {  // no rows: dL/dW = 0 (an empty contraction)
     if (int rc = ok(cis::launch_gemm_nt(
-            cis::gemm_args(Wt, Wt, m.dweight, V, H, 0, 8, 8, m.ld_dw), false, nullptr, ncu,
-            stream)))
+            cis::gemm_args(Wt, Wt, m.dweight, V, H, 0, 8, 8, m.ld_dw), false, nullptr, queue,
+            ncu, stream)))
       return rc;
   }
   return launch_finalize(ws, T, c.loss_out, stream);

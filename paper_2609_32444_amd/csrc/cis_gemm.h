@@ -8,7 +8,7 @@ namespace cis {
 
 // C[M, N] (float32, row stride ldc) = alpha * A[M, K] * B[N, K]^T (+ C when accumulating).
 // A and B are bf16, row-major with K contiguous (row strides lda, ldb: multiples of 8 elements,
-// bases 16-byte aligned). Any M, N, K >= 0. The last four fields are set by launch_gemm_nt.
+// bases 16-byte aligned). Any M, N, K >= 0. The fields after alpha are set by launch_gemm_nt.
 struct GemmArgs {
   const void* A;
   const void* B;
@@ -19,6 +19,8 @@ struct GemmArgs {
   bool c_vec;               // C rows and base allow 16-byte stores
   int64_t k_split;          // contraction length per split
   int64_t c_split_stride;   // elements between the splits' partial outputs
+  int64_t units;            // tiles x splits
+  int* queue;               // kGemmQueues work counters (zero at launch), or null
 };
 
 inline GemmArgs gemm_args(const void* A, const void* B, float* C, int64_t M, int64_t N,
@@ -53,6 +55,7 @@ constexpr int kGemmWaveM = 128;     // C tile per wave: 128 rows x 64 columns (8
 constexpr int kGemmWaveN = 64;
 constexpr int kGemmMaxSplits = 8;   // split-K partial buffers
 constexpr int kTransposeTile = 64;
+constexpr int kGemmQueues = 8;      // one work queue per XCD
 
 // Number of K splits launch_gemm_nt uses for an M x N x K product when given a partial buffer
 // (enough workgroups for every CU; 1 when the tiles already cover the chip).
@@ -60,8 +63,13 @@ int64_t gemm_splitk_count(int64_t M, int64_t N, int64_t K, int num_cu);
 
 // Launch on `stream`; `beta` adds the product to C instead of overwriting it. With `partial`
 // (float32, >= gemm_splitk_count(...) * M * N elements, 16-byte aligned) small products are
-// split along K and the partials summed in a fixed order.
-hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int num_cu, hipStream_t stream);
+// split along K and the partials summed in a fixed order. With `queue` (kGemmQueues ints of
+// device scratch, cleared on `stream` before the product) and more tiles than CUs, one
+// workgroup per CU takes tiles from per-XCD queues until all are taken, so XCDs that run faster
+// take over tiles of slower ones. Results do not depend on it: a tile is computed the same way
+// by whichever workgroup takes it.
+hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int* queue, int num_cu,
+                          hipStream_t stream);
 hipError_t launch_transpose(TransposeArgs t, bool in_f32, hipStream_t stream);
 
 }  // namespace cis

@@ -44,16 +44,12 @@ __device__ __forceinline__ uint32_t span_bytes(int64_t R, int64_t r0, int64_t K,
   return b > 0xFFFFFFFFll ? 0xFFFFFFFFu : (uint32_t)b;
 }
 
-// Workgroup -> (split, tile). Consecutive workgroup ids go to the 8 XCDs in turn and each XCD
-// has an L2 of its own, so the id is first remapped so that every XCD receives a contiguous run
-// of the logical order. Logically the smaller operand's tile index runs fastest: the larger
-// operand's panel is then shared by consecutive workgroups and streamed from HBM about once.
+// Logical work unit -> (split, tile). Logically the smaller operand's tile index runs fastest:
+// the larger operand's panel is then shared by consecutive units and streamed from HBM about
+// once.
 template <int BM, int BN>
-__device__ __forceinline__ void tile_of(const GemmArgs& g, int64_t& tm, int64_t& tn,
-                                        int64_t& split) {
-  const int64_t nwg = (int64_t)gridDim.x, id = blockIdx.x;
-  const int64_t per = nwg / 8, rem = nwg % 8, x = id % 8, loc = id / 8;
-  const int64_t lin = (x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per) + loc;
+__device__ __forceinline__ void unit_tile(const GemmArgs& g, int64_t lin, int64_t& tm,
+                                          int64_t& tn, int64_t& split) {
   const int64_t mt = (g.M + BM - 1) / BM, nt = (g.N + BN - 1) / BN;
   split = lin / (mt * nt);
   const int64_t t = lin % (mt * nt);
@@ -64,6 +60,35 @@ __device__ __forceinline__ void tile_of(const GemmArgs& g, int64_t& tm, int64_t&
     tn = t % nt;
     tm = t / nt;
   }
+}
+
+// Consecutive workgroup ids go to the 8 XCDs in turn and each XCD has an L2 of its own, so XCD
+// x is given the contiguous run [xcd_first(x), xcd_first(x) + xcd_count(x)) of the n units.
+__device__ __forceinline__ int64_t xcd_count(int64_t n, int x) {
+  return n / kGemmQueues + (x < n % kGemmQueues ? 1 : 0);
+}
+__device__ __forceinline__ int64_t xcd_first(int64_t n, int x) {
+  const int64_t per = n / kGemmQueues, rem = n % kGemmQueues;
+  return x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per;
+}
+
+// One workgroup per unit: workgroup id -> unit.
+__device__ __forceinline__ int64_t unit_of_workgroup() {
+  const int64_t nwg = (int64_t)gridDim.x, id = blockIdx.x;
+  return xcd_first(nwg, (int)(id % kGemmQueues)) + id / kGemmQueues;
+}
+
+// Work queues (thread 0 of a persistent workgroup): the next unit of the home XCD's run, then
+// of the other XCDs' runs in turn; -1 when all are taken. `tried` counts the runs found empty
+// (kept across calls), so a workgroup makes at most kGemmQueues failed attempts in all.
+__device__ __forceinline__ int64_t next_unit(const GemmArgs& g, int home, int& tried) {
+  while (tried < kGemmQueues) {
+    const int x = (home + tried) % kGemmQueues;
+    const int i = atomicAdd(&g.queue[x], 1);
+    if (i < xcd_count(g.units, x)) return xcd_first(g.units, x) + i;
+    ++tried;
+  }
+  return -1;
 }
 
 // One slab of MFMAs for a wave's TM x TN blocks over KS steps of 16. The fragments of step
@@ -108,15 +133,17 @@ struct Cfg {
   static_assert(BK % 16 == 0 && WM % 32 == 0 && WN % 32 == 0, "MFMA blocks");
 };
 
+// The (tm, tn) tile of C over split `split` of the contraction, by the whole workgroup. Every
+// wave passes a barrier after its last LDS access (the K loop ends on one, and there is one
+// even when K is empty) and the epilogue touches only registers and C, so the next tile may
+// refill LDS at once.
 template <int BM, int BN, int BK, int WM, int WN, bool BETA>
-__global__ __launch_bounds__((Cfg<BM, BN, BK, WM, WN>::kThreads)) void gemm_bf16_kernel(
-    const GemmArgs g) {
+__device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t tn,
+                                          int64_t split,
+                                          __bf16 (&lds)[2][(BM + BN) * (BK + 8)]) {
   using C = Cfg<BM, BN, BK, WM, WN>;
-  __shared__ __attribute__((aligned(16))) __bf16 lds[2][(BM + BN) * C::kLdw];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / C::kWavesN, wn = wave % C::kWavesN;
-  int64_t tm, tn, split;
-  tile_of<BM, BN>(g, tm, tn, split);
   const int64_t m0 = tm * BM, n0 = tn * BN;
   const int64_t kbeg = split * g.k_split;
   const int64_t kend = kbeg + g.k_split < g.K ? kbeg + g.k_split : g.K;
@@ -231,6 +258,31 @@ __global__ __launch_bounds__((Cfg<BM, BN, BK, WM, WN>::kThreads)) void gemm_bf16
   }
 }
 
+template <int BM, int BN, int BK, int WM, int WN, bool BETA, bool QUEUED>
+__global__ __launch_bounds__((Cfg<BM, BN, BK, WM, WN>::kThreads)) void gemm_bf16_kernel(
+    const GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2][(BM + BN) * (BK + 8)];
+  __shared__ int64_t unit;
+  constexpr bool queued = QUEUED;
+  const int home = (int)(blockIdx.x % kGemmQueues);
+  int tried = 0;
+  // one unit per workgroup, or (queued) units until every queue is empty: all threads read the
+  // same `unit` and leave together
+  for (int64_t u = queued ? -1 : unit_of_workgroup();;) {
+    if (queued) {
+      if (threadIdx.x == 0) unit = next_unit(g, home, tried);
+      __syncthreads();
+      u = unit;
+    }
+    if (u < 0) break;
+    int64_t tm, tn, split;
+    unit_tile<BM, BN>(g, u, tm, tn, split);
+    // gemm_tile's barriers keep thread 0's next write of `unit` after every wave's read
+    gemm_tile<BM, BN, BK, WM, WN, BETA>(g, tm, tn, split, lds);
+    if (!queued) break;
+  }
+}
+
 // C = alpha * sum_s P[s] (+ C): the split-K partials summed in split order.
 struct ReduceArgs {
   const float* P;
@@ -315,15 +367,24 @@ __global__ __launch_bounds__(256) void transpose_kernel(const TransposeArgs t) {
   }
 }
 
+// Launch over `splits` splits; with g.queue, one workgroup per CU (the LDS tile allows one)
+// works through the queues.
 template <int BM, int BN, int BK, int WM, int WN>
-hipError_t launch_cfg(GemmArgs g, bool beta, int splits, hipStream_t stream) {
+hipError_t launch_cfg(GemmArgs g, bool beta, int splits, int num_cu, hipStream_t stream) {
   const int64_t mt = (g.M + BM - 1) / BM, nt = (g.N + BN - 1) / BN;
-  const void* fn = beta ? (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, true>
-                        : (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, false>;
+  g.units = mt * nt * splits;
+  const int64_t grid = g.queue && num_cu < g.units ? num_cu : g.units;
+  const void* fn =
+      g.queue ? (beta ? (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, true, true>
+                      : (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, false, true>)
+              : (beta ? (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, true, false>
+                      : (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, false, false>);
   void* args[] = {&g};
-  return hipLaunchKernel(fn, dim3((unsigned)(mt * nt * splits)),
-                         dim3(Cfg<BM, BN, BK, WM, WN>::kThreads), args, 0, stream);
+  return hipLaunchKernel(fn, dim3((unsigned)grid), dim3(Cfg<BM, BN, BK, WM, WN>::kThreads), args,
+                         0, stream);
 }
+
+__global__ __launch_bounds__(kGemmQueues) void zero_queue_kernel(int* q) { q[threadIdx.x] = 0; }
 
 }  // namespace
 
@@ -335,18 +396,29 @@ int64_t gemm_splitk_count(int64_t M, int64_t N, int64_t K, int num_cu) {
   return s;
 }
 
-hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int num_cu,
+hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int* queue, int num_cu,
                           hipStream_t stream) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
   // A is M x K, B is N x K: the smaller one's tiles run fastest
   g.m_fastest = g.M <= g.N;
   const int64_t splits = partial ? gemm_splitk_count(g.M, g.N, g.K, num_cu) : 1;
+  const int64_t units =
+      ((g.M + kGemmTile - 1) / kGemmTile) * ((g.N + kGemmTile - 1) / kGemmTile) * splits;
+  // the queues pay off once there is more than one workgroup per CU to place
+  g.queue = units > num_cu ? queue : nullptr;
+  if (g.queue) {  // a fill kernel rather than a memset node, so the call can be graph-captured
+    void* zargs[] = {&g.queue};
+    if (hipError_t e = hipLaunchKernel((const void*)&zero_queue_kernel, dim3(1),
+                                       dim3(kGemmQueues), zargs, 0, stream))
+      return e;
+  }
   const bool c_aligned = ((uintptr_t)g.C % 16 == 0) && g.ldc % 4 == 0;
   if (splits <= 1) {
     g.k_split = g.K > 0 ? g.K : 1;
     g.c_split_stride = 0;
     g.c_vec = c_aligned;
-    return launch_cfg<kGemmTile, kGemmTile, kGemmBK, kGemmWaveM, kGemmWaveN>(g, beta, 1, stream);
+    return launch_cfg<kGemmTile, kGemmTile, kGemmBK, kGemmWaveM, kGemmWaveN>(g, beta, 1, num_cu,
+                                                                             stream);
   }
   // split-K: partial products into `partial` [splits][M][N], then summed in split order
   const int64_t kper = ((g.K + splits - 1) / splits + kGemmBK - 1) / kGemmBK * kGemmBK;
@@ -358,7 +430,7 @@ hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int num_cu,
   p.c_split_stride = g.M * g.N;
   p.c_vec = ((uintptr_t)partial % 16 == 0) && g.N % 4 == 0;
   if (hipError_t e = launch_cfg<kGemmTile, kGemmTile, kGemmBK, kGemmWaveM, kGemmWaveN>(
-          p, false, (int)splits, stream))
+          p, false, (int)splits, num_cu, stream))
     return e;
   ReduceArgs r{partial, g.C, g.M, g.N, g.ldc, g.M * g.N, (int32_t)splits, g.alpha, beta};
   const int64_t blocks = (g.M * g.N + 255) / 256;

@@ -56,7 +56,7 @@ constexpr int64_t kLmSplits = 8;
 struct LmLayout {
   WsLayout loss;
   int64_t ldz, ldv, ldc;
-  size_t z, wt, gt, ht, gb, part, total;
+  size_t z, wt, gt, ht, gb, part, queue, total;
 };
 inline LmLayout lm_layout(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_t n_seq,
                           bool bwd) {
@@ -66,7 +66,8 @@ inline LmLayout lm_layout(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_
   M.ldz = (V + 7) / 8 * 8;
   M.ldv = M.ldz;
   M.ldc = ((rows > 0 ? rows : 1) + 7) / 8 * 8;
-  M.z = align_up(M.loss.total, 256);
+  M.queue = align_up(M.loss.total, 256);  // the products' work queues
+  M.z = M.queue + 256;
   size_t end = M.z + align_up((size_t)rows * (size_t)M.ldz * 4, 256);
   M.wt = M.gt = M.ht = M.gb = M.part = end;
   if (bwd) {

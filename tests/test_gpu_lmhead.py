@@ -139,6 +139,21 @@ def test_lmhead_parity_small(name, T, V, H, chunk, gen):
     run_case(name, b, chunk=chunk)
 
 
+def test_lmhead_products_with_more_tiles_than_cus():
+    """Logits and dL/dW products of 314 tiles of 256 x 256 each (more than one per CU): their
+    workgroups take tiles from the per-XCD work queues. The full comparison with the oracle, a
+    ragged last tile in V, and a second call that must reproduce every output bit for bit
+    (whichever workgroup takes a tile computes it the same way)."""
+    b = make_lmhead_batch(512, 40000, 512, device=DEV, seed=13, min_len=16, max_len=96)
+    out, _ = run_case("queued_products", b, chunk=512)
+    prm, _ = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
+    again = cis.lmhead_loss_bwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
+                                params=prm, chunk=512)
+    torch.cuda.synchronize()
+    for k in ("logp_train", "w", "acted", "terms", "eps", "loss", "dhidden", "dweight"):
+        assert torch.equal(out[k], again[k]), k
+
+
 def test_lmhead_forward_matches_backward_and_chunking():
     b = make_lmhead_batch(300, 9001, 136, device=DEV, seed=5, min_len=16, max_len=96)
     prm, _ = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
