@@ -295,7 +295,8 @@ int cis_loss_bwd_ex(const void* logits, int dtype, int64_t T, int64_t V, int64_t
 
 /* Workspace bytes for cis_lmhead_loss_fwd (with_grad = 0) or _bwd (with_grad != 0): the loss
  * workspace of cis_workspace_bytes_ex plus the chunk's float32 logits (min(T, chunk) x V) and,
- * with gradients, W^T and two transposed chunk operands (about 2*V*H + 2*(V + H)*chunk bytes).
+ * with gradients, W^T, the chunk's bf16 dL/dz and the transposed operands of one dL/dW group
+ * (about 2*V*H + 2*V*chunk + 2*(V + H)*min(T, group) bytes; group as for cis_lmhead_loss_bwd).
  * Returns 0 for T < 0, V outside [1, 2^22], H outside [1, 2^16], chunk outside [1, 2^16] or
  * n_seq < 0. */
 size_t cis_lmhead_workspace_bytes(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_t n_seq,
@@ -333,7 +334,11 @@ int cis_lmhead_loss_fwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
  *
  *   dhidden [T, ld_dh] float32   dL/dh (overwritten; rows of invalid tokens are 0); ld_dh >= H
  *   dweight [V, ld_dw] float32   dL/dW; ld_dw >= H. accumulate_dweight = 0 overwrites it (zeros
- *                                when T = 0), nonzero adds the gradient to its contents.
+ *                                when T = 0), nonzero adds the gradient to its contents. It is
+ *                                formed by one product per group of consecutive rows, float32
+ *                                partial sums added group by group: a group is
+ *                                chunk * floor(16384 / chunk) rows when chunk is a multiple of 8
+ *                                below 16384, otherwise chunk rows.
  *   workspace                    >= cis_lmhead_workspace_bytes(T, V, H, chunk, n_seq, 1)
  * dhidden and dweight must not overlap each other, hidden, weight or the used part of the
  * workspace (CIS_ERR_ALIAS otherwise).

@@ -392,8 +392,10 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
   if (T > 0 && c.logp_old) {
     if (int rc = launch_prepass(c, ws, info, stream)) return rc;
   }
+  const int64_t group = cis::lm_dw_rows(m.chunk);  // rows per dL/dW product
   for (int64_t t0 = 0; t0 < T; t0 += m.chunk) {
     const int64_t tc = T - t0 < m.chunk ? T - t0 : m.chunk;
+    const int64_t g0 = t0 / group * group;  // first row of this chunk's dL/dW group
     const __bf16* hc = hid + t0 * m.ld_h;
     // Z = h_c W^T (float32 logits of the chunk)
     if (int rc = ok(cis::launch_gemm_nt(
@@ -405,22 +407,26 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
                              stream))
       return rc;
     if (!bwd) continue;
-    // G^T (operand of dL/dW) and h_c^T
+    // G^T and h_c^T (operands of dL/dW) into the group's columns t0 - g0 ..
     if (int rc = ok(cis::launch_transpose(
-            cis::TransposeArgs{Gb, Gt, nullptr, tc, V, LM.ldv, LM.ldc, 0}, false, stream)))
+            cis::TransposeArgs{Gb, Gt + (t0 - g0), nullptr, tc, V, LM.ldv, LM.ldc, 0}, false,
+            stream)))
       return rc;
     if (int rc = ok(cis::launch_transpose(
-            cis::TransposeArgs{hc, Ht, nullptr, tc, H, m.ld_h, LM.ldc, 0}, false, stream)))
+            cis::TransposeArgs{hc, Ht + (t0 - g0), nullptr, tc, H, m.ld_h, LM.ldc, 0}, false,
+            stream)))
       return rc;
     // dL/dh_c = G W = G (W^T)^T
     if (int rc = ok(cis::launch_gemm_nt(
             cis::gemm_args(Gb, Wt, m.dhidden + t0 * m.ld_dh, tc, H, V, LM.ldv, LM.ldv, m.ld_dh),
             false, part, queue, ncu, stream)))
       return rc;
-    // dL/dW (+)= G^T h_c, contracted over the chunk's rows
+    // dL/dW (+)= G^T h over the group's rows, once its last chunk is in
+    const int64_t gend = g0 + group < T ? g0 + group : T;
+    if (t0 + tc < gend) continue;
     if (int rc = ok(cis::launch_gemm_nt(
-            cis::gemm_args(Gt, Ht, m.dweight, V, H, tc, LM.ldc, LM.ldc, m.ld_dw),
-            m.accumulate || t0 > 0, nullptr, queue, ncu, stream)))
+            cis::gemm_args(Gt, Ht, m.dweight, V, H, gend - g0, LM.ldc, LM.ldc, m.ld_dw),
+            m.accumulate || g0 > 0, nullptr, queue, ncu, stream)))
       return rc;
   }
   if (bwd && T == 0 && !m.accumulate) {  // no rows: dL/dW = 0 (an empty contraction)

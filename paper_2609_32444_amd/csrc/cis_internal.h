@@ -39,13 +39,15 @@ inline WsLayout ws_layout(int64_t T, int64_t n_seq) {
 inline size_t ws_bytes(int64_t T) { return ws_layout(T, 0).total; }
 
 // LM-head workspace: the loss workspace above, then (256-byte aligned)
+//   Q   int[kGemmQueues]   the products' work queues (256 bytes)
 //   Z   float[rows, ldz]   the chunk's logits
 //   Wt  bf16[H, ldv]       W^T (backward)
-//   Gt  bf16[V, ldc]       (dL/dz)^T of the chunk (backward)
-//   Ht  bf16[H, ldc]       the chunk's hidden states transposed (backward)
+//   Gt  bf16[V, ldc]       (dL/dz)^T of the rows of a dL/dW group (backward)
+//   Ht  bf16[H, ldc]       their hidden states transposed (backward)
 //   Gb  bf16[rows, ldv]    dL/dz of the chunk in bf16, written by the loss rows (backward)
 //   P   float[kLmSplits, rows, H]  split-K partials of dL/dh (backward)
-// with rows = min(T, chunk) and row strides rounded up to 8 elements.
+// with rows = min(T, chunk), ldc = min(T, lm_dw_rows(chunk)) and row strides rounded up to 8
+// elements.
 constexpr int64_t kLmMaxH = int64_t(1) << 16;
 constexpr int64_t kLmMaxChunk = int64_t(1) << 16;
 // The products address a 256-row operand tile with 32-bit byte offsets, so operand row strides
@@ -53,6 +55,14 @@ constexpr int64_t kLmMaxChunk = int64_t(1) << 16;
 constexpr int64_t kLmMaxV = int64_t(1) << 22;
 constexpr int64_t kLmMaxLd = int64_t(1) << 22;
 constexpr int64_t kLmSplits = 8;
+// dL/dW is one product per group of consecutive chunks, up to kLmDwRows rows: fewer products
+// that accumulate into dL/dW. A group holds whole chunks; the chunk's columns of Gt and Ht start
+// 16-byte aligned only when chunk is a multiple of 8, otherwise a group is one chunk.
+constexpr int64_t kLmDwRows = int64_t(1) << 14;
+inline int64_t lm_dw_rows(int64_t chunk) {
+  if (chunk % 8 != 0 || chunk >= kLmDwRows) return chunk;
+  return chunk * (kLmDwRows / chunk);
+}
 struct LmLayout {
   WsLayout loss;
   int64_t ldz, ldv, ldc;
@@ -65,7 +75,8 @@ inline LmLayout lm_layout(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_
   const int64_t rows = T < chunk ? T : chunk;
   M.ldz = (V + 7) / 8 * 8;
   M.ldv = M.ldz;
-  M.ldc = ((rows > 0 ? rows : 1) + 7) / 8 * 8;
+  const int64_t grows = T < lm_dw_rows(chunk) ? T : lm_dw_rows(chunk);
+  M.ldc = ((grows > 0 ? grows : 1) + 7) / 8 * 8;
   M.queue = align_up(M.loss.total, 256);  // the products' work queues
   M.z = M.queue + 256;
   size_t end = M.z + align_up((size_t)rows * (size_t)M.ldz * 4, 256);

@@ -12,9 +12,9 @@ of dL/dh (dL/dW likewise with |G|^T |h|):
     |gpu - ref| <= (2^-8 + 4e-5 + (8 sqrt(K) + n_add) 2^-24) (|G| |W|) + 1e-30
 
 2^-8 is the unit roundoff of bf16 (8-bit significand, round to nearest even), 4e-5 covers the
-float32 G, K is the contracted length (V for dL/dh, the chunk's rows for dL/dW) and n_add the
-float32 additions of whole partial results (1 for dL/dh; the number of chunks for dL/dW, which
-is accumulated chunk by chunk). The accumulation term is the probabilistic bound of blocked
+float32 G, K is the contracted length (V for dL/dh, the rows of one dL/dW group for dL/dW) and
+n_add the float32 additions of whole partial results (1 for dL/dh; the number of groups for
+dL/dW, which is accumulated group by group). The accumulation term is the probabilistic bound of blocked
 float32 summation (sqrt(K) u with a factor of 8) rather than the worst case K u, which at
 K = 151936 would allow 0.9% and test nothing.
 """
@@ -54,6 +54,12 @@ def _dump(name, rep):
     os.makedirs(OUT, exist_ok=True)
     with open(os.path.join(OUT, f"parity_lmhead_{name}.json"), "w") as f:
         json.dump({k: v for k, v in rep.items() if not k.startswith("_")}, f, default=str)
+
+
+def dw_group(chunk, T):
+    """Rows per dL/dW product (cis_lmhead_loss_bwd in include/cis.h) and the number of them."""
+    g = chunk * (16384 // chunk) if chunk % 8 == 0 and chunk < 16384 else chunk
+    return min(g, T), (T + g - 1) // g
 
 
 def grad_bound(Gabs_B, K, n_add):
@@ -110,12 +116,12 @@ def run_case(name, b, op=X.OP_CIS, kw=None, chunk=4096, decoupled=False, seq=Fal
             near = (np.abs(res.rho - hi_c) <= 1e-5 * hi_c) | (np.abs(res.rho - lo_c) <= 1e-5 * lo_c)
             assert not near[(res.flags & 1) > 0].any(), "rows at the PPO clip edge: other seed"
         G = np.abs(res.grad)
-        nch = (b.T + chunk - 1) // chunk
+        kdw, ngr = dw_group(chunk, b.T)
         dh = out["dhidden"].cpu().double().numpy()
         dW = out["dweight"].cpu().double().numpy()
         rep["dhidden"] = check_grad("dhidden", dh, res.dhidden, grad_bound(G @ np.abs(W), b.V, 1))
         rep["dweight"] = check_grad("dweight", dW, res.dW,
-                                    grad_bound(G.T @ np.abs(h), min(chunk, b.T), nch))
+                                    grad_bound(G.T @ np.abs(h), kdw, ngr))
         inval = (res.flags & 1) == 0
         assert np.all(dh[inval] == 0), "dhidden rows of invalid tokens must be zero"
     _dump(name, rep)
@@ -170,9 +176,8 @@ def test_lmhead_forward_matches_backward_and_chunking():
     for k in ("logp_train", "w", "terms"):
         assert torch.allclose(a[k], f[k], rtol=1e-5, atol=2e-6), k
     assert torch.equal(a["acted"], f["acted"])
-    # dL/dW is summed chunk by chunk: equal up to float32 rounding of the partial sums
-    rel = (a["dweight"] - c["dweight"]).abs().max() / c["dweight"].abs().max()
-    assert rel.item() < 1e-5
+    # both chunkings form dL/dW in one product over all 300 rows (one group)
+    assert torch.equal(a["dweight"], c["dweight"])
 
 
 TOKEN_OPS = [("icepop", X.OP_ICEPOP, dict(lo=0.5, hi=5.0)), ("tis", X.OP_TIS, dict(hi=2.0)),
@@ -275,8 +280,8 @@ def test_lmhead_full_size_sampled():
     c = (b.scale * out["w"].double() * b.adv.double()).abs()
     lhs = float((dW * Wd).sum())
     rhs = float((out["dhidden"].double() * hd).sum())
-    nch = FULL_T // FULL_CHUNK
-    gam = (8 * math.sqrt(FULL_V) + 8 * math.sqrt(FULL_CHUNK) + nch + 2) * U32
+    kdw, ngr = dw_group(FULL_CHUNK, FULL_T)
+    gam = (8 * math.sqrt(FULL_V) + 8 * math.sqrt(kdw) + ngr + 2) * U32
     bound = gam * 2 * float((c * hd.abs().sum(1)).sum()) * float(Wd.abs().max())
     assert abs(lhs - rhs) <= bound, (lhs, rhs, bound)
     col = dW.sum(0)
@@ -310,7 +315,7 @@ def test_lmhead_full_size_few_valid_rows_dweight():
                 | set(b.ids.cpu().numpy()[rows].tolist()) | {0, FULL_V - 1})
     dW = out["dweight"][vs].cpu().double().numpy()
     G = np.abs(res.grad)
-    bound = grad_bound(G[:, vs].T @ np.abs(h[rows]), FULL_CHUNK, FULL_T // FULL_CHUNK)
+    bound = grad_bound(G[:, vs].T @ np.abs(h[rows]), *dw_group(FULL_CHUNK, FULL_T))
     rep = {"case": "full_size_few_valid", "dweight_rows": check_grad("dweight", dW, res.dW[vs],
                                                                       bound)}
     dh = out["dhidden"].cpu().double().numpy()
