@@ -3,18 +3,25 @@
 // for the logits of a row chunk (hidden * W^T), the gradient with respect to the hidden states
 // (G * W) and the gradient of the head weight (G^T * hidden).
 //
-// Tiling: a workgroup owns a BM x BN tile of C, split over (BM / WM) x (BN / WN) waves of
-// WM x WN, each a grid of v_mfma_f32_32x32x16_bf16 blocks. K advances BK at a time through two
-// LDS buffers: the next slab's global loads are issued before the current slab is multiplied
-// and written to the other buffer after it; within a slab the fragments of the next 16-step are
-// read while the current one is multiplied. LDS rows hold BK + 8 bf16, so that the 16-byte
-// fragment reads of a wave's lanes fall into distinct bank groups.
+// Tiling: a workgroup of 8 waves owns a 256 x 256 tile of C; each wave owns 128 x 64 as 8 x 4
+// blocks of v_mfma_f32_16x16x32_bf16 (which sustains about 98% of the matrix cores' peak on this
+// part against about 86% for the 32x32x16 form). K advances 64 at a time through a ring of two
+// LDS slabs that the buffer unit fills directly (buffer loads that write LDS: no registers
+// staged, no LDS store instructions): the next slab is requested right after the barrier that
+// frees its buffer and is multiplied one slab later. Within a slab the fragments of the second
+// 32-step are read while the first is multiplied.
 //
-// MFMA operand layout (32x32x16): lane l supplies X[i = l % 32][k = 8 (l / 32) + j], j = 0..7,
+// LDS slab: 512 rows (A's 256, then B's) of 64 bf16 = 128 bytes, unpadded because one
+// buffer->LDS instruction fills 1 KiB contiguously. The 16-byte chunk c of row r is stored at
+// chunk c ^ (r & 7): a fragment read then touches 16 rows at one logical chunk without bank
+// conflicts (measured with the LDS counters; without the swizzle every read is a 4-way
+// conflict).
+//
+// MFMA operand layout (16x16x32): lane l supplies X[i = l % 16][k = 8 (l / 16) + j], j = 0..7,
 // for both operands, and accumulator register r of lane l is the product's element
-// (i = r % 4 + 8 (r / 4) + 4 (l / 32), i' = l % 32). The B fragment is passed as the first
-// operand, so a lane's registers r = 4q .. 4q + 3 hold four consecutive columns of one row of C
-// and the epilogue stores 16 bytes at a time.
+// (i = 4 (l / 16) + r, i' = l % 16) (checked on the device against an exact integer product).
+// The B fragment is passed as the first operand, so a lane's four registers hold four
+// consecutive columns of one row of C and the epilogue stores 16 bytes at a time.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -25,7 +32,6 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -91,59 +97,80 @@ __device__ __forceinline__ int64_t next_unit(const GemmArgs& g, int home, int& t
   return -1;
 }
 
-// One slab of MFMAs for a wave's TM x TN blocks over KS steps of 16. The fragments of step
-// ks + 1 are read from LDS while step ks is multiplied (two register sets); scheduling fences
-// keep those reads ahead of the MFMAs, which the compiler would otherwise sink to just before
-// their use and wait on. fa(i, ks) / fb(j, ks) give the LDS address of a fragment.
-template <int TM, int TN, int KS, class FA, class FB>
-__device__ __forceinline__ void mfma_slab(f32x16 (&acc)[TM][TN], FA fa, FB fb) {
-  bf16x8 a[2][TM], b[2][TN];
+// Waits until at most N of this wave's buffer operations are outstanding (gfx9 encoding: vmcnt
+// in bits 3:0 and 15:14; expcnt and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// 16-byte buffer load that writes LDS: lane l stores at lds_wave + 16 l bytes (lds_wave is the
+// same for the whole wave). Counted by vmcnt. (The builtin sits in a device function of its own:
+// inside a lambda it loses its host-side declaration.)
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, __bf16* lds_wave,
+                                           uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_wave,
+                                           16, voff, 0, 0, 0);
+}
+
+// Workgroup barrier after this wave's LDS operations. __syncthreads() would also wait for every
+// buffer->LDS load still in flight; the slab waits are explicit (wait_vmcnt) instead. The memory
+// clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+constexpr int kWaves = (kGemmTile / kGemmWaveM) * (kGemmTile / kGemmWaveN);  // 8
+constexpr int kThreads = kWaves * 64;
+constexpr int kTm = kGemmWaveM / 16, kTn = kGemmWaveN / 16;                 // 8 x 4 blocks
+constexpr int kSlab = 2 * kGemmTile * kGemmBK;       // bf16 per LDS slab (A rows, B rows)
+constexpr int kLoads = 2 * kGemmTile * (kGemmBK / 8) / kThreads;  // 16-byte units per lane
+constexpr int kALoads = kLoads / 2;                  // the first half fill A's rows
+static_assert(kGemmBK == 64 && kThreads * 8 / 64 * kALoads == kGemmTile,
+              "a slab row is 8 chunks; each load covers 64 rows");
+
+// One slab of MFMAs for a wave's kTm x kTn blocks: two 32-steps, the fragments of the second
+// read from LDS while the first is multiplied. Each step's 12 reads have landed before the next
+// step's are issued: the LDS counter tracks at most 15, and with 24 in flight the compiler
+// would wait for all of them before the first MFMA. fa(i, s) / fb(j, s) give fragment addresses.
+template <class FA, class FB>
+__device__ __forceinline__ void mfma_slab(f32x4 (&acc)[kTm][kTn], FA fa, FB fb) {
+  constexpr int KS = kGemmBK / 32;
+  bf16x8 a[2][kTm], b[2][kTn];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) a[0][i] = *(const bf16x8*)fa(i, 0);
+  for (int i = 0; i < kTm; ++i) a[0][i] = *(const bf16x8*)fa(i, 0);
 #pragma unroll
-  for (int j = 0; j < TN; ++j) b[0][j] = *(const bf16x8*)fb(j, 0);
+  for (int j = 0; j < kTn; ++j) b[0][j] = *(const bf16x8*)fb(j, 0);
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     const int c = ks & 1;
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt at their maxima
+    __builtin_amdgcn_sched_barrier(0);
     if (ks + 1 < KS) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i) a[c ^ 1][i] = *(const bf16x8*)fa(i, ks + 1);
+      for (int i = 0; i < kTm; ++i) a[c ^ 1][i] = *(const bf16x8*)fa(i, ks + 1);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) b[c ^ 1][j] = *(const bf16x8*)fb(j, ks + 1);
+      for (int j = 0; j < kTn; ++j) b[c ^ 1][j] = *(const bf16x8*)fb(j, ks + 1);
     }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < kTm; ++i)
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[c][j], a[c][i], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < kTn; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[c][j], a[c][i], acc[i][j], 0, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-template <int BM, int BN, int BK, int WM, int WN>
-struct Cfg {
-  static constexpr int kWavesN = BN / WN;
-  static constexpr int kThreads = (BM / WM) * (BN / WN) * 64;
-  static constexpr int kLdw = BK + 8;     // LDS row, elements
-  static constexpr int kKv = BK / 8;      // 16-byte vectors per tile row
-  static constexpr int kAv = BM * kKv / kThreads, kBv = BN * kKv / kThreads;
-  static constexpr int kTm = WM / 32, kTn = WN / 32;
-  static_assert(BM * kKv % kThreads == 0 && BN * kKv % kThreads == 0, "staging split");
-  static_assert(BK % 16 == 0 && WM % 32 == 0 && WN % 32 == 0, "MFMA blocks");
-};
-
-// The (tm, tn) tile of C over split `split` of the contraction, by the whole workgroup. Every
-// wave passes a barrier after its last LDS access (the K loop ends on one, and there is one
-// even when K is empty) and the epilogue touches only registers and C, so the next tile may
-// refill LDS at once.
-template <int BM, int BN, int BK, int WM, int WN, bool BETA>
+// The (tm, tn) tile of C over split `split` of the contraction, by the whole workgroup. The
+// caller puts a barrier between two tiles of one workgroup (the last slab's reads must end
+// before the next tile refills LDS).
+template <bool BETA>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t tn,
-                                          int64_t split,
-                                          __bf16 (&lds)[2][(BM + BN) * (BK + 8)]) {
-  using C = Cfg<BM, BN, BK, WM, WN>;
+                                          int64_t split, __bf16 (&lds)[2 * kSlab]) {
+  constexpr int BM = kGemmTile, BN = kGemmTile, BK = kGemmBK;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / C::kWavesN, wn = wave % C::kWavesN;
+  const int wm = wave / (BN / kGemmWaveN), wn = wave % (BN / kGemmWaveN);
   const int64_t m0 = tm * BM, n0 = tn * BN;
   const int64_t kbeg = split * g.k_split;
   const int64_t kend = kbeg + g.k_split < g.K ? kbeg + g.k_split : g.K;
@@ -152,134 +179,114 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, span_bytes(g.M, m0, g.K, g.lda, 2));
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(B, span_bytes(g.N, n0, g.K, g.ldb, 2));
 
-  // staging: vector v = tid + j * kThreads holds row v / kKv, K-chunk v % kKv of the slab
-  uint32_t aoff[C::kAv], boff[C::kBv];
-#pragma unroll
-  for (int j = 0; j < C::kAv; ++j) {
-    const int v = tid + j * C::kThreads;
-    aoff[j] = (uint32_t)(((int64_t)(v / C::kKv) * g.lda + (v % C::kKv) * 8) * 2);
-  }
-#pragma unroll
-  for (int j = 0; j < C::kBv; ++j) {
-    const int v = tid + j * C::kThreads;
-    boff[j] = (uint32_t)(((int64_t)(v / C::kKv) * g.ldb + (v % C::kKv) * 8) * 2);
-  }
-  u32x4 sa[C::kAv], sb[C::kBv];
-  auto gload = [&](int64_t k0) {
-    const uint32_t ko = (uint32_t)(k0 * 2);
-#pragma unroll
-    for (int j = 0; j < C::kAv; ++j)
-      sa[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, aoff[j] + ko, 0, 0);
-#pragma unroll
-    for (int j = 0; j < C::kBv; ++j)
-      sb[j] = __builtin_amdgcn_raw_buffer_load_b128(rb, boff[j] + ko, 0, 0);
-    if (k0 + BK > kend) {
-      // the slab crosses the end of this split's K range: zero what lies past it. A vector that
-      // straddles the end is read again element by element (a 16-byte buffer load that is
-      // partly outside the resource returns zeros).
-      auto fix = [&](u32x4& x, int v, __amdgpu_buffer_rsrc_t rs, uint32_t off) {
-        const int64_t k = k0 + (v % C::kKv) * 8;
-        if (k + 8 <= kend) return;
-        bf16x8 e{};
-        for (int i = 0; i < 8; ++i)
-          if (k + i < kend)
-            e[i] = __builtin_bit_cast(
-                __bf16, (unsigned short)__builtin_amdgcn_raw_buffer_load_b16(rs, off + 2 * i, 0, 0));
-        x = __builtin_bit_cast(u32x4, e);
-      };
-#pragma unroll
-      for (int j = 0; j < C::kAv; ++j) fix(sa[j], tid + j * C::kThreads, ra, aoff[j] + ko);
-#pragma unroll
-      for (int j = 0; j < C::kBv; ++j) fix(sb[j], tid + j * C::kThreads, rb, boff[j] + ko);
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int j = 0; j < C::kAv; ++j) {
-      const int v = tid + j * C::kThreads;
-      *(u32x4*)&lds[buf][(v / C::kKv) * C::kLdw + (v % C::kKv) * 8] = sa[j];
-    }
-#pragma unroll
-    for (int j = 0; j < C::kBv; ++j) {
-      const int v = tid + j * C::kThreads;
-      *(u32x4*)&lds[buf][(BM + v / C::kKv) * C::kLdw + (v % C::kKv) * 8] = sb[j];
-    }
-  };
-
-  f32x16 acc[C::kTm][C::kTn];
-#pragma unroll
-  for (int i = 0; i < C::kTm; ++i)
-#pragma unroll
-    for (int j = 0; j < C::kTn; ++j) acc[i][j] = f32x16{};
-
+  // Load j of a wave fills the slab's 16-byte units (8 j + wave) 64 + lane: slab row
+  // r = 64 j + 8 wave + lane / 8 (A rows, then B rows from j = kALoads on), stored chunk
+  // lane % 8, holding logical chunk (lane % 8) ^ (r & 7) = (lane % 8) ^ (lane / 8 % 8).
+  // Rows past M or N read as zero through the buffer range check.
+  const int lchunk = (lane & 7) ^ ((lane >> 3) & 7);
+  const int64_t r0 = wave * 8 + (lane >> 3);
+  const uint32_t offa = (uint32_t)((r0 * g.lda + lchunk * 8) * 2);
+  const uint32_t offb = (uint32_t)((r0 * g.ldb + lchunk * 8) * 2);
+  const uint32_t stepa = (uint32_t)(64 * g.lda * 2), stepb = (uint32_t)(64 * g.ldb * 2);
+  auto off = [&](int j) { return j < kALoads ? offa + j * stepa : offb + (j - kALoads) * stepb; };
   const int64_t nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
-  if (nk > 0) {
-    gload(kbeg);
-    lstore(0);
-  }
-  __syncthreads();
-  const int fr = lane & 31, fk = 8 * (lane >> 5);
+  auto issue = [&](int64_t kt) {
+    __bf16* st = lds + (int)(kt & 1) * kSlab;
+    const int64_t k0 = kbeg + kt * BK;
+    const uint32_t ko = (uint32_t)(k0 * 2);
+    if (k0 + BK <= kend) {
+#pragma unroll
+      for (int j = 0; j < kLoads; ++j)
+        load_lds16(j < kALoads ? ra : rb, st + (j * kWaves + wave) * 512, off(j) + ko);
+    } else {
+      // the last slab of the range goes through registers: zero past kend, and a vector that
+      // straddles kend is read element by element (a 16-byte buffer load that is partly
+      // outside the resource returns zeros)
+#pragma unroll
+      for (int j = 0; j < kLoads; ++j) {
+        const __amdgpu_buffer_rsrc_t rs = j < kALoads ? ra : rb;
+        const uint32_t o = off(j) + ko;
+        const int64_t k = k0 + lchunk * 8;
+        bf16x8 e{};
+        if (k + 8 <= kend) {
+          e = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, o, 0, 0));
+        } else if (k < kend) {
+          for (int i = 0; i < 8; ++i)
+            if (k + i < kend)
+              e[i] = __builtin_bit_cast(
+                  __bf16, (unsigned short)__builtin_amdgcn_raw_buffer_load_b16(rs, o + 2 * i, 0, 0));
+        }
+        *(bf16x8*)(st + ((j * kWaves + wave) * 64 + lane) * 8) = e;
+      }
+    }
+  };
+
+  f32x4 acc[kTm][kTn];
+#pragma unroll
+  for (int i = 0; i < kTm; ++i)
+#pragma unroll
+    for (int j = 0; j < kTn; ++j) acc[i][j] = f32x4{};
+
+  // a fragment row is a multiple of 16 plus lane % 16, so its swizzle is lane & 7
+  const int fr = lane & 15, fq = lane >> 4, sw = lane & 7;
+  if (nk > 0) issue(0);
   for (int64_t kt = 0; kt < nk; ++kt) {
-    const int cur = (int)(kt & 1);
-    if (kt + 1 < nk) gload(kbeg + (kt + 1) * BK);
-    const __bf16* la = &lds[cur][(wm * WM + fr) * C::kLdw + fk];
-    const __bf16* lb = &lds[cur][(BM + wn * WN + fr) * C::kLdw + fk];
-    mfma_slab<C::kTm, C::kTn, BK / 16>(
-        acc, [&](int i, int ks) { return la + i * 32 * C::kLdw + ks * 16; },
-        [&](int j, int ks) { return lb + j * 32 * C::kLdw + ks * 16; });
-    if (kt + 1 < nk) lstore(cur ^ 1);
-    __syncthreads();
+    wait_vmcnt<0>();  // this wave's part of slab kt is in LDS
+    lds_barrier();    // every wave's is, and every wave is done with slab kt - 1's buffer
+    if (kt + 1 < nk) issue(kt + 1);
+    const __bf16* st = lds + (int)(kt & 1) * kSlab;
+    const __bf16* la = st + (wm * kGemmWaveM + fr) * BK;
+    const __bf16* lb = st + (BM + wn * kGemmWaveN + fr) * BK;
+    mfma_slab(acc, [&](int i, int s) { return la + i * 16 * BK + ((4 * s + fq) ^ sw) * 8; },
+              [&](int j, int s) { return lb + j * 16 * BK + ((4 * s + fq) ^ sw) * 8; });
   }
 
-  // epilogue: lane holds C[m][n .. n + 3] for m = row of lane, n = 8q + 4 (lane / 32)
+  // epilogue: lane holds C[m][n .. n + 3] for m = m-block row + lane % 16,
+  // n = n-block column + 4 (lane / 16)
   float* Cp = g.C + split * g.c_split_stride;
   const bool vec = g.c_vec;
 #pragma unroll
-  for (int i = 0; i < C::kTm; ++i) {
-    const int64_t m = m0 + wm * WM + i * 32 + fr;
+  for (int i = 0; i < kTm; ++i) {
+    const int64_t m = m0 + wm * kGemmWaveM + i * 16 + fr;
     if (m >= g.M) continue;
     float* crow = Cp + m * g.ldc;
 #pragma unroll
-    for (int j = 0; j < C::kTn; ++j)
+    for (int j = 0; j < kTn; ++j) {
+      const int64_t n = n0 + wn * kGemmWaveN + j * 16 + 4 * fq;
+      f32x4 v = acc[i][j] * g.alpha;
+      if (vec && n + 3 < g.N) {
+        if (BETA) v += *(const f32x4*)(crow + n);
+        *(f32x4*)(crow + n) = v;
+      } else {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t n = n0 + wn * WN + j * 32 + 8 * q + 4 * (lane >> 5);
-        f32x4 v = {acc[i][j][4 * q] * g.alpha, acc[i][j][4 * q + 1] * g.alpha,
-                   acc[i][j][4 * q + 2] * g.alpha, acc[i][j][4 * q + 3] * g.alpha};
-        if (vec && n + 3 < g.N) {
-          if (BETA) v += *(const f32x4*)(crow + n);
-          *(f32x4*)(crow + n) = v;
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (n + e < g.N) crow[n + e] = BETA ? v[e] + crow[n + e] : v[e];
-        }
+        for (int e = 0; e < 4; ++e)
+          if (n + e < g.N) crow[n + e] = BETA ? v[e] + crow[n + e] : v[e];
       }
+    }
   }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool BETA, bool QUEUED>
-__global__ __launch_bounds__((Cfg<BM, BN, BK, WM, WN>::kThreads)) void gemm_bf16_kernel(
-    const GemmArgs g) {
-  __shared__ __attribute__((aligned(16))) __bf16 lds[2][(BM + BN) * (BK + 8)];
+template <bool BETA, bool QUEUED>
+__global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(const GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) __bf16 lds[2 * kSlab];
   __shared__ int64_t unit;
-  constexpr bool queued = QUEUED;
   const int home = (int)(blockIdx.x % kGemmQueues);
   int tried = 0;
   // one unit per workgroup, or (queued) units until every queue is empty: all threads read the
   // same `unit` and leave together
-  for (int64_t u = queued ? -1 : unit_of_workgroup();;) {
-    if (queued) {
+  for (int64_t u = QUEUED ? -1 : unit_of_workgroup();;) {
+    if (QUEUED) {
       if (threadIdx.x == 0) unit = next_unit(g, home, tried);
+      // also orders the previous tile's last LDS reads before this tile's first slab
       __syncthreads();
       u = unit;
     }
     if (u < 0) break;
     int64_t tm, tn, split;
-    unit_tile<BM, BN>(g, u, tm, tn, split);
-    // gemm_tile's barriers keep thread 0's next write of `unit` after every wave's read
-    gemm_tile<BM, BN, BK, WM, WN, BETA>(g, tm, tn, split, lds);
-    if (!queued) break;
+    unit_tile<kGemmTile, kGemmTile>(g, u, tm, tn, split);
+    // at least one barrier inside keeps thread 0's next write of `unit` after every wave's read
+    gemm_tile<BETA>(g, tm, tn, split, lds);
+    if (!QUEUED) break;
   }
 }
 
@@ -367,21 +374,18 @@ __global__ __launch_bounds__(256) void transpose_kernel(const TransposeArgs t) {
   }
 }
 
-// Launch over `splits` splits; with g.queue, one workgroup per CU (the LDS tile allows one)
+// Launch over `splits` splits; with g.queue, one workgroup per CU (the LDS ring allows one)
 // works through the queues.
-template <int BM, int BN, int BK, int WM, int WN>
-hipError_t launch_cfg(GemmArgs g, bool beta, int splits, int num_cu, hipStream_t stream) {
-  const int64_t mt = (g.M + BM - 1) / BM, nt = (g.N + BN - 1) / BN;
+hipError_t launch_tiles(GemmArgs g, bool beta, int splits, int num_cu, hipStream_t stream) {
+  const int64_t mt = (g.M + kGemmTile - 1) / kGemmTile, nt = (g.N + kGemmTile - 1) / kGemmTile;
   g.units = mt * nt * splits;
   const int64_t grid = g.queue && num_cu < g.units ? num_cu : g.units;
-  const void* fn =
-      g.queue ? (beta ? (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, true, true>
-                      : (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, false, true>)
-              : (beta ? (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, true, false>
-                      : (const void*)&gemm_bf16_kernel<BM, BN, BK, WM, WN, false, false>);
+  const void* fn = g.queue ? (beta ? (const void*)&gemm_bf16_kernel<true, true>
+                                   : (const void*)&gemm_bf16_kernel<false, true>)
+                           : (beta ? (const void*)&gemm_bf16_kernel<true, false>
+                                   : (const void*)&gemm_bf16_kernel<false, false>);
   void* args[] = {&g};
-  return hipLaunchKernel(fn, dim3((unsigned)grid), dim3(Cfg<BM, BN, BK, WM, WN>::kThreads), args,
-                         0, stream);
+  return hipLaunchKernel(fn, dim3((unsigned)grid), dim3(kThreads), args, 0, stream);
 }
 
 __global__ __launch_bounds__(kGemmQueues) void zero_queue_kernel(int* q) { q[threadIdx.x] = 0; }
@@ -417,8 +421,7 @@ hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int* queue, int
     g.k_split = g.K > 0 ? g.K : 1;
     g.c_split_stride = 0;
     g.c_vec = c_aligned;
-    return launch_cfg<kGemmTile, kGemmTile, kGemmBK, kGemmWaveM, kGemmWaveN>(g, beta, 1, num_cu,
-                                                                             stream);
+    return launch_tiles(g, beta, 1, num_cu, stream);
   }
   // split-K: partial products into `partial` [splits][M][N], then summed in split order
   const int64_t kper = ((g.K + splits - 1) / splits + kGemmBK - 1) / kGemmBK * kGemmBK;
@@ -429,8 +432,7 @@ hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int* queue, int
   p.k_split = kper;
   p.c_split_stride = g.M * g.N;
   p.c_vec = ((uintptr_t)partial % 16 == 0) && g.N % 4 == 0;
-  if (hipError_t e = launch_cfg<kGemmTile, kGemmTile, kGemmBK, kGemmWaveM, kGemmWaveN>(
-          p, false, (int)splits, num_cu, stream))
+  if (hipError_t e = launch_tiles(p, false, (int)splits, num_cu, stream))
     return e;
   ReduceArgs r{partial, g.C, g.M, g.N, g.ldc, g.M * g.N, (int32_t)splits, g.alpha, beta};
   const int64_t blocks = (g.M * g.N + 255) / 256;
