@@ -162,6 +162,37 @@ __device__ __forceinline__ void mfma_slab(f32x4 (&acc)[kTm][kTn], FA fa, FB fb) 
   }
 }
 
+// Epilogue of a tile: lane holds C[m][n .. n + 3] for m = m-block row + lane % 16,
+// n = n-block column + 4 (lane / 16); 16-byte stores where the row allows them.
+template <bool BETA>
+__device__ __forceinline__ void store_tile(const GemmArgs& g, const f32x4 (&acc)[kTm][kTn],
+                                           int64_t m0, int64_t n0, int64_t split) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / (kGemmTile / kGemmWaveN), wn = wave % (kGemmTile / kGemmWaveN);
+  const int fr = lane & 15, fq = lane >> 4;
+  float* Cp = g.C + split * g.c_split_stride;
+  const bool vec = g.c_vec;
+#pragma unroll
+  for (int i = 0; i < kTm; ++i) {
+    const int64_t m = m0 + wm * kGemmWaveM + i * 16 + fr;
+    if (m >= g.M) continue;
+    float* crow = Cp + m * g.ldc;
+#pragma unroll
+    for (int j = 0; j < kTn; ++j) {
+      const int64_t n = n0 + wn * kGemmWaveN + j * 16 + 4 * fq;
+      f32x4 v = acc[i][j] * g.alpha;
+      if (vec && n + 3 < g.N) {
+        if (BETA) v += *(const f32x4*)(crow + n);
+        *(f32x4*)(crow + n) = v;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (n + e < g.N) crow[n + e] = BETA ? v[e] + crow[n + e] : v[e];
+      }
+    }
+  }
+}
+
 // The (tm, tn) tile of C over split `split` of the contraction, by the whole workgroup. The
 // caller puts a barrier between two tiles of one workgroup (the last slab's reads must end
 // before the next tile refills LDS).
@@ -241,29 +272,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t
               [&](int j, int s) { return lb + j * 16 * BK + ((4 * s + fq) ^ sw) * 8; });
   }
 
-  // epilogue: lane holds C[m][n .. n + 3] for m = m-block row + lane % 16,
-  // n = n-block column + 4 (lane / 16)
-  float* Cp = g.C + split * g.c_split_stride;
-  const bool vec = g.c_vec;
-#pragma unroll
-  for (int i = 0; i < kTm; ++i) {
-    const int64_t m = m0 + wm * kGemmWaveM + i * 16 + fr;
-    if (m >= g.M) continue;
-    float* crow = Cp + m * g.ldc;
-#pragma unroll
-    for (int j = 0; j < kTn; ++j) {
-      const int64_t n = n0 + wn * kGemmWaveN + j * 16 + 4 * fq;
-      f32x4 v = acc[i][j] * g.alpha;
-      if (vec && n + 3 < g.N) {
-        if (BETA) v += *(const f32x4*)(crow + n);
-        *(f32x4*)(crow + n) = v;
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (n + e < g.N) crow[n + e] = BETA ? v[e] + crow[n + e] : v[e];
-      }
-    }
-  }
+  store_tile<BETA>(g, acc, m0, n0, split);
 }
 
 template <bool BETA, bool QUEUED>
