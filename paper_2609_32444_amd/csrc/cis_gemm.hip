@@ -195,7 +195,7 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, const f32x4 (&acc)
 
 // The (tm, tn) tile of C over split `split` of the contraction, by the whole workgroup. The
 // caller puts a barrier between two tiles of one workgroup (the last slab's reads must end
-// before the next tile refills LDS).
+// before the next tile refills LDS; with an empty K range there is no barrier inside).
 template <bool BETA>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t tn,
                                           int64_t split, __bf16 (&lds)[2 * kSlab]) {
@@ -285,15 +285,16 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(const GemmArgs g) {
   // same `unit` and leave together
   for (int64_t u = QUEUED ? -1 : unit_of_workgroup();;) {
     if (QUEUED) {
+      // every wave has read the previous `unit` and is done with the previous tile's LDS (a
+      // tile with an empty K range has no barrier of its own)
+      __syncthreads();
       if (threadIdx.x == 0) unit = next_unit(g, home, tried);
-      // also orders the previous tile's last LDS reads before this tile's first slab
       __syncthreads();
       u = unit;
     }
     if (u < 0) break;
     int64_t tm, tn, split;
     unit_tile<kGemmTile, kGemmTile>(g, u, tm, tn, split);
-    // at least one barrier inside keeps thread 0's next write of `unit` after every wave's read
     gemm_tile<BETA>(g, tm, tn, split, lds);
     if (!QUEUED) break;
   }

@@ -221,7 +221,7 @@ def test_lmhead_empty_batch_and_accumulation():
     out = cis.lmhead_loss_bwd(h0, b.weight, ei, e, e, None, params=prm, dweight=dW)
     torch.cuda.synchronize()
     assert torch.all(out["dweight"] == 0.0) and float(out["loss"].item()) == 0.0
-    # accumulate: dW0 + the gradient, summed onto dW0 chunk by chunk (3 chunks)
+    # accumulate: dW0 + the gradient (3 chunks of 32 rows, one dL/dW group)
     args = (b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask)
     dW0 = torch.randn(1000, 64, device=DEV) * 1e-3
     acc = cis.lmhead_loss_bwd(*args, params=prm, chunk=32, dweight=dW0.clone(),
@@ -233,8 +233,23 @@ def test_lmhead_empty_batch_and_accumulation():
                             b.adv.cpu().double().numpy(), b.mask.cpu().numpy(), prm_ref,
                             keep_grad=True)
     d0 = dW0.cpu().double().numpy()
-    bound = grad_bound(np.abs(res.grad).T @ np.abs(h), 32, 3) + 4 * U32 * np.abs(d0)
+    bound = grad_bound(np.abs(res.grad).T @ np.abs(h), *dw_group(32, b.T)) + 4 * U32 * np.abs(d0)
     check_grad("dweight_accumulated", acc.cpu().double().numpy(), d0 + res.dW, bound)
+
+
+def test_lmhead_empty_batch_zero_dweight_from_work_queues():
+    """No rows and a head of 157 x 2 tiles of 256 x 256 (more than one per CU): dL/dW = 0 comes
+    from a product with an empty contraction whose tiles are taken from the work queues."""
+    W = torch.randn(40000, 512, device=DEV).to(torch.bfloat16)
+    prm, _ = make_params(X.OP_CIS, dict(lam=1.0, kappa=0.005), -1.0)
+    e = torch.empty(0, device=DEV)
+    ei = torch.empty(0, dtype=torch.int64, device=DEV)
+    h0 = torch.empty(0, 512, dtype=torch.bfloat16, device=DEV)
+    for _ in range(2):
+        dW = torch.full((40000, 512), 3.0, device=DEV)
+        out = cis.lmhead_loss_bwd(h0, W, ei, e, e, None, params=prm, dweight=dW)
+        torch.cuda.synchronize()
+        assert torch.all(out["dweight"] == 0.0) and float(out["loss"].item()) == 0.0
 
 
 # ------------------------------------------------------------------------------------------
