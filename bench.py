@@ -321,6 +321,7 @@ def bench_lmhead(args, torch, cis):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
+        # the dominant arithmetic: bf16 matrix-core products (float32 accumulation)
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"moe-rollout LM head T={T} V={V} H={H} bf16 chunk={chunk} "
@@ -474,9 +475,11 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if esize == 2 else "f32",
+        # the arithmetic: float32 throughout (logits widened on load, gradients rounded on store)
+        "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": workload, "T": T, "V": V, "valid_tokens": n_valid,
+                   "storage": "bf16" if esize == 2 else "f32",
                    "lambda": b.lam, "kappa": b.kappa, "seed": b.meta["seed"]},
         "roofline": {
             "bound": "hbm",
