@@ -31,6 +31,19 @@ from oracle import cis as O
 F32_TINY = 2.0 ** -126
 
 
+def write_report(filename: str, report: dict) -> None:
+    """Writes a test's comparison report as JSON into the directory named by the environment
+    variable CIS_PARITY_REPORT_DIR; nothing is written when it is not set."""
+    import json
+    out = os.environ.get("CIS_PARITY_REPORT_DIR")
+    if not out:
+        return
+    os.makedirs(out, exist_ok=True)
+    rep = {k: v for k, v in report.items() if not str(k).startswith("_")}
+    with open(os.path.join(out, filename), "w") as f:
+        json.dump(rep, f, indent=1, default=str)
+
+
 def host_logits(logits: torch.Tensor):
     """Host copy of device logits whose rows read exactly as float64: a Bf16Matrix of the
     bfloat16 bit patterns, or a float64 array for float32 logits."""

@@ -19,9 +19,7 @@ float32 summation (sqrt(K) u with a factor of 8) rather than the worst case K u,
 K = 151936 would allow 0.9% and test nothing.
 """
 
-import json
 import math
-import os
 
 import numpy as np
 import pytest
@@ -37,7 +35,6 @@ from workloads import make_lmhead_batch
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
-OUT = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "gpurun_out")
 U32 = 2.0 ** -24
 U16 = 2.0 ** -8
 
@@ -51,9 +48,7 @@ def host(b):
 
 
 def _dump(name, rep):
-    os.makedirs(OUT, exist_ok=True)
-    with open(os.path.join(OUT, f"parity_lmhead_{name}.json"), "w") as f:
-        json.dump({k: v for k, v in rep.items() if not k.startswith("_")}, f, default=str)
+    P.write_report(f"parity_lmhead_{name}.json", rep)
 
 
 def dw_group(chunk, T):

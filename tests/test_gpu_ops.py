@@ -4,9 +4,7 @@ decoupled path, the sequence operators over packed responses, cis_weights_ex on 
 log-probabilities (with saturated probabilities), float32 logits, long rows, and the
 decoupled path at the full MoE-rollout size on sampled rows."""
 
-import json
 import math
-import os
 
 import numpy as np
 import pytest
@@ -22,7 +20,6 @@ from workloads import make_batch, make_random_batch, old_logprobs, response_offs
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
-OUT = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "gpurun_out")
 
 # (operator, bounds) at update ratio 1; bounds other than the paper's defaults put many tokens
 # on both sides of them
@@ -52,10 +49,7 @@ def f32(x):
 
 
 def _dump(name, rep):
-    os.makedirs(OUT, exist_ok=True)
-    rep = {k: v for k, v in rep.items() if not k.startswith("_")}
-    with open(os.path.join(OUT, f"parity_ops_{name}.json"), "w") as f:
-        json.dump(rep, f, default=str)
+    P.write_report(f"parity_ops_{name}.json", rep)
 
 
 def run_case(name, b, op, kw, logp_old=None, offsets=None, bwd=True, rows=None):

@@ -7,7 +7,6 @@ seeded sample of rows that always includes the first and last rows and the heavy
 """
 
 import json
-import os
 
 import numpy as np
 import pytest
@@ -19,13 +18,8 @@ from workloads import make_batch
 
 pytestmark = pytest.mark.gpu
 
-OUT = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "gpurun_out")
-
-
 def _record(name, report):
-    os.makedirs(OUT, exist_ok=True)
-    with open(os.path.join(OUT, f"parity_{name}.json"), "w") as f:
-        json.dump(report, f, indent=1, default=float)
+    P.write_report(f"parity_{name}.json", report)
     print(name, json.dumps(report, default=float), flush=True)
 
 
