@@ -11,7 +11,7 @@ softmax(z + delta) at temperature 1 (Gumbel-max, exact), and the recorded infere
 log-probability is log_softmax(z + delta)[y] (App. C.4: the raw value from the sampling step).
 Advantages are GRPO group-normalised binary rewards (Sec. 2.1).
 
-Configurations (the sizes of the five workloads this build is measured and checked on):
+Configurations (the sizes of the five workloads the library is measured and checked on):
 
   0  tiny:    T = 256 (1 prompt x 4 responses x 64 tokens), V = 1024, float32 logits
               z ~ N(0, 3^2); delta ~ N(0, 0.02^2) per logit, and 1% of the rows (3) get
