@@ -192,8 +192,10 @@ def cpu_baseline(b, V: int, target_s: float = 15.0):
     except OSError:
         pass
     return {"value": n / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"{n} random valid rows of the same batch, float64 oracle with gradient, "
-                      f"{cores} worker processes, {dt:.1f} s wall ({per_row * n:.0f} s CPU est.)",
+            "sample": (f"all {n} valid rows of the batch" if n == len(rows_all) else
+                       f"{n} random valid rows of the same batch")
+                      + f", float64 oracle with gradient, {cores} worker processes, {dt:.1f} s wall "
+                        f"({per_row * n:.0f} s CPU est.)",
             "cpu_model": model}
 
 
