@@ -1,6 +1,6 @@
 """Plain float64 CPU oracle for the CIS token loss, forward and backward.
 
-TEST INFRASTRUCTURE ONLY. This package is the checker, not the product: only the test
+TEST INFRASTRUCTURE ONLY. This package checks the product and is not part of it: only the test
 suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may import it.
 The HIP library never calls it, and it shares no code, tables or constants with it.
 
