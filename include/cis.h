@@ -37,6 +37,9 @@
  *   - Data errors (ids out of range on unmasked rows, non-finite rows) are not return codes:
  *     they are counted in the cis_stats_t at the start of the workspace (below).
  *   - Results are deterministic: repeated calls on the same inputs give identical bits.
+ *   - A call issues kernel launches only (no memset or copy operations), so it can be captured
+ *     into a HIP graph on `stream` and replayed; a replay reads the buffers as they are then.
+ *     The workspace must not be shared by two graphs or calls that may run concurrently.
  */
 #ifndef CIS_H
 #define CIS_H
