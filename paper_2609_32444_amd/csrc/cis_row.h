@@ -352,9 +352,14 @@ __device__ __forceinline__ void stream_lse(__amdgpu_buffer_rsrc_t rs, const RowG
                                            uint32_t voff, int V, int y, float& m, float& s,
                                            float& zy_mine) {
   constexpr int EPV = E::kPerVec;
+  // Two-level sum: the exponentials of kFold consecutive slots go into a partial that is then
+  // added to the thread's total. With one float32 accumulator, a long row (2^28 logits: 2^18 per
+  // thread) would round away every term below half an ulp of the growing total.
+  constexpr uint32_t kFold = 64;
   const uint32_t end = (uint32_t)g.nvec * 16u, step = (uint32_t)(BLOCK * 16);
   uint32_t o = voff + (uint32_t)g.sbeg * step;
   u32x4 cur = PIPE ? bload(rs, o < end ? o : kOutOfRange, 0u) : u32x4{0u, 0u, 0u, 0u};
+  float part = 0.f;  // both relative to the running max m
   for (; o < end; o += step) {
     u32x4 nxt = cur;
     if (PIPE)
@@ -379,13 +384,19 @@ __device__ __forceinline__ void stream_lse(__amdgpu_buffer_rsrc_t rs, const RowG
       }
     }
     const float mb = mv * kLog2e;
-    float acc = s * fast_exp2((m - mv) * kLog2e);
+    const float sc = fast_exp2((m - mv) * kLog2e);
+    float acc = part * sc;
 #pragma unroll
     for (int e = 0; e < EPV; ++e) acc += fast_exp2(__builtin_fmaf(f[e], kLog2e, -mb));
-    s = acc;
+    s *= sc;
+    // slot (o - voff) / step ends a group of kFold: move the partial into the total
+    const bool fold = (((o - voff) / step) % kFold) == kFold - 1;
+    s = fold ? s + acc : s;
+    part = fold ? 0.f : acc;
     m = mv;
     cur = nxt;
   }
+  s += part;
 }
 
 // Per-row inputs other than the logits. Each workgroup fetches them one row ahead, so their

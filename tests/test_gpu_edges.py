@@ -84,6 +84,16 @@ def test_forward_only_matches(V, dtype):
     run_and_check(b, bwd=False)
 
 
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_largest_vocabulary(dtype):
+    """V = 2^28, the largest the ABI accepts (a row's byte offsets stay within 32 bits; 2^28 + 1
+    is refused, tests/test_abi_cpu.py): two rows of 512 MB (bf16) or 1 GB (float32) through the
+    streamed row path, fused and forward only, every element against the oracle."""
+    b = make_random_batch(2, 1 << 28, dtype=dtype, device=DEV, seed=71)
+    run_and_check(b)
+    run_and_check(b, bwd=False)
+
+
 def test_empty_batch():
     b = make_random_batch(1, 16, torch.bfloat16, DEV, seed=1)
     z = b.logits[:0]
