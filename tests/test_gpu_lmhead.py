@@ -155,6 +155,14 @@ def test_lmhead_products_with_more_tiles_than_cus():
         assert torch.equal(out[k], again[k]), k
 
 
+def test_lmhead_largest_vocabulary():
+    """V = 2^22, the largest vocabulary the LM-head calls accept: float32 logit rows of 16 MB
+    through the streamed row path, a logits product of 16384 tiles, dL/dh split along V into
+    2^19-long contractions and dL/dW over all 2^22 rows, every output against the oracle."""
+    b = make_lmhead_batch(64, 1 << 22, 64, device=DEV, seed=17, min_len=16, max_len=32)
+    run_case("max_vocab", b, chunk=64)
+
+
 def test_lmhead_forward_matches_backward_and_chunking():
     b = make_lmhead_batch(300, 9001, 136, device=DEV, seed=5, min_len=16, max_len=96)
     prm, _ = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
