@@ -163,6 +163,14 @@ def test_lmhead_largest_vocabulary():
     run_case("max_vocab", b, chunk=64)
 
 
+def test_lmhead_largest_chunk():
+    """chunk = 2^16, the largest the LM-head calls accept, over a batch of exactly that many
+    rows: one logits product of 65536 rows and one dL/dW group of K = 65536, against the
+    oracle."""
+    b = make_lmhead_batch(1 << 16, 1000, 64, device=DEV, seed=19, min_len=64, max_len=512)
+    run_case("max_chunk", b, chunk=1 << 16)
+
+
 def test_lmhead_forward_matches_backward_and_chunking():
     b = make_lmhead_batch(300, 9001, 136, device=DEV, seed=5, min_len=16, max_len=96)
     prm, _ = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
