@@ -32,8 +32,10 @@
  *   - All array pointers are DEVICE pointers owned by the caller; the library never frees or
  *     retains them and never allocates device memory.
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null stream). The return
- *     value reports argument and launch errors only; it never synchronises. On a nonzero
- *     return nothing has been launched and no output has been written.
+ *     value reports argument and launch errors only; it never synchronises. Arguments are
+ *     checked before the first launch: on any error other than CIS_ERR_LAUNCH nothing has
+ *     been launched and no output has been written. CIS_ERR_LAUNCH means the runtime refused
+ *     a launch; kernels queued before it may have run, so the outputs are undefined.
  *   - Data errors (ids out of range on unmasked rows, non-finite rows) are not return codes:
  *     they are counted in the cis_stats_t at the start of the workspace (below).
  *   - Results are deterministic: repeated calls on the same inputs give identical bits.
