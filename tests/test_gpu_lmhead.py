@@ -171,6 +171,23 @@ def test_lmhead_largest_chunk():
     run_case("max_chunk", b, chunk=1 << 16)
 
 
+def test_lmhead_largest_hidden_size():
+    """H = 2^16, the largest hidden size the LM-head calls accept: logits contracted over 65536
+    (1024 slabs), dL/dh and dL/dW 256 tiles wide. The per-token inputs come from a small batch;
+    hidden and weight entries are {-1, 0, 1} * 2^-3, so every float32 partial sum of a logit is
+    an integer multiple of 2^-6 below 2^17 in magnitude, exact, and the logits equal the
+    oracle's float64 ones as with make_lmhead_batch."""
+    import dataclasses
+    T, V, H = 64, 1000, 1 << 16
+    b0 = make_lmhead_batch(T, V, 64, device=DEV, seed=29, min_len=16, max_len=32)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(30)
+    h = (torch.randint(-1, 2, (T, H), generator=g, device=DEV).float() * 0.125).to(torch.bfloat16)
+    W = (torch.randint(-1, 2, (V, H), generator=g, device=DEV).float() * 0.125).to(torch.bfloat16)
+    b = dataclasses.replace(b0, hidden=h, weight=W)
+    run_case("max_hidden", b, chunk=64)
+
+
 def test_lmhead_forward_matches_backward_and_chunking():
     b = make_lmhead_batch(300, 9001, 136, device=DEV, seed=5, min_len=16, max_len=96)
     prm, _ = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
