@@ -1,8 +1,11 @@
 """bench.py's checks that need no GPU: the one-GPU refusal and the source hash that ties the
 committed traffic records to the kernels they were measured on."""
 
+import glob
 import json
 import os
+import re
+import shlex
 import subprocess
 import sys
 
@@ -44,3 +47,21 @@ def test_traffic_records_name_their_source_and_summary():
         for r in recs:
             assert len(r["source_hash"]) == 16
             assert os.path.isfile(os.path.join(ROOT, r["summary"]))
+
+
+def test_profile_commands_run_committed_files():
+    """Every command in a profile summary runs bench.py (a committed file) with options that
+    bench.py accepts, directly after rocprofv3's `--`."""
+    ap = bench.make_parser()
+    found = 0
+    for md in glob.glob(os.path.join(ROOT, "profiles", "*.md")):
+        text = open(md).read()
+        for block in re.findall(r"```\n(.*?)```", text, flags=re.S):
+            for line in block.strip().splitlines():
+                words = shlex.split(line)
+                if words[0] == "rocprofv3":
+                    words = words[words.index("--") + 1:]
+                assert words[:2] == ["python3", "bench.py"], (md, line)
+                ap.parse_args(words[2:])
+                found += 1
+    assert found >= 10
