@@ -10,7 +10,7 @@ Prints one JSON line. `roofline` refers to the fused row kernel: algorithmic byt
 the average call time measured with HIP events on the stream the kernels run on (the call also
 contains the tiny loss-reduction kernel, so this slightly understates the row kernel's rate).
 `cpu_baseline` times the float64 CPU oracle on a bounded sample of the same rows, on the host's
-cores.
+cores, and also states its rate as the GB/s of the same algorithmic bytes per token.
 
     python bench.py [--steps K] [--warmup W] [--c C] [--mode bwd|fwd] [--config N]
                     [--op NAME] [--decoupled] [--no-cpu-baseline] [--no-copy-ceiling]
@@ -191,7 +191,10 @@ def cpu_baseline(b, V: int, target_s: float = 15.0):
                 break
     except OSError:
         pass
+    # the oracle's rate in the HBM terms of the roofline: the same algorithmic bytes per token
+    per_tok = algorithmic_bytes(1, 0, V, b.logits.element_size(), True)
     return {"value": n / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "equivalent_gbs": n / dt * per_tok / 1e9,
             "sample": (f"all {n} valid rows of the batch" if n == len(rows_all) else
                        f"{n} random valid rows of the same batch")
                       + f", float64 oracle with gradient, {cores} worker processes, {dt:.1f} s wall "
@@ -244,7 +247,10 @@ def cpu_baseline_lmhead(b, prm_ref, target_s: float = 40.0):
     t0 = time.perf_counter()
     run(rows)
     dt = time.perf_counter() - t0
+    # the oracle's rate in the HBM terms of the roofline: the same algorithmic bytes per token
+    per_tok = algorithmic_bytes(1, 0, V, b.logits.element_size(), True)
     return {"value": n / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "equivalent_gbs": n / dt * per_tok / 1e9,
             "sample": f"{n} random rows of the same batch through oracle.lmhead (float64 logits, "
                       f"loss, dL/dh and dL/dW of those rows), one process, BLAS on {cores} "
                       f"threads, {dt:.1f} s wall"}
