@@ -216,6 +216,32 @@ def test_weights_kernel_matches_oracle():
         assert np.all((tr == tr64) | (margin < 1e-5))
 
 
+def test_weights_beyond_2_31_tokens():
+    """T = 2^31 + 2^24 tokens (about 30 GB of device arrays): the elementwise weights kernel
+    indexes in 64 bits. Outputs are compared with the oracle on the first and last 2^20 tokens
+    and on 2^20 random ones."""
+    T = (1 << 31) + (1 << 24)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(5)
+    lt = torch.rand(T, generator=g, device=DEV).mul_(-6.0)          # log p in (-6, 0]
+    li = torch.randn(T, generator=g, device=DEV).neg_().add_(lt)    # log q = log p - N(0, 1)
+    mask = (torch.rand(T, generator=g, device=DEV) > 0.1).to(torch.uint8)
+    lam, kappa = 2.3, 5e-3
+    w, tr = cis.weights(lt, li, mask, lam=lam, kappa=kappa)
+    idx = torch.cat([torch.arange(0, 1 << 20, device=DEV),
+                     torch.arange(T - (1 << 20), T, device=DEV),
+                     torch.randint(0, T, (1 << 20,), generator=g, device=DEV)])
+    lt64, li64 = lt[idx].double().cpu().numpy(), li[idx].double().cpu().numpy()
+    m = mask[idx].cpu().numpy()
+    w64, tr64 = O.cis_weights(lt64, li64, m, float(np.float32(lam)), float(np.float32(kappa)))
+    wg = w[idx].double().cpu().numpy()
+    tg = tr[idx].cpu().numpy().astype(bool)
+    assert np.all(np.abs(wg - w64) <= 1e-5 * np.abs(w64) + 1e-38)
+    phi = np.maximum(-np.expm1(lt64), np.float32(kappa))
+    margin = np.abs((lt64 - li64) - np.log1p(np.float32(lam) * phi))
+    assert np.all((tg == tr64) | (margin < 1e-5))
+
+
 def test_binding_errors():
     b = make_random_batch(4, 64, torch.bfloat16, DEV, seed=1)
     with pytest.raises(cis.CisError) as e:
