@@ -139,20 +139,44 @@ def bandwidth_ceilings(rows: int, row_bytes: int, torch) -> dict:
     return out
 
 
+MAX_WORKERS = 16   # the host CPU share of one GPU on the measurement boxes
+
+
+def host_cpu():
+    """(cores this process may run on, /proc/cpuinfo model name and family/model numbers)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    info = {}
+    try:
+        for line in open("/proc/cpuinfo"):
+            k, _, v = line.partition(":")
+            k = k.strip()
+            if k in ("model name", "cpu family", "model", "stepping") and k not in info:
+                info[k] = v.strip()
+            if len(info) == 4:
+                break
+    except OSError:
+        pass
+    model = info.get("model name", "")
+    if "cpu family" in info:
+        model += f" (family {info['cpu family']}, model {info.get('model', '?')}, " \
+                 f"stepping {info.get('stepping', '?')})"
+    return n, model
+
+
 def cpu_baseline(b, V: int, target_s: float = 15.0):
     """The oracle as it stands (float64, with the gradient) on a sample of rows, in a process
-    pool over the host cores; sized to roughly target_s of CPU time."""
+    pool over the host cores (at most MAX_WORKERS); sized to roughly target_s of CPU time."""
     import multiprocessing as mp
 
     import numpy as np
 
     from oracle import cis as O
 
-    try:
-        cores = len(os.sched_getaffinity(0))
-    except AttributeError:
-        cores = os.cpu_count() or 1
-    cores = max(1, min(cores, 16))
+    host_cores, model = host_cpu()
+    cores = max(1, min(host_cores, MAX_WORKERS))
     # probe one row to size the sample
     rows_all = np.nonzero(b.mask.cpu().numpy())[0]
     rng = np.random.default_rng(0)
@@ -183,22 +207,16 @@ def cpu_baseline(b, V: int, target_s: float = 15.0):
     with ctx.Pool(cores) as pool:
         pool.map(_baseline_worker, blocks)
     dt = time.perf_counter() - t0
-    model = ""
-    try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                model = line.split(":", 1)[1].strip()
-                break
-    except OSError:
-        pass
     # the oracle's rate in the HBM terms of the roofline: the same algorithmic bytes per token
     per_tok = algorithmic_bytes(1, 0, V, b.logits.element_size(), True)
     return {"value": n / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "equivalent_gbs": n / dt * per_tok / 1e9,
             "sample": (f"all {n} valid rows of the batch" if n == len(rows_all) else
                        f"{n} random valid rows of the same batch")
-                      + f", float64 oracle with gradient, {cores} worker processes, {dt:.1f} s wall "
-                        f"({per_row * n:.0f} s CPU est.)",
+                      + f", float64 oracle with gradient, {cores} worker processes "
+                        f"(the pool is held to {MAX_WORKERS}; this process may run on "
+                        f"{host_cores} cores), {dt:.1f} s wall ({per_row * n:.0f} s CPU est.)",
+            "host_cores": host_cores,
             "cpu_model": model}
 
 
@@ -222,10 +240,7 @@ def cpu_baseline_lmhead(b, prm_ref, target_s: float = 40.0):
 
     from oracle import lmhead as L
 
-    try:
-        cores = len(os.sched_getaffinity(0))
-    except AttributeError:
-        cores = os.cpu_count() or 1
+    cores, model = host_cpu()
     W = b.weight.float().cpu().double().numpy()
     h = b.hidden.float().cpu().double().numpy()
     ids = b.ids.cpu().numpy()
@@ -247,13 +262,26 @@ def cpu_baseline_lmhead(b, prm_ref, target_s: float = 40.0):
     t0 = time.perf_counter()
     run(rows)
     dt = time.perf_counter() - t0
-    # the oracle's rate in the HBM terms of the roofline: the same algorithmic bytes per token
-    per_tok = algorithmic_bytes(1, 0, V, b.logits.element_size(), True)
-    return {"value": n / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "equivalent_gbs": n / dt * per_tok / 1e9,
+    # the oracle's rate in the terms of the roofline: the three products' FLOPs per token
+    flops_per_tok = 3 * 2.0 * b.V * b.H
+    threads = blas_threads(cores)
+    return {"value": n / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "equivalent_tflops": n / dt * flops_per_tok / 1e12,
             "sample": f"{n} random rows of the same batch through oracle.lmhead (float64 logits, "
-                      f"loss, dL/dh and dL/dW of those rows), one process, BLAS on {cores} "
-                      f"threads, {dt:.1f} s wall"}
+                      f"loss, dL/dh and dL/dW of those rows), one process, BLAS on {threads} "
+                      f"threads ({cores} cores available), {dt:.1f} s wall",
+            "host_cores": cores,
+            "cpu_model": model}
+
+
+def blas_threads(cores: int) -> int:
+    """Threads numpy's BLAS runs on: OMP_NUM_THREADS / OPENBLAS_NUM_THREADS when set (the
+    measurement boxes set them to the CPU share of one GPU), else the available cores."""
+    for k in ("OPENBLAS_NUM_THREADS", "OMP_NUM_THREADS"):
+        v = os.environ.get(k, "")
+        if v.isdigit() and int(v) > 0:
+            return min(int(v), cores)
+    return cores
 
 
 def bench_lmhead(args, torch, cis):
@@ -263,15 +291,10 @@ def bench_lmhead(args, torch, cis):
     from oracle import ops as X
     from workloads import make_lmhead_batch
 
-    spec = {2: (16384, 151936)}.get(args.config)
-    if spec is None:
-        raise SystemExit("--lmhead runs the MoE-rollout shape (--config 2)")
-    T, V = spec
+    T, V = 16384, 151936
     H, chunk = args.hidden, args.chunk
     ext = args.op is not None or args.decoupled
     op = args.op or "cis"
-    if op in ("seq_tis", "seq_mis") and not args.decoupled:
-        raise SystemExit("sequence operators need --decoupled")
     b = make_lmhead_batch(T, V, H, device="cuda", seed=2, c=args.c,
                           old_sd=0.3 if args.decoupled else None)
     bwd = args.mode == "bwd"
@@ -392,13 +415,25 @@ def make_parser() -> argparse.ArgumentParser:
     return ap
 
 
-def main():
-    args = make_parser().parse_args()
-
+def check_args(ap: argparse.ArgumentParser, args) -> None:
+    """Rejects option combinations that bench.py does not run (exit status 2, before any
+    device work)."""
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the CIS loss is measured on one MI355X "
               "(multi-GPU sharding is a design note only)", file=sys.stderr)
         sys.exit(2)
+    if args.op in ("seq_tis", "seq_mis") and not args.decoupled:
+        ap.error("sequence operators need --decoupled")
+    if args.lmhead and args.config != 2:
+        ap.error("--lmhead runs the MoE-rollout shape (--config 2)")
+    if args.config not in (0, 1, 2, 3, 4):
+        ap.error("--config is one of 0..4")
+
+
+def main():
+    ap = make_parser()
+    args = ap.parse_args()
+    check_args(ap, args)
 
     import torch
 
@@ -423,8 +458,6 @@ def main():
     bwd = args.mode == "bwd"
     ext = args.op is not None or args.decoupled
     op = args.op or "cis"
-    if op in ("seq_tis", "seq_mis") and not args.decoupled:
-        ap.error("sequence operators need --decoupled")
     if ext:
         from workloads import old_logprobs, response_offsets
         lo, hi = OP_BOUNDS.get(op, (0.0, math.inf))

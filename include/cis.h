@@ -38,6 +38,11 @@
  *     a launch; kernels queued before it may have run, so the outputs are undefined.
  *   - Data errors (ids out of range on unmasked rows, non-finite rows) are not return codes:
  *     they are counted in the cis_stats_t at the start of the workspace (below).
+ *   - The row kernels read a uint8 mask through scalar loads of the aligned 4-byte words that
+ *     hold its bytes, so up to 3 bytes before mask[0] and after mask[T-1] are read (and
+ *     ignored). Those bytes must be mapped: any hipMalloc allocation or caching-allocator
+ *     block (PyTorch's are 512-byte granular) satisfies this; a mask placed within 3 bytes of
+ *     the end of a mapped range does not.
  *   - Results are deterministic: repeated calls on the same inputs give identical bits.
  *   - A call issues kernel launches only (no memset or copy operations), so it can be captured
  *     into a HIP graph on `stream` and replayed; a replay reads the buffers as they are then.
@@ -77,13 +82,13 @@ enum {
 
 /* Per-call statistics, written at byte offset 0 of the workspace by every entry point that
  * takes a workspace, once every row is done (read it after synchronising the stream). The
- * last three fields are the training diagnostics of App. D.4/D.5. */
+ * last three fields are the training diagnostics of App. D.1/D.5. */
 typedef struct cis_stats {
   double  loss;         /* sum_t term_t, accumulated in double in a fixed order             */
   int64_t n_valid;      /* rows with mask != 0 and 0 <= id < V                              */
   int64_t n_bad_id;     /* rows with mask != 0 and id outside [0, V)                        */
   int64_t n_nonfinite;  /* valid rows whose log-sum-exp is not finite or whose w is NaN     */
-  int64_t n_trunc;      /* valid rows the operator acted on ("acted on", App. D.4): for CIS */
+  int64_t n_trunc;      /* valid rows the operator acted on ("acted on", App. D.1): for CIS */
                         /* the truncated rows (k > 1 + lambda*phi)                          */
   double  max_abs_logk; /* largest |log k_t| over valid rows (NaN ignored; 0 if none)      */
   double  trunc_excess; /* sum over valid rows of (k_t - w_t) in double, fixed order        */

@@ -28,10 +28,10 @@ What it restates (arXiv 2609.32444):
 * The q-fixed cap: holding q fixed instead of p, a displacement threshold eps <= c maps through
   Lemma 1 to k <= 1 / (q + (1 - q) e^{-c}); here c = log(1 + lambda), so at kappa = 0 it truncates
   exactly the tokens that CIS truncates.
-* App. D.4 (training statistics table and dynamics figure) and App. D.5: the diagnostics
+* App. D.1 (training statistics table and dynamics figure) and App. D.5: the diagnostics
   "fraction of tokens acted on" (whole responses for Seq-TIS/Seq-MIS), "largest |log k_t| in the
   batch", the truncated excess sum_t (k_t - f_t), and the per-token displacement
-  eps_t = logit p_t - logit q_t computed from the two log-probabilities (App. D.1).
+  eps_t = logit p_t - logit q_t computed from the two log-probabilities (App. A).
 
 Readings where the paper is silent (each is a parameter of the tests, not hidden here):
 
@@ -210,7 +210,7 @@ def seq_weights(op: int, logk: np.ndarray, valid: np.ndarray, offsets: np.ndarra
 
 
 # --------------------------------------------------------------------------------------------
-# Diagnostics (App. D.1, D.4, D.5)
+# Diagnostics (App. A, D.1, D.5)
 # --------------------------------------------------------------------------------------------
 
 def displacement(logp_p: float, logp_q: float, one_minus_p: float) -> float:

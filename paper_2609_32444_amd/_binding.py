@@ -159,8 +159,6 @@ def _mask_u8(mask: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
 
 
 def _logits_args(logits: torch.Tensor, V: Optional[int]):
-    if not logits.is_cuda:
-        raise ValueError("logits must be a device tensor")
     if logits.dim() != 2 or logits.stride(1) != 1:
         raise ValueError("logits must be [T, >=V] with unit column stride")
     if logits.dtype == torch.bfloat16:
@@ -171,7 +169,16 @@ def _logits_args(logits: torch.Tensor, V: Optional[int]):
         raise ValueError(f"logits dtype must be bfloat16 or float32, got {logits.dtype}")
     T = logits.shape[0]
     V = logits.shape[1] if V is None else int(V)
-    ld = logits.stride(0) if T > 1 else max(logits.stride(0), V)
+    if V < 1 or V > logits.shape[1]:
+        raise ValueError(f"V must be in [1, {logits.shape[1]}] (the logits' columns), got {V}")
+    ld = logits.stride(0)
+    if T <= 1:
+        # one row (or none): the row stride never moves an address, so any stride that keeps
+        # the 16-byte row alignment the library asks for will do
+        epv = 16 // logits.element_size()
+        ld = (V + epv - 1) // epv * epv
+    if not logits.is_cuda:
+        raise ValueError("logits must be a device tensor")
     return dtype, T, V, ld
 
 

@@ -416,8 +416,10 @@ template <class T>
 __device__ __forceinline__ T sload(const T* p) {
   return *(const __attribute__((address_space(4))) T*)p;
 }
-// Byte `i` of a uint8 array through a scalar load of the aligned 4-byte word that holds it
-// (scalar loads read whole dwords; the word never crosses a page, so it is always mapped).
+// Byte `i` of a uint8 array through a scalar load of the aligned 4-byte word that holds it.
+// Scalar loads read whole dwords, so for the first and last bytes of the array up to 3
+// neighbouring bytes outside it are read and ignored; the C ABI states that those bytes must
+// be mapped (the word never crosses a page).
 __device__ __forceinline__ uint32_t sload_byte(const uint8_t* p, int64_t i) {
   const uintptr_t addr = (uintptr_t)(p + i);
   const uint32_t word = sload((const uint32_t*)(addr & ~(uintptr_t)3));

@@ -110,7 +110,7 @@ _SHARED = {}
 
 
 def _worker(args):
-    rows, with_grad = args
+    rows, pos, with_grad = args
     d = _SHARED
     res = O.cis_loss(d["z"], d["ids"], d["linf"], d["adv"], d["mask"], d["lam"], d["kappa"],
                      d["scale"], with_grad=with_grad, rows=rows)
@@ -118,8 +118,10 @@ def _worker(args):
     if with_grad and d.get("gdev") is not None:
         fin = (res.flags & O.FLAG_NONFINITE) == 0
         gdev = d["gdev"]
-        g = O.bf16_bits_to_float64(gdev[rows]) if gdev.dtype == np.uint16 else \
-            gdev[rows].astype(np.float64)
+        # gdev holds either every row of the batch or only the compared ones, in order
+        at = pos if d["gdev_compared_only"] else rows
+        g = O.bf16_bits_to_float64(gdev[at]) if gdev.dtype == np.uint16 else \
+            gdev[at].astype(np.float64)
         gst = grad_stats(g[fin], res.grad[fin], gdev.dtype == np.uint16)
         res.grad = None
     return rows, res, gst
@@ -133,27 +135,38 @@ def _nproc() -> int:
     return max(1, min(n, 16))
 
 
+# Largest number of gradient elements a worker holds per block (each float64 array of a block
+# is then at most 64 MB; the comparison keeps a handful of them alive).
+_BLOCK_ELEMENTS = 1 << 23
+
+
 def run_oracle(z, ids, linf, adv, mask, lam, kappa, scale, rows=None, with_grad=True,
-               gdev=None, procs=None) -> dict:
+               gdev=None, procs=None, gdev_compared_only=False) -> dict:
     """Oracle results for `rows` (all rows if None) as a dict of arrays indexed like rows.
 
-    With `gdev` (the device gradient on the host: uint16 bf16 bits or float32, [T, V]) the
-    workers compare gradients themselves and only the merged counts come back ("grad_stats");
-    otherwise the float64 gradient rows are returned under "grad".
+    With `gdev` (the device gradient on the host: uint16 bf16 bits or float32, [T, V], or
+    only the compared rows in the order of `rows` when gdev_compared_only) the workers compare
+    gradients themselves and only the merged counts come back ("grad_stats"); otherwise the
+    float64 gradient rows are returned under "grad".
     """
-    T = z.shape[0]
+    T, V = z.shape
     rows = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64)
     _SHARED.clear()
     _SHARED.update(z=z, ids=ids, linf=linf, adv=adv, mask=mask, lam=lam, kappa=kappa,
-                   scale=scale, gdev=gdev)
+                   scale=scale, gdev=gdev, gdev_compared_only=gdev_compared_only)
     procs = _nproc() if procs is None else procs
-    blocks = [b for b in np.array_split(rows, max(1, min(len(rows), procs * 4))) if len(b)]
+    nblk = procs * 4
+    if with_grad:
+        nblk = max(nblk, -(-len(rows) * V // _BLOCK_ELEMENTS))
+    pos = np.arange(len(rows))
+    blocks = [(r, p) for r, p in zip(np.array_split(rows, max(1, min(len(rows), nblk))),
+                                     np.array_split(pos, max(1, min(len(rows), nblk)))) if len(r)]
     if procs > 1 and len(blocks) > 1:
         ctx = mp.get_context("fork")
         with ctx.Pool(procs) as pool:
-            parts = pool.map(_worker, [(b, with_grad) for b in blocks])
+            parts = pool.map(_worker, [(r, p, with_grad) for r, p in blocks])
     else:
-        parts = [_worker((b, with_grad)) for b in blocks]
+        parts = [_worker((r, p, with_grad)) for r, p in blocks]
     _SHARED.clear()
     out = {k: [] for k in ("logp_train", "w", "trunc", "term", "flags", "grad")}
     gsts = []
@@ -181,14 +194,26 @@ def device_grad_host(g: torch.Tensor, V: int) -> np.ndarray:
     return g.contiguous().cpu().numpy()
 
 
-def oracle_for_batch(b, rows=None, with_grad=True, grad=None) -> dict:
-    """Oracle on batch `b`; pass the device gradient as `grad` to compare it in the workers."""
-    z = host_logits(b.logits)
+def oracle_for_batch(b, rows=None, with_grad=True, grad=None, z=None) -> dict:
+    """Oracle on batch `b`; pass the device gradient as `grad` to compare it in the workers.
+
+    `z` is the batch's logits already on the host (host_logits), to reuse one copy for several
+    comparisons. When `rows` is given, only those rows of `grad` are copied to the host.
+    """
+    z = host_logits(b.logits) if z is None else z
     mask = None if b.mask is None else b.mask.cpu().numpy()
-    gdev = None if grad is None else device_grad_host(grad, b.V)
+    compared_only = grad is not None and rows is not None
+    if grad is None:
+        gdev = None
+    elif compared_only:
+        idx = torch.as_tensor(np.asarray(rows, dtype=np.int64), device=grad.device)
+        gdev = device_grad_host(grad.index_select(0, idx), b.V)
+    else:
+        gdev = device_grad_host(grad, b.V)
     return run_oracle(z, b.ids.cpu().numpy(), b.logp_infer.cpu().double().numpy(),
                       b.adv.cpu().double().numpy(), mask, f32(b.lam), f32(b.kappa), f32(b.scale),
-                      rows=rows, with_grad=with_grad or grad is not None, gdev=gdev)
+                      rows=rows, with_grad=with_grad or grad is not None, gdev=gdev,
+                      gdev_compared_only=compared_only)
 
 
 # ------------------------------------------------------------------------------------------

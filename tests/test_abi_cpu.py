@@ -6,6 +6,7 @@ import os
 import re
 
 import pytest
+import torch
 
 import paper_2609_32444_amd as cis
 from paper_2609_32444_amd import _binding
@@ -285,3 +286,18 @@ def test_lmhead_binding_rejects_accumulating_into_nothing():
         cis.lmhead_loss_bwd(h, torch.zeros(10, 64, dtype=torch.bfloat16),
                             torch.zeros(4, dtype=torch.int64), torch.zeros(4), torch.zeros(4),
                             params=cis.params(), accumulate=True)
+
+
+def test_binding_rejects_a_vocabulary_wider_than_the_logits():
+    """V may not exceed the logits' columns (the kernel would read past each row, and for a
+    single row past the tensor); it is checked before anything touches a device."""
+    z = torch.zeros(1, 8, dtype=torch.bfloat16)
+    for V in (9, 1 << 20, 0, -1):
+        with pytest.raises(ValueError, match="V must be in"):
+            _binding._logits_args(z, V)
+    z4 = torch.zeros(4, 16, dtype=torch.float32)[:, :12]
+    with pytest.raises(ValueError, match="V must be in"):
+        _binding._logits_args(z4, 13)
+    # in range, the host tensor is refused only as not being a device tensor
+    with pytest.raises(ValueError, match="device tensor"):
+        _binding._logits_args(z4, 12)

@@ -65,3 +65,37 @@ def test_profile_commands_run_committed_files():
                 ap.parse_args(words[2:])
                 found += 1
     assert found >= 10
+
+
+def test_rejects_option_combinations_before_device_work():
+    # sequence operators run on the decoupled path only; the LM head runs one shape
+    r = _run(["--op", "seq_tis"])
+    assert r.returncode == 2 and "need --decoupled" in r.stderr and r.stdout == ""
+    r = _run(["--lmhead", "--config", "1"])
+    assert r.returncode == 2 and "MoE-rollout" in r.stderr and r.stdout == ""
+    r = _run(["--config", "7"])
+    assert r.returncode == 2 and r.stdout == ""
+
+
+def test_cpu_baseline_on_a_tiny_host_batch():
+    """The oracle timing leg on a small batch held in host memory: it runs, reports a rate,
+    the worker count it used and the host's core count."""
+    from workloads import make_batch
+    b = make_batch(1, device="cpu", rows=64)
+    rec = bench.cpu_baseline(b, b.V, target_s=0.2)
+    assert rec["kind"] == "oracle" and rec["value"] > 0 and rec["equivalent_gbs"] > 0
+    assert 1 <= rec["cores"] <= min(rec["host_cores"], bench.MAX_WORKERS)
+    assert f"{rec['cores']} worker processes" in rec["sample"]
+
+
+def test_cpu_baseline_lmhead_on_a_tiny_host_batch():
+    import math
+
+    from oracle import ops as X
+    from workloads import make_lmhead_batch
+    b = make_lmhead_batch(96, 200, 24, device="cpu", seed=2, c=1.0)
+    prm = X.OpParams(op=X.OP_CIS, lam=b.lam, kappa=b.kappa, lo=0.0, hi=math.inf,
+                     clip_low=0.2, clip_high=0.28, scale=b.scale)
+    rec = bench.cpu_baseline_lmhead(b, prm, target_s=0.3)
+    assert rec["kind"] == "oracle" and rec["value"] > 0 and rec["equivalent_tflops"] > 0
+    assert 1 <= rec["cores"] <= rec["host_cores"]

@@ -140,6 +140,99 @@ def test_lmhead_parity_small(name, T, V, H, chunk, gen):
     run_case(name, b, chunk=chunk)
 
 
+# ------------------------------------------------------------------------------------------
+# General bf16 inputs: the logits' own float32 rounding, bounded from the inputs
+# ------------------------------------------------------------------------------------------
+U_ADD = 2.0 ** -23   # float32 unit roundoff, doubled to also cover a truncating adder
+
+
+def _gamma(n):
+    return n * U_ADD / (1.0 - n * U_ADD)
+
+
+GENERAL = [
+    # name, T, V, H, chunk
+    ("vocab_151936", 128, 151936, 2048, 64),
+    ("ragged_9001", 300, 9001, 2048, 128),
+]
+
+
+@pytest.mark.parametrize("name,T,V,H,chunk", GENERAL, ids=[g[0] for g in GENERAL])
+def test_lmhead_general_bf16_inputs(name, T, V, H, chunk):
+    """Hidden states N(0, 1) and head weights N(0, 4/(H-1)) rounded once to bf16, so the
+    float32 logits h W^T carry their own dot-product rounding. The bounds follow from it:
+
+    * each float32 logit is within E_v = gamma_H sum_k |h_k| |W_vk| of the exact one
+      (gamma_n = n u / (1 - n u), u = 2^-23: any summation order, round-to-nearest or
+      truncating additions); E = max_v E_v per row;
+    * log-sum-exp moves by at most E, so l_train = z_y - lse by at most 2E; every
+      probability, and 1 - p, by a factor within exp(+-2E): delta_p = expm1(2E);
+    * w = min{k, 1 + lambda max(1 - p, kappa)} is then within delta_w = delta_p (+1e-5, the
+      kernel's own float32 tolerance) relative; the truncation decision moves by at most 4E,
+      so flags may differ where the oracle's margin is below 4E + 1e-5;
+    * term = scale w A l_train and the loss follow by the product rule; G = coef (onehot - p)
+      is within rho = delta_w (1 + delta_p) + delta_p relative per row, which widens the
+      products' bounds of the module docstring by that factor.
+    """
+    b = make_lmhead_batch(T, V, H, device=DEV, seed=23, min_len=16, max_len=96, exact=False)
+    prm_dev, prm_ref = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
+    out = cis.lmhead_loss_bwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
+                              params=prm_dev, chunk=chunk)
+    torch.cuda.synchronize()
+    h, W = host(b)
+    ids = b.ids.cpu().numpy()
+    linf = b.logp_infer.cpu().double().numpy()
+    adv = b.adv.cpu().double().numpy()
+    res = L.lmhead_cis_loss(h, W, ids, linf, adv, b.mask.cpu().numpy(), prm_ref,
+                            with_grad=True, keep_grad=True)
+    valid = (res.flags & 1) > 0
+    assert valid.all()
+    E = _gamma(H) * (np.abs(h) @ np.abs(W).T).max(axis=1)
+    dp = np.expm1(2.0 * E)
+    dw = dp + 1e-5
+    rho = dw * (1.0 + dp) + dp
+
+    lt = out["logp_train"].cpu().double().numpy()
+    w = out["w"].cpu().double().numpy()
+    term = out["terms"].cpu().double().numpy()
+    acted = out["acted"].cpu().numpy().astype(bool)
+    lref, wref, tref = res.logp_train, res.w, res.term
+    tol_l = 2.0 * E + 1e-5 * np.abs(lref) + 2e-6
+    err_l = np.abs(lt - lref)
+    assert np.all(err_l <= tol_l), f"l_train: worst err/bound {np.max(err_l / tol_l):.3g}"
+    err_w = np.abs(w - wref)
+    tol_w = dw * np.abs(wref) + P.F32_TINY
+    assert np.all(err_w <= tol_w), f"w: worst err/bound {np.max(err_w / tol_w):.3g}"
+    sA = np.abs(P.f32(b.scale) * adv)
+    tol_t = sA * (dw * wref * np.abs(lref) + wref * (1.0 + dw) * tol_l) \
+        + 1e-5 * np.abs(tref) + P.F32_TINY
+    err_t = np.abs(term - tref)
+    assert np.all(err_t <= tol_t), f"term: worst err/bound {np.max(err_t / tol_t):.3g}"
+    one_m_p = -np.expm1(lref)
+    margin = np.abs((lref - linf) - np.log1p(prm_ref.lam * np.maximum(one_m_p, prm_ref.kappa)))
+    differ = acted != res.acted
+    assert np.all(margin[differ] < 4.0 * E[differ] + 1e-5), "acted flags differ outside 4E"
+    Lg, L64 = float(out["loss"].item()), res.loss
+    assert abs(Lg - L64) <= float(np.sum(tol_t)) + 1e-5 * float(np.sum(np.abs(tref))) + 1e-6
+
+    G = np.abs(res.grad)
+    kdw, ngr = dw_group(chunk, b.T)
+    dh = out["dhidden"].cpu().double().numpy()
+    dW = out["dweight"].cpu().double().numpy()
+    acc_h = (8.0 * math.sqrt(b.V) + 1) * U32
+    acc_w = (8.0 * math.sqrt(kdw) + ngr) * U32
+    ch = (1.0 + rho) * (U16 + 4e-5 + acc_h) + rho
+    cw = (1.0 + rho) * (U16 + 4e-5 + acc_w) + rho
+    rep = {"case": name, "T": T, "V": V, "H": H, "chunk": chunk,
+           "max_E": float(E.max()), "max_err_logp_over_E": float(np.max(err_l / E)),
+           "max_err_logp": float(err_l.max()), "acted_differ": int(differ.sum())}
+    rep["dhidden"] = check_grad("dhidden", dh, res.dhidden,
+                                ch[:, None] * (G @ np.abs(W)) + 1e-30)
+    rep["dweight"] = check_grad("dweight", dW, res.dW, (cw[:, None] * G).T @ np.abs(h) + 1e-30)
+    _dump(f"general_{name}", rep)
+    print(rep, flush=True)
+
+
 def test_lmhead_products_with_more_tiles_than_cus():
     """Logits and dL/dW products of 314 tiles of 256 x 256 each (more than one per CU): their
     workgroups take tiles from the per-XCD work queues. The full comparison with the oracle, a

@@ -1,9 +1,12 @@
 """Parity of the HIP path (through the C ABI) with the CPU oracle on the five workloads.
 
-Tiny and small configurations are compared on every row. The full-size configurations are run
-exactly as the benchmark runs them (same entry point, same launch configuration): every row's
-per-token outputs and the loss are compared with the oracle, and the gradient is compared on a
-seeded sample of rows that always includes the first and last rows and the heavy-tail rows.
+Every workload runs exactly as the benchmark runs it (same entry point, same launch
+configuration). The tiny, small and MoE-rollout workloads are compared on every row: per-token
+outputs, the loss and every gradient element, the MoE rollout at each of its three thresholds.
+Each of the eight 65536-row chunks of the long-response workload, and the wide-vocabulary
+workload, is compared on every row's per-token outputs and the loss, and on the gradients of
+4096 (long response) or 1024 (wide vocabulary) seeded rows that always include the first and
+last rows and the heavy-tail rows.
 """
 
 import json
@@ -39,19 +42,25 @@ def _run(b, bwd=True):
     return out
 
 
-def _check_full(name, b, out, grad_rows=None, scalar_rows=None):
-    """Scalars + loss on all rows (or scalar_rows), gradients on grad_rows (all if None)."""
+def _check_full(name, b, out, grad_rows=None, scalar_rows=None, z=None, ref=None):
+    """Scalars + loss on all rows (or scalar_rows), gradients on grad_rows (all if None).
+
+    `z` (the logits on the host) and `ref` (the oracle's scalars over the same rows) can be
+    passed in to share them between two comparisons of one batch."""
     report = {"config": {k: v for k, v in b.meta.items() if k != "outlier_rows"}}
     all_grads = grad_rows is None and "dlogits" in out
-    ref = P.oracle_for_batch(b, rows=scalar_rows, with_grad=False,
-                             grad=out["dlogits"] if all_grads else None)
+    z = P.host_logits(b.logits) if z is None else z
+    if ref is None or all_grads:
+        ref = P.oracle_for_batch(b, rows=scalar_rows, with_grad=False,
+                                 grad=out["dlogits"] if all_grads else None, z=z)
     P.compare_scalars(out, ref, b, report)
     if scalar_rows is None:
         P.compare_loss(out, ref, report)
     if all_grads:
         P.check_grad_stats(ref["grad_stats"], report)
+        report["grad_rows"] = int(b.T)
     elif "dlogits" in out:
-        refg = P.oracle_for_batch(b, rows=grad_rows, with_grad=False, grad=out["dlogits"])
+        refg = P.oracle_for_batch(b, rows=grad_rows, with_grad=False, grad=out["dlogits"], z=z)
         P.check_grad_stats(refg["grad_stats"], report)
         report["grad_rows"] = int(len(grad_rows))
     stats = cis.read_stats(out["workspace"])
@@ -77,30 +86,38 @@ def test_config1_small_bf16_all_rows():
 
 @pytest.mark.parametrize("c", [0.5, 1.0, 2.0])
 def test_config2_moe_full_size(c):
+    """Every row of the MoE-rollout batch: per-token outputs, loss and all 2.5e9 gradient
+    elements against the oracle."""
     b = make_batch(2, device="cuda", c=c)
     out = _run(b)
-    rows = _sample_rows(b.T, 192, seed=int(c * 10), extra=b.meta["outlier_rows"])
-    _check_full(f"cfg2_c{c}", b, out, grad_rows=rows)
+    rep = _check_full(f"cfg2_c{c}", b, out)
+    assert rep["grad"]["n_rows"] == b.T
 
 
-@pytest.mark.parametrize("chunk", [0, 7])
+@pytest.mark.parametrize("chunk", range(8))
 def test_config3_long_chunk(chunk):
+    """One 65536-row chunk of the long-response workload: every row's per-token outputs and
+    the chunk's loss, and the gradients of 4096 seeded rows plus the first, last and
+    heavy-tail rows."""
     b = make_batch(3, device="cuda", chunk=chunk)
     out = _run(b)
-    srows = _sample_rows(b.T, 4096, seed=100 + chunk, extra=b.meta["outlier_rows"])
-    grows = _sample_rows(b.T, 96, seed=200 + chunk, extra=b.meta["outlier_rows"][:8])
-    rep = _check_full(f"cfg3_chunk{chunk}", b, out, grad_rows=grows, scalar_rows=srows)
-    assert rep["trunc"] > 0
+    grows = _sample_rows(b.T, 4096, seed=200 + chunk, extra=b.meta["outlier_rows"])
+    rep = _check_full(f"cfg3_chunk{chunk}", b, out, grad_rows=grows)
+    assert rep["trunc"] > 0 and rep["grad_rows"] >= 4096
 
 
 def test_config4_wide_vocab_fwd_and_bwd():
+    """Wide vocabulary, forward only and fused: every row's per-token outputs and the loss,
+    and the fused pass's gradients on 1024 seeded rows plus the first and last rows."""
     b = make_batch(4, device="cuda")
-    srows = _sample_rows(b.T, 4096, seed=400)
-    grows = _sample_rows(b.T, 64, seed=401)
+    grows = _sample_rows(b.T, 1024, seed=401)
+    z = P.host_logits(b.logits)
+    ref = P.oracle_for_batch(b, with_grad=False, z=z)
     out_f = _run(b, bwd=False)
-    _check_full("cfg4_fwd", b, out_f, scalar_rows=srows)
+    _check_full("cfg4_fwd", b, out_f, z=z, ref=ref)
     out_b = _run(b, bwd=True)
-    _check_full("cfg4_bwd", b, out_b, grad_rows=grows, scalar_rows=srows)
+    rep = _check_full("cfg4_bwd", b, out_b, grad_rows=grows, z=z, ref=ref)
+    assert rep["grad_rows"] >= 1024
     # Both passes also agree with each other to float32 rounding. (Not bit for bit: on rows
     # this long the fused pass keeps part of the row in LDS, the forward pass streams it, so
     # the exp-sum is accumulated in a different order.)

@@ -224,7 +224,7 @@ def check_seq_weights():
 
 
 # ------------------------------------------------------------------------------------------
-# Diagnostics (App. D.1, D.4, D.5)
+# Diagnostics (App. A, D.1, D.5)
 # ------------------------------------------------------------------------------------------
 
 def check_displacement():

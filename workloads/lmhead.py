@@ -14,6 +14,11 @@ row's dot product stays below 2^24 such units: float32 accumulation in any order
 exact logits, so a kernel's float32 logits equal the float64 ones and the loss comparisons see
 only the loss's own rounding.
 
+General inputs (exact=False). Hidden entries N(0, 1) and head entries N(0, 4 / (H - 1)) rounded
+once to bf16 (column 0 as above: 1 and the bias rounded to bf16), with no further quantisation:
+float32 dot products of these are not exact, which is what a test of the products' own rounding
+needs.
+
 The sampled ids come from softmax(z + delta) (Gumbel-max), delta ~ N(0, 0.03^2) per logit with
 0.1% of the rows at N(0, 2^2), and the recorded inference log-probability is
 log_softmax(z + delta)[y] in float32 (the model of ``workloads.synth``). Advantages are GRPO
@@ -78,11 +83,12 @@ def make_lmhead_batch(T: int, V: int, H: int, device="cuda", seed: int = 0, c: f
                       group: int = 16, zipf: bool = True, delta_sd: float = 0.03,
                       outlier_frac: float = 0.001, outlier_sd: float = 2.0,
                       old_sd: Optional[float] = None, ld_h: Optional[int] = None,
-                      ld_w: Optional[int] = None, rows_per_step: int = 1024) -> LmHeadBatch:
+                      ld_w: Optional[int] = None, rows_per_step: int = 1024,
+                      exact: bool = True) -> LmHeadBatch:
     """One batch; `old_sd` also draws logp_old = log_softmax(z + old_sd N(0, 1))[y] (the
     rollout snapshot of the decoupled objective). ld_h / ld_w >= H give padded row strides
-    (padding holds NaN)."""
-    if H > MAX_EXACT_H:
+    (padding holds NaN). exact=False draws general bf16 inputs (module docstring)."""
+    if exact and H > MAX_EXACT_H:
         raise ValueError(f"exact logits need H <= {MAX_EXACT_H}")
     g = _gen(device, seed)
     p = _scale_exponent(H)
@@ -114,18 +120,26 @@ def make_lmhead_batch(T: int, V: int, H: int, device="cuda", seed: int = 0, c: f
     # ---- head weight and hidden states ------------------------------------------------------
     sw = 2.0 / math.sqrt(max(H - 1, 1))
     weight = _padded(V, H, ld_w or H, device)
-    m = torch.round(sw * 2.0 ** p * torch.randn(V, H, generator=g, device=device))
-    wt = m.clamp_(-127, 127) * 2.0 ** -p
+    if exact:
+        m = torch.round(sw * 2.0 ** p * torch.randn(V, H, generator=g, device=device))
+        wt = m.clamp_(-127, 127) * 2.0 ** -p
+    else:
+        m = None
+        wt = sw * torch.randn(V, H, generator=g, device=device)
     if zipf:
         bias = -1.1 * torch.log(torch.arange(1, V + 1, device=device, dtype=torch.float64))
-        bias = (torch.round(bias / unit) * unit).to(torch.bfloat16).float()
+        if exact:
+            bias = torch.round(bias / unit) * unit
+        bias = bias.to(torch.bfloat16).float()
     else:
         bias = torch.zeros(V, device=device)
     wt[:, 0] = bias
     weight.copy_(wt.to(torch.bfloat16))
     del wt, m
     hidden = _padded(T, H, ld_h or H, device)
-    hv = torch.round(4.0 * torch.randn(T, H, generator=g, device=device)).clamp_(-15, 15) / 4.0
+    hv = torch.randn(T, H, generator=g, device=device)
+    if exact:
+        hv = torch.round(4.0 * hv).clamp_(-15, 15) / 4.0
     hv[:, 0] = 1.0
     hidden.copy_(hv.to(torch.bfloat16))
     del hv
@@ -150,7 +164,8 @@ def make_lmhead_batch(T: int, V: int, H: int, device="cuda", seed: int = 0, c: f
         del z, delta
     del wf
     n_valid = int(mask.sum().item())
-    meta = {"seed": seed, "c": c, "p": p, "n_resp": n_resp, "outlier_rows": int(n_odd)}
+    meta = {"seed": seed, "c": c, "p": p, "n_resp": n_resp, "outlier_rows": int(n_odd),
+            "exact": bool(exact)}
     return LmHeadBatch(hidden, weight, ids, lq, adv, mask,
                        torch.tensor(offs, dtype=torch.int64, device=device), lambda_of(c),
                        KAPPA, -1.0 / max(n_valid, 1), lold, meta)
