@@ -8,13 +8,18 @@ Tolerances (the readings used by every parity test):
 * l_train: |gpu - ref| <= 1e-5 |ref| + 2e-6 (float32 log-sum-exp resolution).
 * w: relative 1e-5.
 * term: |gpu - ref| <= 1e-5 |ref| + 2e-6 |scale w A|; loss: <= 1e-5 sum_t |term_t| + 1e-6.
-* bf16 gradient: every element is one of the two bfloat16 values bracketing the float64
-  gradient (a faithful rounding; agreement with the float64 value rounded to nearest is
-  reported as the bit-equal fraction), except elements with |g| < 2^-126 that may be flushed
-  to zero; per row, ||g - g_ref|| / ||g_ref|| <= 2e-3 with g_ref the float64 gradient rounded
-  to nearest bfloat16 (bfloat16's own unit roundoff, 2^-8, exceeds 2e-3, so the bound is
-  taken against the best bfloat16 answer), leaving out entries below 2^-126.
-* float32 gradient: |g - g64| <= 2e-5 |g64| + 2^-126.
+* float32 gradient: |g - g64| <= 2e-5 |g64| + 2^-126 (G_REL: the float32 evaluation of
+  coef * exp(z - lse), whose argument and exponential carry a few 1e-6 relative).
+* bf16 gradient: every element is the round-to-nearest-even bfloat16 of some value within
+  that float32 tolerance of the float64 gradient: it equals the correctly rounded g64 except
+  where g64 lies within 2e-5 |g64| of a rounding midpoint, where either neighbour is correct;
+  values below 2^-126 may be flushed to zero. (bfloat16's unit roundoff 2^-8 exceeds the
+  2e-3 relative bound, so the bound is taken against the best bfloat16 answer.) Reported
+  beside it: the bit-equal fraction, the fraction within 2e-3 relative of g64, and per row
+  ||g - g_ref|| / ||g_ref|| against g_ref = RNE(g64) over the elements outside the midpoint
+  bands, which must be <= 2e-3 (it is 0 when the elementwise criterion holds; a row whose
+  norm sits in one element near a midpoint can exceed 2e-3 over all elements while every
+  element is a correct rounding, and that value is reported as well).
 """
 
 from __future__ import annotations
@@ -29,6 +34,7 @@ import torch
 from oracle import cis as O
 
 F32_TINY = 2.0 ** -126
+G_REL = 2e-5
 
 
 def write_report(filename: str, report: dict) -> None:
@@ -68,23 +74,33 @@ def grad_stats(g: np.ndarray, g64: np.ndarray, bf16: bool) -> dict:
     st["max_row_rel_l2_vs_f64"] = float(rel64.max()) if rel64.size else 0.0
     st["zero_row_violations"] = int(np.sum(np.any(g[nrm == 0] != 0, axis=1)))
     if bf16:
-        lo, hi = O.bf16_neighbors(g64)
+        rnd = lambda x: O.bf16_bits_to_float64(O.round_float64_to_bf16_bits(x))  # noqa: E731
+        slack = G_REL * np.abs(g64)
+        lo, hi = rnd(g64 - slack), rnd(g64 + slack)
         ok = (g >= lo) & (g <= hi)
-        ok |= (np.abs(g64) < F32_TINY) & (np.abs(g) <= F32_TINY)
-        st["not_faithful"] = int((~ok).sum())
-        rn = O.bf16_bits_to_float64(O.round_float64_to_bf16_bits(g64))
+        flush = (np.abs(g64) < F32_TINY * (1.0 + G_REL)) & (np.abs(g) <= F32_TINY)
+        ok |= flush
+        st["out_of_tolerance"] = int((~ok).sum())
+        rn = rnd(g64)
         st["bit_equal"] = int(np.sum(g == rn))
+        st["midpoint_band"] = int(np.sum((lo != hi) & ~flush))
         st["within_2e-3_rel"] = int(np.sum(np.abs(g - g64) <= 2e-3 * np.abs(g64)))
         # per row, against the correctly rounded bfloat16 reference; entries below the float32
-        # normal range (which may be flushed) are left out of both sides
+        # normal range (which may be flushed) are left out of both sides, and the criterion row
+        # value also leaves out the midpoint bands
         keep = np.abs(g64) >= F32_TINY
         rnk = np.where(keep, rn, 0.0)
         nrn = np.linalg.norm(rnk, axis=1)
-        rel = np.linalg.norm(np.where(keep, g, 0.0) - rnk, axis=1) / np.where(nrn > 0, nrn, 1.0)
+        den = np.where(nrn > 0, nrn, 1.0)
+        rel_all = np.linalg.norm(np.where(keep, g, 0.0) - rnk, axis=1) / den
+        st["max_row_rel_l2_all_elements"] = float(rel_all.max()) if rel_all.size else 0.0
+        st["rows_over_2e-3_all_elements"] = int(np.sum(rel_all > 2e-3))
+        out = keep & (lo == hi)
+        rel = np.linalg.norm(np.where(out, g, 0.0) - np.where(out, rn, 0.0), axis=1) / den
     else:
         rel = rel64
         err = np.abs(g - g64)
-        st["not_faithful"] = int(np.sum(err > 2e-5 * np.abs(g64) + F32_TINY))
+        st["out_of_tolerance"] = int(np.sum(err > G_REL * np.abs(g64) + F32_TINY))
         st["max_rel"] = float(np.max(err / np.maximum(np.abs(g64), F32_TINY))) if g.size else 0.0
         st["bit_equal"] = int(np.sum(g == g64.astype(np.float32)))
         st["within_2e-3_rel"] = int(np.sum(err <= 2e-3 * np.abs(g64)))
@@ -278,7 +294,7 @@ def compare_loss(out: dict, ref_all: dict, report: dict) -> None:
 
 
 def check_grad_stats(st: dict, report: dict) -> None:
-    assert st["not_faithful"] == 0, f"{st['not_faithful']} gradient elements out of tolerance"
+    assert st["out_of_tolerance"] == 0, f"{st['out_of_tolerance']} gradient elements out of tolerance"
     assert st["zero_row_violations"] == 0
     assert st["max_row_rel_l2"] <= 2e-3, f"row rel L2 {st['max_row_rel_l2']:.3g}"
     report["grad"] = dict(st, bit_equal_frac=st["bit_equal"] / max(st["n_el"], 1),
