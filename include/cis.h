@@ -77,7 +77,8 @@ enum {
   CIS_ERR_WORKSPACE = -7, /* workspace smaller than cis_workspace_bytes(T)                    */
   CIS_ERR_ALIAS = -8,     /* dlogits == logits with ld_g != ld, a partial overlap, or an
                              LM-head gradient overlapping an operand or the workspace        */
-  CIS_ERR_DEVICE = -9     /* the current device is not a gfx950 GPU, or no device            */
+  CIS_ERR_DEVICE = -9,    /* the current device is not a gfx950 GPU, or no device            */
+  CIS_ERR_SCRATCH = -10   /* T > CIS_NOALLOC_MAX_T (cis_loss_bwd_noalloc)                     */
 };
 
 /* Per-call statistics, written at byte offset 0 of the workspace by every entry point that
@@ -173,6 +174,35 @@ int cis_loss_bwd(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld
                  float* logp_train_out, float* w_out, uint8_t* trunc_out,
                  float* loss_terms_out, float* loss_out,
                  void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Rows per call of cis_loss_bwd_noalloc (the capacity of its fixed scratch). */
+#define CIS_NOALLOC_MAX_T 262144
+
+/*
+ * cis_loss_bwd_noalloc — cis_loss_bwd for callers that cannot allocate device memory or pass
+ * a workspace (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc). Same operation, kernels and results as cis_loss_bwd; the per-row scratch and
+ * the cis_stats_t live in a fixed device array of the library (4.5 MiB per device, held until
+ * the process ends) instead of a caller's workspace. The call allocates nothing.
+ *
+ *   T          0 <= T <= CIS_NOALLOC_MAX_T (262144); larger T returns CIS_ERR_SCRATCH before
+ *              anything else is checked or launched
+ *   stats_out  optional device pointer that receives the call's cis_stats_t (NULL = not
+ *              written); the copy kept in the library's array is overwritten by the next call
+ *   other arguments as for cis_loss_bwd.
+ * Every call on one device uses that device's one array: two calls that may overlap on a
+ * device (different streams, or graphs replayed concurrently) race on it and must be
+ * serialised by the caller. Nothing in the array needs clearing between calls.
+ * Errors: those of cis_loss_bwd except CIS_ERR_WORKSPACE, plus CIS_ERR_SCRATCH; the device
+ * check (CIS_ERR_DEVICE) comes before the other argument checks.
+ */
+int cis_loss_bwd_noalloc(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
+                         const int64_t* ids, const float* logp_infer, const float* adv,
+                         const uint8_t* mask, float lambda, float kappa, float scale,
+                         void* dlogits, int64_t ld_g,
+                         float* logp_train_out, float* w_out, uint8_t* trunc_out,
+                         float* loss_terms_out, float* loss_out, cis_stats_t* stats_out,
+                         hipStream_t stream);
 
 /* =========================================================================================
  * The operator family and the decoupled PPO-clip path.

@@ -12,6 +12,7 @@ from ._binding import (  # noqa: F401
     CIS_F32,
     LMHEAD_CHUNK,
     LossCall,
+    NOALLOC_MAX_T,
     OP_CIS,
     OP_EXACT,
     OP_ICEPOP,
@@ -32,6 +33,7 @@ from ._binding import (  # noqa: F401
     load_library,
     loss_bwd,
     loss_bwd_ex,
+    loss_bwd_noalloc,
     loss_fwd,
     loss_fwd_ex,
     params,
@@ -44,10 +46,10 @@ from ._binding import (  # noqa: F401
 )
 
 __all__ = [
-    "CisError", "CIS_BF16", "CIS_F32", "LMHEAD_CHUNK", "LossCall", "OP_CIS", "OP_EXACT", "OP_ICEPOP", "OP_KPOP",
+    "CisError", "CIS_BF16", "CIS_F32", "LMHEAD_CHUNK", "LossCall", "NOALLOC_MAX_T", "OP_CIS", "OP_EXACT", "OP_ICEPOP", "OP_KPOP",
     "OP_NONE", "OP_QFIXED", "OP_SEQ_MIS", "OP_SEQ_TIS", "OP_TIS", "OP_TWO_SIDED", "Params",
     "SEQ_OPS", "lambda_from_logodds", "library_path", "lmhead_loss_bwd", "lmhead_loss_fwd",
-    "lmhead_workspace_bytes", "load_library", "loss_bwd", "loss_bwd_ex",
+    "lmhead_workspace_bytes", "load_library", "loss_bwd", "loss_bwd_ex", "loss_bwd_noalloc",
     "loss_fwd", "loss_fwd_ex", "params", "read_stats", "status_string", "weights", "weights_ex",
     "workspace_bytes", "workspace_bytes_ex",
 ]

@@ -77,6 +77,9 @@ def load_library() -> ctypes.CDLL:
     lib.cis_loss_bwd.argtypes = [_vp, _int, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _f32, _f32, _f32,
                                  _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _size, _vp]
     lib.cis_loss_bwd.restype = _int
+    lib.cis_loss_bwd_noalloc.argtypes = [_vp, _int, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _f32,
+                                         _f32, _f32, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+    lib.cis_loss_bwd_noalloc.restype = _int
     lib.cis_workspace_bytes_ex.argtypes = [_i64, _i64]
     lib.cis_workspace_bytes_ex.restype = _size
     lib.cis_weights_ex.argtypes = [_vp, _vp, _vp, _i64, _vp, _i64, ctypes.POINTER(Params),
@@ -245,6 +248,47 @@ def _loss(bwd: bool, logits, ids, logp_infer, adv, mask, lam, kappa, scale, V, d
     if bwd:
         out["dlogits"] = dlogits
     return out
+
+
+NOALLOC_MAX_T = 262144  # CIS_NOALLOC_MAX_T in include/cis.h
+
+
+def loss_bwd_noalloc(logits, ids, logp_infer, adv, mask=None, *, lam, kappa=5e-3, scale=1.0,
+                     V=None, dlogits, outputs, stats_out=None):
+    """cis_loss_bwd_noalloc: the fused pass into caller-provided buffers, with the library's
+    fixed scratch instead of a workspace (nothing is allocated, here or in the library).
+
+    `dlogits` is a [T, >=V] tensor like logits; `outputs` a dict holding any of "logp_train",
+    "w", "terms" ([T] float32), "trunc" ([T] uint8) and "loss" ([1] float32); `stats_out`
+    an optional [64] uint8 device tensor that receives the cis_stats_t (see read_stats).
+    Returns nothing: the results are in the given tensors once the stream has run."""
+    dtype, T, V, ld = _logits_args(logits, V)
+    dev = logits.device
+    _check_vec("ids", ids, T, torch.int64, dev)
+    _check_vec("logp_infer", logp_infer, T, torch.float32, dev)
+    _check_vec("adv", adv, T, torch.float32, dev)
+    mask = _check_vec("mask", _mask_u8(mask), T, torch.uint8, dev, optional=True)
+    for k, t in outputs.items():
+        want = (1 if k == "loss" else T, torch.uint8 if k == "trunc" else torch.float32)
+        if k not in ("logp_train", "w", "terms", "trunc", "loss"):
+            raise ValueError(f"unknown output {k!r}")
+        _check_vec(k, t, want[0], want[1], dev)
+    if dlogits.dtype != logits.dtype or dlogits.dim() != 2 or dlogits.stride(1) != 1 \
+            or dlogits.shape[0] != T or dlogits.shape[1] < V or dlogits.device != dev:
+        raise ValueError("dlogits must be a [T, >=V] tensor like logits")
+    if stats_out is not None and (stats_out.device != dev or stats_out.dtype != torch.uint8
+                                  or stats_out.numel() < 64 or not stats_out.is_contiguous()):
+        raise ValueError("stats_out must be a contiguous uint8 device tensor of >= 64 bytes")
+    lib = load_library()
+    with torch.cuda.device(dev):
+        rc = lib.cis_loss_bwd_noalloc(
+            _ptr(logits), dtype, T, V, ld, _ptr(ids), _ptr(logp_infer), _ptr(adv), _ptr(mask),
+            float(lam), float(kappa), float(scale), _ptr(dlogits), dlogits.stride(0),
+            _ptr(outputs.get("logp_train")), _ptr(outputs.get("w")), _ptr(outputs.get("trunc")),
+            _ptr(outputs.get("terms")), _ptr(outputs.get("loss")), _ptr(stats_out),
+            _stream(dev))
+    if rc != 0:
+        raise CisError("cis_loss_bwd_noalloc", rc)
 
 
 def loss_fwd(logits, ids, logp_infer, adv, mask=None, *, lam, kappa=5e-3, scale=1.0, V=None,

@@ -161,6 +161,7 @@ struct LossCall {
   float *logp_train_out, *w_out;
   uint8_t* acted_out;
   float *terms_out, *eps_out, *loss_out;
+  cis_stats_t* stats_out;   // nullable: a copy of the workspace's statistics
   void* workspace;
   size_t workspace_bytes;
 };
@@ -261,9 +262,10 @@ int launch_rows(const LossCall& c, const Ws& ws, const void* logits, void* dlogi
   return launch(var.fn, grid, var.block, &ra, stream);
 }
 
-int launch_finalize(const Ws& ws, int64_t T, float* loss_out, hipStream_t stream) {
+int launch_finalize(const Ws& ws, int64_t T, float* loss_out, hipStream_t stream,
+                    cis_stats_t* stats_out = nullptr) {
   cis::FinalizeArgs fa{ws.f(ws.L.terms), ws.b(ws.L.flags), ws.f(ws.L.logk), ws.f(ws.L.excess), T,
-                       ws.stats(), loss_out};
+                       ws.stats(), loss_out, stats_out};
   return launch(cis::finalize_kernel(), 1, cis::kFinalizeBlock, &fa, stream);
 }
 
@@ -309,7 +311,31 @@ int run_loss(const LossCall& c, hipStream_t stream) {
     if (int rc = launch_rows(c, ws, c.logits, c.dlogits, c.ld, c.ld_g, 0, T, dev, info, stream))
       return rc;
   }
-  return launch_finalize(ws, T, c.loss_out, stream);
+  return launch_finalize(ws, T, c.loss_out, stream, c.stats_out);
+}
+
+// ------------------------------------------------------------------------------------------
+// Fixed scratch for cis_loss_bwd_noalloc: the loss workspace of up to CIS_NOALLOC_MAX_T rows
+// in a file-scope device array (one copy per device, held until the process ends). In host
+// code `scratch` names a host-side stand-in, not device memory: host code uses only the
+// address that hipGetSymbolAddress returns for the current device.
+// ------------------------------------------------------------------------------------------
+constexpr size_t kScratchBytes = cis::ws_bytes(CIS_NOALLOC_MAX_T);
+static_assert(kScratchBytes % 256 == 0, "whole 256-byte blocks");
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of `scratch` on device `dev` (the current device), looked up once per device.
+int scratch_on(int dev, void** out) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return CIS_ERR_DEVICE;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return CIS_OK;
 }
 
 // Byte range [lo, hi) of a rows x cols matrix with a row stride of ld elements of es bytes
@@ -584,6 +610,9 @@ const char* cis_status_string(int status) {
     case CIS_ERR_WORKSPACE: return "workspace too small (see cis_workspace_bytes)";
     case CIS_ERR_ALIAS: return "dlogits overlaps logits other than exactly in place (ld_g == ld)";
     case CIS_ERR_DEVICE: return "current device is not a gfx950 GPU";
+    case CIS_ERR_SCRATCH:
+      return "T exceeds the fixed scratch of cis_loss_bwd_noalloc (CIS_NOALLOC_MAX_T = 262144 "
+             "rows); use cis_loss_bwd with a workspace";
     default: return "unknown status";
   }
 }
@@ -673,6 +702,27 @@ int cis_loss_bwd(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld
                             kappa, scale, dlogits, ld_g, logp_train_out, w_out, trunc_out,
                             loss_terms_out, loss_out, workspace, workspace_bytes),
                   stream);
+}
+
+int cis_loss_bwd_noalloc(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,
+                         const int64_t* ids, const float* logp_infer, const float* adv,
+                         const uint8_t* mask, float lambda, float kappa, float scale,
+                         void* dlogits, int64_t ld_g, float* logp_train_out, float* w_out,
+                         uint8_t* trunc_out, float* loss_terms_out, float* loss_out,
+                         cis_stats_t* stats_out, hipStream_t stream) {
+  if (T > CIS_NOALLOC_MAX_T) return CIS_ERR_SCRATCH;
+  if (T < 0) return CIS_ERR_SHAPE;
+  // the device check comes before the scratch lookup (the lookup needs a gfx950 device)
+  DeviceInfo info;
+  const int dev = current_device(&info);
+  if (dev < 0) return dev;
+  void* ws = nullptr;
+  if (int rc = scratch_on(dev, &ws)) return rc;
+  LossCall c = base_call(true, logits, dtype, T, V, ld, ids, logp_infer, adv, mask, lambda, kappa,
+                         scale, dlogits, ld_g, logp_train_out, w_out, trunc_out, loss_terms_out,
+                         loss_out, ws, kScratchBytes);
+  c.stats_out = stats_out;
+  return run_loss(c, stream);
 }
 
 int cis_loss_fwd_ex(const void* logits, int dtype, int64_t T, int64_t V, int64_t ld,

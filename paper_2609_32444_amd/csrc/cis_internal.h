@@ -19,13 +19,13 @@ namespace cis {
 //   pflags uint8[T]   pre-pass bits (kFlagTrunc = acted on)
 //   logK   double[n_seq]  per-response log K (sequence operators)
 constexpr size_t kStatsBytes = 256;
-inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+constexpr size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 struct WsLayout {
   size_t terms, logk, excess, wpre, flags, pflags, logK, total;
 };
-inline WsLayout ws_layout(int64_t T, int64_t n_seq) {
+constexpr WsLayout ws_layout(int64_t T, int64_t n_seq) {
   const size_t f = align_up(4 * (size_t)T, 256), b = align_up((size_t)T, 256);
-  WsLayout L;
+  WsLayout L{};
   L.terms = kStatsBytes;
   L.logk = L.terms + f;
   L.excess = L.logk + f;
@@ -36,7 +36,7 @@ inline WsLayout ws_layout(int64_t T, int64_t n_seq) {
   L.total = L.logK + align_up(8 * (size_t)n_seq, 256);
   return L;
 }
-inline size_t ws_bytes(int64_t T) { return ws_layout(T, 0).total; }
+constexpr size_t ws_bytes(int64_t T) { return ws_layout(T, 0).total; }
 
 // LM-head workspace: the loss workspace above, then (256-byte aligned)
 //   Q   int[kGemmQueues]   the products' work queues (256 bytes)
@@ -144,6 +144,7 @@ struct FinalizeArgs {
   int64_t T;
   cis_stats_t* stats;
   float* loss_out;          // nullable
+  cis_stats_t* stats_copy;  // nullable: a second copy of the statistics (caller's memory)
 };
 
 struct WeightsArgs {

@@ -86,6 +86,7 @@ __global__ __launch_bounds__(kFinalizeBlock) void cis_finalize_kernel(const Fina
     a.stats->max_abs_logk = (double)Mx;
     a.stats->trunc_excess = X;
     a.stats->reserved = 0;
+    if (a.stats_copy) *a.stats_copy = *a.stats;
     if (a.loss_out) *a.loss_out = (float)L;
   }
 }

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == {"cis_workspace_bytes", "cis_workspace_bytes_ex", "cis_status_string",
                           "cis_weights", "cis_weights_ex", "cis_loss_fwd", "cis_loss_bwd",
                           "cis_loss_fwd_ex", "cis_loss_bwd_ex", "cis_lmhead_workspace_bytes",
-                          "cis_lmhead_loss_fwd", "cis_lmhead_loss_bwd"}
+                          "cis_lmhead_loss_fwd", "cis_lmhead_loss_bwd", "cis_loss_bwd_noalloc"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -301,3 +301,16 @@ def test_binding_rejects_a_vocabulary_wider_than_the_logits():
     # in range, the host tensor is refused only as not being a device tensor
     with pytest.raises(ValueError, match="device tensor"):
         _binding._logits_args(z4, 12)
+
+
+def test_noalloc_rejects_more_rows_than_its_scratch_holds():
+    """cis_loss_bwd_noalloc refuses T > CIS_NOALLOC_MAX_T before anything else (no device is
+    needed to see it), and says why."""
+    lib = cis.load_library()
+    T = cis.NOALLOC_MAX_T + 1
+    rc = lib.cis_loss_bwd_noalloc(FAKE, 0, T, 8, 8, FAKE, FAKE, FAKE, NULL, 1.0, 0.0, 1.0,
+                                  FAKE, 8, NULL, NULL, NULL, NULL, NULL, NULL, NULL)
+    assert rc == -10
+    assert "262144" in cis.status_string(rc)
+    hdr = open(HEADER).read()
+    assert re.search(r"#define CIS_NOALLOC_MAX_T 262144\b", hdr)
