@@ -104,10 +104,17 @@ def lmhead_traffic():
 LMHEAD_SOURCES = ("paper_2609_32444_amd/csrc/cis_gemm.hip", "paper_2609_32444_amd/csrc/cis_gemm.h")
 
 
+PROBE_MAX_ROW_BYTES = 19 * 1024 * 16   # the row-pattern probes hold one row per workgroup
+
+
 def bandwidth_ceilings(rows: int, row_bytes: int, torch) -> dict:
     """Measured ceilings on this device (libcis_probe.so), in GB/s: the row kernel's access
     pattern as copy (equal read and write), read only and write only of rows x row_bytes, and
-    the fastest equal read/write stream found on this part (4 KiB short-lived workgroups)."""
+    the fastest equal read/write and read-only streams found on this part (4 KiB short-lived
+    workgroups). Rows longer than the row-pattern probes hold are probed as pieces of the
+    same total size."""
+    while row_bytes > PROBE_MAX_ROW_BYTES and row_bytes % 32 == 0:
+        rows, row_bytes = rows * 2, row_bytes // 2
     import ctypes
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_32444_amd", "libcis_probe.so"))
     lib.cis_probe_bandwidth.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
@@ -121,7 +128,9 @@ def bandwidth_ceilings(rows: int, row_bytes: int, torch) -> dict:
     grid = torch.cuda.get_device_properties(0).multi_processor_count
     out = {}
     for mode, name, moved in ((0, "copy", 2 * n), (1, "read", n), (2, "write", n),
-                              (3, "copy_small_blocks", 2 * n)):
+                              (3, "copy_small_blocks", 2 * n), (4, "read_small_blocks", n)):
+        if row_bytes > PROBE_MAX_ROW_BYTES and mode < 3:
+            continue
         def go():
             rc = lib.cis_probe_bandwidth(mode, src.data_ptr(), dst.data_ptr(), rows, row_bytes,
                                          grid, sink.data_ptr(), stream)
@@ -543,11 +552,14 @@ def main():
     if not args.no_copy_ceiling:
         ceil = bandwidth_ceilings(T, ((V * esize + 15) // 16) * 16, torch)
         line["roofline"]["measured_ceiling_gbs"] = ceil
-        best_copy = max(ceil["copy"], ceil["copy_small_blocks"])
-        line["roofline"]["frac_of_measured_copy"] = achieved_gbs / best_copy if bwd else \
-            achieved_gbs / ceil["read"]
-        line["roofline"]["frac_of_row_pattern_copy"] = achieved_gbs / ceil["copy"] if bwd else \
-            achieved_gbs / ceil["read"]
+        if bwd:
+            best = max(ceil.get("copy", 0.0), ceil["copy_small_blocks"])
+            line["roofline"]["frac_of_measured_copy"] = achieved_gbs / best
+            if "copy" in ceil:
+                line["roofline"]["frac_of_row_pattern_copy"] = achieved_gbs / ceil["copy"]
+        else:
+            best = max(ceil.get("read", 0.0), ceil["read_small_blocks"])
+            line["roofline"]["frac_of_measured_read"] = achieved_gbs / best
     if ext:
         line["config"]["op"] = op
         line["config"]["decoupled"] = bool(args.decoupled)

@@ -23,12 +23,13 @@ extern "C" {
  *           workgroups of 4 KiB each (two 16-byte non-temporal vectors per thread): the
  *           fastest equal read/write stream found on this part (grid is ignored, row_bytes
  *           only needs to be a multiple of 16)
- *   src, dst   device buffers of rows*row_bytes bytes (src unused in mode 2, dst in mode 1)
+ *   mode 4: read src only, in the workgroups of mode 3: the fastest read stream found
+ *   src, dst   device buffers of rows*row_bytes bytes (src unused in mode 2, dst in modes 1, 4)
  *   row_bytes  multiple of 16, at most 19*1024*16
  *   grid       workgroups (persistent over rows), >= 1
  *   sink       device uint32[1024] receiving nothing in practice (read mode keeps its loads
- *              alive through it); required in mode 1
- * Returns 0, or -1 (NULL pointer), -2 (row_bytes, or a mode-3 size beyond 2^31 workgroups),
+ *              alive through it); required in modes 1 and 4
+ * Returns 0, or -1 (NULL pointer), -2 (row_bytes, or a mode-3/4 size beyond 2^31 workgroups),
  * -4 (mode/rows/grid), -6 (launch failed).
  */
 int cis_probe_bandwidth(int mode, const void* src, void* dst, int64_t rows, int64_t row_bytes,

@@ -256,6 +256,28 @@ int launch_rows(const LossCall& c, const Ws& ws, const void* logits, void* dlogi
   ra.eps_out = at(c.eps_out, t0);
   ra.clip_low = c.prm.clip_low;
   ra.clip_high = c.prm.clip_high;
+  // forward pass over long rows: segment kernel + combine (when the workspace has the room)
+  const cis::SegVariant* sv =
+      (!c.bwd && ws.L.seg) ? cis::select_seg_variant(c.dtype, nvec) : nullptr;
+  if (sv) {
+    cis::SegArgs sa{};
+    sa.segvec = sv->block * sv->k;
+    sa.nseg = (int32_t)((nvec + sa.segvec - 1) / sa.segvec);
+    sa.part = reinterpret_cast<float2*>(ws.base + ws.L.part) + t0 * cis::kSegMax;
+    sa.zy = ws.f(ws.L.zy) + t0;
+    void* args[] = {&ra, &sa};
+    // one short-lived workgroup per (row, segment); the kernel loops only past 2^30 of them
+    const int64_t total = rows * sa.nseg;
+    const int64_t cap = int64_t(1) << 30;
+    if (hipLaunchKernel(sv->fn, dim3((unsigned)(total < cap ? total : cap)), dim3(sv->block),
+                        args, 0, stream) != hipSuccess)
+      return CIS_ERR_LAUNCH;
+    const int64_t per = cis::kCombineBlock / 64;
+    return hipLaunchKernel(cis::combine_kernel(c.ext), dim3((unsigned)((rows + per - 1) / per)),
+                           dim3(cis::kCombineBlock), args, 0, stream) == hipSuccess
+               ? CIS_OK
+               : CIS_ERR_LAUNCH;
+  }
   const int per_cu = blocks_per_cu(var.fn, var.block, dev);
   const int64_t resident = (int64_t)per_cu * info.num_cu;
   const int grid = (int)(rows < resident ? rows : resident);
@@ -284,7 +306,8 @@ int run_loss(const LossCall& c, hipStream_t stream) {
     return CIS_ERR_NULL;
   if (n_seq > 0 && T > 0 && !c.offsets) return CIS_ERR_NULL;
   if (!aligned(c.workspace, 256)) return CIS_ERR_ALIGN;
-  const cis::WsLayout L = cis::ws_layout(T, n_seq);
+  // the forward pass keeps room for the split kernels' partials (cis_workspace_bytes covers it)
+  const cis::WsLayout L = cis::ws_layout(T, n_seq, !bwd);
   if (c.workspace_bytes < L.total) return CIS_ERR_WORKSPACE;
   if (T > 0) {
     if (!aligned(c.logits, 16) || (c.ld * esize) % 16 != 0) return CIS_ERR_ALIGN;
@@ -585,10 +608,10 @@ int cis_lmhead_loss_bwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
                     stream);
 }
 
-size_t cis_workspace_bytes(int64_t T) { return T < 0 ? 0 : cis::ws_bytes(T); }
+size_t cis_workspace_bytes(int64_t T) { return T < 0 ? 0 : cis::ws_layout(T, 0, true).total; }
 
 size_t cis_workspace_bytes_ex(int64_t T, int64_t n_seq) {
-  return (T < 0 || n_seq < 0) ? 0 : cis::ws_layout(T, n_seq).total;
+  return (T < 0 || n_seq < 0) ? 0 : cis::ws_layout(T, n_seq, true).total;
 }
 
 const char* cis_status_string(int status) {

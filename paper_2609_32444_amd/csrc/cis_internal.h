@@ -18,12 +18,19 @@ namespace cis {
 //   flags  uint8[T]   per-row status bits (kFlag*)
 //   pflags uint8[T]   pre-pass bits (kFlagTrunc = acted on)
 //   logK   double[n_seq]  per-response log K (sequence operators)
+//   part   float2[T * kSegMax]  per-segment (max, exp-sum) of the split forward pass
+//   zy     float[T]           the sampled logit (split forward pass)
+// The last two exist only in the layout of the forward entry points (`seg`); the fused pass and
+// the LM-head path do not use them.
 constexpr size_t kStatsBytes = 256;
+// Segments per row at most in the split forward pass (the partials per row in the workspace).
+constexpr int kSegMax = 32;
 constexpr size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 struct WsLayout {
-  size_t terms, logk, excess, wpre, flags, pflags, logK, total;
+  size_t terms, logk, excess, wpre, flags, pflags, logK, part, zy, total;
+  bool seg;
 };
-constexpr WsLayout ws_layout(int64_t T, int64_t n_seq) {
+constexpr WsLayout ws_layout(int64_t T, int64_t n_seq, bool seg = false) {
   const size_t f = align_up(4 * (size_t)T, 256), b = align_up((size_t)T, 256);
   WsLayout L{};
   L.terms = kStatsBytes;
@@ -33,7 +40,10 @@ constexpr WsLayout ws_layout(int64_t T, int64_t n_seq) {
   L.flags = L.wpre + f;
   L.pflags = L.flags + b;
   L.logK = L.pflags + b;
-  L.total = L.logK + align_up(8 * (size_t)n_seq, 256);
+  L.part = L.logK + align_up(8 * (size_t)n_seq, 256);
+  L.zy = L.part + (seg ? align_up(8 * (size_t)kSegMax * (size_t)T, 256) : 0);
+  L.total = L.zy + (seg ? f : 0);
+  L.seg = seg;
   return L;
 }
 constexpr size_t ws_bytes(int64_t T) { return ws_layout(T, 0).total; }
@@ -135,6 +145,26 @@ struct RowArgs {
   float* eps_out;           // nullable; rate-1 path only (the pre-pass writes it otherwise)
   float clip_low, clip_high;
 };
+
+// Split forward pass (cis_seg_kernel, cis_combine_kernel).
+struct SegArgs {
+  float2* part;    // [T * kSegMax] (max, exp-sum without the sampled logit) per segment
+  float* zy;       // [T] the sampled logit
+  int32_t nseg;    // segments per row (<= kSegMax)
+  int32_t segvec;  // 16-byte vectors per segment (kSegBlock * K)
+};
+constexpr int kCombineBlock = 256;
+// A compiled segment kernel: `block` threads with K 16-byte vectors each, so block * K vectors
+// per segment.
+struct SegVariant {
+  int block, k;
+  const void* fn;
+};
+// The segment kernel for rows of `nvec` vectors, or nullptr when the row kernel serves them
+// better (short rows) or they need more than kSegMax segments of the largest variant.
+const SegVariant* select_seg_variant(int dtype, int32_t nvec);
+const void* combine_kernel(bool ext);
+const void* combine_kernel_ext();
 
 struct FinalizeArgs {
   const float* terms_ws;

@@ -3,6 +3,7 @@
 // kernel of Algorithm 1. The row kernel itself is in cis_row.h.
 #define CIS_EXT false
 #include "cis_row.h"
+#include "cis_seg.h"
 
 namespace cis {
 
@@ -124,6 +125,30 @@ const RowVariant& select_row_variant(int dtype, bool bwd, int32_t nvec) {
   constexpr int nf = sizeof(kBf16Fwd) / sizeof(kBf16Fwd[0]);
   const RowVariant* t = dtype == CIS_BF16 ? (bwd ? kBf16Bwd : kBf16Fwd) : (bwd ? kF32Bwd : kF32Fwd);
   return pick_variant(t, bwd ? nb : nf, nvec);
+}
+
+// Split forward pass. Rows shorter than kSegMinVec vectors stay with the row kernel (one short
+// row per workgroup is already a small independent read); longer rows take the first variant
+// that covers them with at most kSegMax segments.
+constexpr int32_t kSegMinVec = 2048;
+#define CIS_SEG(E, B, K, RE) SegVariant{B, K, (const void*)&cis_seg_kernel<E, B, K, RE>}
+// 128-thread workgroups of 8 vectors each (16 KiB of bf16 logits) measured best at V = 32768,
+// 151936 and 262144 among 64-256 threads x 4-16 vectors; longer rows take longer segments.
+static const SegVariant kSegBf16[] = {CIS_SEG(Bf16, 128, 8, true), CIS_SEG(Bf16, 128, 16, true),
+                                      CIS_SEG(Bf16, 256, 16, true)};
+static const SegVariant kSegF32[] = {CIS_SEG(F32, 128, 8, true), CIS_SEG(F32, 128, 16, true),
+                                     CIS_SEG(F32, 256, 16, true)};
+
+const SegVariant* select_seg_variant(int dtype, int32_t nvec) {
+  if (nvec < kSegMinVec) return nullptr;
+  const SegVariant* t = dtype == CIS_BF16 ? kSegBf16 : kSegF32;
+  for (int i = 0; i < 3; ++i)
+    if ((int64_t)t[i].block * t[i].k * kSegMax >= nvec) return &t[i];
+  return nullptr;
+}
+
+const void* combine_kernel(bool ext) {
+  return ext ? combine_kernel_ext() : (const void*)&cis_combine_kernel<false>;
 }
 
 const void* finalize_kernel() { return (const void*)&cis_finalize_kernel; }

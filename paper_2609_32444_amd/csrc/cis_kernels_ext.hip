@@ -4,6 +4,7 @@
 // decoupled path's pre-pass).
 #define CIS_EXT true
 #include "cis_row.h"
+#include "cis_seg.h"
 
 namespace cis {
 
@@ -120,6 +121,7 @@ __global__ __launch_bounds__(kWeightsBlock) void cis_prepass_kernel(const Prepas
 }
 
 const void* seq_sum_kernel() { return (const void*)&cis_seq_sum_kernel; }
+const void* combine_kernel_ext() { return (const void*)&cis_combine_kernel<true>; }
 const void* prepass_kernel() { return (const void*)&cis_prepass_kernel; }
 
 }  // namespace cis

@@ -524,6 +524,98 @@ __device__ __forceinline__ float displacement(float lp, float lq, float one_m_p)
   return logk - (logf(one_m_p) - logf(one_m_q));
 }
 
+// Epilogue of a valid row (every thread of the row's workgroup or wave computes the same values
+// from the same inputs; `writer` stores the per-row outputs): from the row's max M (sampled
+// element included), its complement exp-sum sr = sum_{j != y} exp(z_j - M) and the sampled
+// logit zy, the training log-probability, 1 - p, the weight (Algorithm 1, an operator of the
+// family, or the decoupled path's pre-pass weight with the clipped ratio of Eq. (1)) and the
+// loss term. Returns the gradient coefficient, the log-sum-exp and 1 - p.
+struct RowResult {
+  float coef, lse, one_m_p;
+};
+template <bool EXT>
+__device__ __forceinline__ RowResult row_epilogue(const RowArgs& a, const RowScalars& rsc,
+                                                  int64_t row, float M, float sr, float zy,
+                                                  bool writer) {
+  const float s_rest = sr;
+  const float e_y = expf(zy - M);
+  const float ssum = e_y + s_rest;
+  const float lse = M + logf(ssum);
+  const float ltr = (e_y >= s_rest) ? -log1pf(s_rest / e_y) : (zy - M) - logf(ssum);
+  const float one_m_p = s_rest / ssum;
+  float coef = 0.f;
+  float w, term, logk = 0.f, excess = 0.f, eps = 0.f;
+  bool acted, bad = false;
+  const bool decoupled = EXT && a.logp_old != nullptr;
+  if (!EXT) {
+    // CIS weight (Algorithm 1) at update ratio 1
+    const float delta = ltr - rsc.logp_infer;
+    const float lam_phi = a.lam * fmaxf(one_m_p, a.kappa);
+    acted = delta > log1pf(lam_phi);
+    const float k = expf(delta);
+    w = acted ? 1.0f + lam_phi : k;
+    excess = acted ? k - w : 0.f;
+    logk = delta;
+    coef = a.scale * w * rsc.adv;
+    term = (coef == 0.f) ? 0.f : coef * ltr;
+  } else if (decoupled) {
+    // Eq. (1): scale * w * min(rho A, clip(rho) A), rho = p(theta) / p_old; the gradient
+    // flows where rho*A is the smaller branch
+    w = rsc.wpre;
+    acted = rsc.pacted;
+    const float rho = expf(ltr - rsc.logp_old);
+    const float A = rsc.adv;
+    const bool gate = (A > 0.f && rho <= 1.f + a.clip_high) || (A < 0.f && rho >= 1.f - a.clip_low);
+    const float sw = a.scale * w;
+    const float clipped = fminf(fmaxf(rho, 1.f - a.clip_low), 1.f + a.clip_high);
+    term = (sw == 0.f || A == 0.f) ? 0.f : sw * fminf(rho * A, clipped * A);
+    coef = gate ? sw * A * rho : 0.f;
+    bad = isnan(rho);
+  } else {
+    // any token operator at update ratio 1
+    w = op_weight(a.ops, ltr, rsc.logp_infer, one_m_p, acted);
+    logk = ltr - rsc.logp_infer;
+    const float k = expf(logk);
+    excess = (k == w) ? 0.f : k - w;
+    eps = displacement(ltr, rsc.logp_infer, one_m_p);
+    coef = a.scale * w * rsc.adv;
+    term = (coef == 0.f) ? 0.f : coef * ltr;
+  }
+  const bool nonfinite =
+      !(isfinite(lse) && M > kMinRef && M < kMaxRef) || isnan(w) || bad;
+  if (writer) {
+    if (a.logp_train_out) a.logp_train_out[row] = ltr;
+    if (a.terms_user) a.terms_user[row] = term;
+    a.terms_ws[row] = term;
+    a.flags_ws[row] = kFlagValid | (acted ? kFlagTrunc : 0) | (nonfinite ? kFlagNonFinite : 0);
+    if (!decoupled) {  // the decoupled path's pre-pass wrote these
+      if (a.w_out) a.w_out[row] = w;
+      if (a.trunc_out) a.trunc_out[row] = acted ? 1 : 0;
+      a.logk_ws[row] = logk;
+      a.excess_ws[row] = excess;
+      if (EXT && a.eps_out) a.eps_out[row] = eps;
+    }
+  }
+  return RowResult{coef, lse, one_m_p};
+}
+
+// Outputs of an invalid row (masked, or id out of range): zeros, and the bad-id flag for an
+// unmasked row.
+template <bool EXT>
+__device__ __forceinline__ void row_invalid(const RowArgs& a, const RowScalars& rsc, int64_t row) {
+  if (a.logp_train_out) a.logp_train_out[row] = 0.f;
+  if (a.terms_user) a.terms_user[row] = 0.f;
+  a.terms_ws[row] = 0.f;
+  a.flags_ws[row] = rsc.on ? kFlagBadId : 0;
+  if (!(EXT && a.logp_old)) {
+    if (a.w_out) a.w_out[row] = 0.f;
+    if (a.trunc_out) a.trunc_out[row] = 0;
+    a.logk_ws[row] = 0.f;
+    a.excess_ws[row] = 0.f;
+    if (EXT && a.eps_out) a.eps_out[row] = 0.f;
+  }
+}
+
 // One persistent workgroup per row at a time.
 //   BWD: write the gradient (sweep 2); otherwise forward only.
 //   PF:  refill each register with the next row's vector during the row's last sweep, so the
@@ -739,80 +831,15 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
       const float zy = sh_zy[buf];
       buf ^= 1;
       // M: max over the row (sampled element included); sr: sum_{j != y} exp(z_j - M).
-      const float s_rest = sr;
-      const float e_y = expf(zy - M);
-      const float ssum = e_y + s_rest;
-      const float lse = M + logf(ssum);
-      const float ltr = (e_y >= s_rest) ? -log1pf(s_rest / e_y) : (zy - M) - logf(ssum);
-      one_m_p = s_rest / ssum;
-      float w, term, logk = 0.f, excess = 0.f, eps = 0.f;
-      bool acted, bad = false;
-      const bool decoupled = EXT && a.logp_old != nullptr;
-      if (!EXT) {
-        // CIS weight (Algorithm 1) at update ratio 1
-        const float delta = ltr - rsc.logp_infer;
-        const float lam_phi = a.lam * fmaxf(one_m_p, a.kappa);
-        acted = delta > log1pf(lam_phi);
-        const float k = expf(delta);
-        w = acted ? 1.0f + lam_phi : k;
-        excess = acted ? k - w : 0.f;
-        logk = delta;
-        coef = a.scale * w * rsc.adv;
-        term = (coef == 0.f) ? 0.f : coef * ltr;
-      } else if (decoupled) {
-        // Eq. (1): scale * w * min(rho A, clip(rho) A), rho = p(theta) / p_old; the gradient
-        // flows where rho*A is the smaller branch
-        w = rsc.wpre;
-        acted = rsc.pacted;
-        const float rho = expf(ltr - rsc.logp_old);
-        const float A = rsc.adv;
-        const bool gate = (A > 0.f && rho <= 1.f + a.clip_high) || (A < 0.f && rho >= 1.f - a.clip_low);
-        const float sw = a.scale * w;
-        const float clipped = fminf(fmaxf(rho, 1.f - a.clip_low), 1.f + a.clip_high);
-        term = (sw == 0.f || A == 0.f) ? 0.f : sw * fminf(rho * A, clipped * A);
-        coef = gate ? sw * A * rho : 0.f;
-        bad = isnan(rho);
-      } else {
-        // any token operator at update ratio 1
-        w = op_weight(a.ops, ltr, rsc.logp_infer, one_m_p, acted);
-        logk = ltr - rsc.logp_infer;
-        const float k = expf(logk);
-        excess = (k == w) ? 0.f : k - w;
-        eps = displacement(ltr, rsc.logp_infer, one_m_p);
-        coef = a.scale * w * rsc.adv;
-        term = (coef == 0.f) ? 0.f : coef * ltr;
-      }
-      const bool nonfinite =
-          !(isfinite(lse) && M > kMinRef && M < kMaxRef) || isnan(w) || bad;
-      if (tid == 0) {
-        if (a.logp_train_out) a.logp_train_out[row] = ltr;
-        if (a.terms_user) a.terms_user[row] = term;
-        a.terms_ws[row] = term;
-        a.flags_ws[row] = kFlagValid | (acted ? kFlagTrunc : 0) | (nonfinite ? kFlagNonFinite : 0);
-        if (!decoupled) {  // the decoupled path's pre-pass wrote these
-          if (a.w_out) a.w_out[row] = w;
-          if (a.trunc_out) a.trunc_out[row] = acted ? 1 : 0;
-          a.logk_ws[row] = logk;
-          a.excess_ws[row] = excess;
-          if (EXT && a.eps_out) a.eps_out[row] = eps;
-        }
-      }
+      const RowResult rr = row_epilogue<EXT>(a, rsc, row, M, sr, zy, tid == 0);
+      coef = rr.coef;
+      one_m_p = rr.one_m_p;
       // g_j = -coef * exp(z_j - lse) = sign * exp2(z_j*log2e - b2) with sign = -sign(coef)
       // and b2 = (lse - ln|coef|) * log2e; coef = 0 keeps b2 = +inf, which gives an all-zero
       // row. The float32 offset is accurate to a few 1e-6 relative, far inside bf16 rounding.
-      if (BWD && coef != 0.f) b2 = (lse - logf(fabsf(coef))) * kLog2e;
+      if (BWD && coef != 0.f) b2 = (rr.lse - logf(fabsf(coef))) * kLog2e;
     } else if (tid == 0) {
-      if (a.logp_train_out) a.logp_train_out[row] = 0.f;
-      if (a.terms_user) a.terms_user[row] = 0.f;
-      a.terms_ws[row] = 0.f;
-      a.flags_ws[row] = rsc.on ? kFlagBadId : 0;
-      if (!(EXT && a.logp_old)) {
-        if (a.w_out) a.w_out[row] = 0.f;
-        if (a.trunc_out) a.trunc_out[row] = 0;
-        a.logk_ws[row] = 0.f;
-        a.excess_ws[row] = 0.f;
-        if (EXT && a.eps_out) a.eps_out[row] = 0.f;
-      }
+      row_invalid<EXT>(a, rsc, row);
     }
 
     // ---- sweep 2: gradient ----------------------------------------------------------------

@@ -43,8 +43,9 @@ def test_workspace_bytes_layout():
     assert cis.workspace_bytes(0) == 256
     for T in (1, 255, 256, 16384, 65536, 524288):
         n = cis.workspace_bytes(T)
-        # stats, four float arrays and two byte arrays per row
-        assert n % 256 == 0 and n >= 256 + 18 * T
+        # stats, four float arrays and two byte arrays per row, and the forward pass's
+        # per-segment partials (32 float pairs) and sampled logit per row
+        assert n % 256 == 0 and n >= 256 + (18 + 32 * 8 + 4) * T
         assert cis.workspace_bytes_ex(T, 0) == n
         assert cis.workspace_bytes_ex(T, 1000) >= n + 8 * 1000
     assert cis.workspace_bytes_ex(-1, 0) == 0 and cis.workspace_bytes_ex(4, -1) == 0
@@ -201,9 +202,9 @@ def test_lmhead_workspace_bytes():
     f = cis.lmhead_workspace_bytes
     T, V, H = 16384, 151936, 2048
     fwd, bwd = f(T, V, H, 4096, 0, False), f(T, V, H, 4096, 0, True)
-    loss = cis.workspace_bytes_ex(T, 0)
-    # the loss workspace plus one float32 chunk of logits; the backward adds W^T and the two
-    # transposed chunk operands
+    loss = 256 + 18 * T
+    # the loss rows' scratch plus one float32 chunk of logits; the backward adds W^T and the
+    # two transposed chunk operands
     assert fwd >= loss + 4 * 4096 * V and fwd % 256 == 0
     assert bwd >= fwd + 2 * V * H + 2 * (V + H) * 4096
     # a chunk larger than the batch only needs the batch's rows

@@ -71,12 +71,16 @@ def test_long_rows_many_per_workgroup(V, dtype):
     run_and_check(b)
 
 
-# forward-pass capacities (vectors): 128, 256, 512, 1024, 2048, 4096, 8192, 12288, then 19456
-# (bf16) or 16384 (fp32), beyond which rows stream
+# Forward pass: rows of fewer than 2048 16-byte vectors go through the row kernel (capacities
+# 128, 256, 512, 1024, 2048 vectors); rows of 2048 up to 131072 vectors through the split
+# kernels (segments of 1024, 2048 or 4096 vectors, at most 32 per row); longer rows through the
+# streamed row kernel. The list puts rows at and just past each boundary, with ragged ends.
 @pytest.mark.parametrize("V,dtype", [(V, torch.bfloat16) for V in
-                                     (1000, 2048, 4000, 8000, 16000, 30001, 60000, 90001, 151936,
-                                      155649, 262144)] +
-                                    [(V, torch.float32) for V in (1000, 16000, 60001, 65537)])
+                                     (1000, 2048, 4000, 8000, 16000, 16384, 16392, 30001, 60000,
+                                      90001, 131080, 151936, 155649, 262144, 262152, 524296,
+                                      1048576, 1048584)] +
+                                    [(V, torch.float32) for V in (1000, 8192, 16000, 60001, 65537,
+                                                                  131072, 131076)])
 def test_forward_only_matches(V, dtype):
     epv = 8 if dtype == torch.bfloat16 else 4
     ld = ((V + epv - 1) // epv) * epv
@@ -105,25 +109,32 @@ def test_empty_batch():
     assert cis.read_stats(out["workspace"])["n_valid"] == 0
 
 
-def test_all_masked_and_invalid_ids():
-    b = make_random_batch(32, 3000, torch.bfloat16, DEV, seed=2)
+@pytest.mark.parametrize("V,bwd", [(3000, True), (3000, False), (40000, False)])
+def test_all_masked_and_invalid_ids(V, bwd):
+    """(V = 40000 runs the forward pass through the split-row kernels.)"""
+    b = make_random_batch(32, V, torch.bfloat16, DEV, seed=2)
     b.mask.zero_()
-    out, ref, _ = run_and_check(b)
-    assert torch.count_nonzero(out["dlogits"]) == 0 and out["loss"].item() == 0.0
-    b = make_random_batch(32, 3000, torch.bfloat16, DEV, seed=3)
+    out, ref, _ = run_and_check(b, bwd=bwd)
+    assert out["loss"].item() == 0.0
+    if bwd:
+        assert torch.count_nonzero(out["dlogits"]) == 0
+    b = make_random_batch(32, V, torch.bfloat16, DEV, seed=3)
     b.ids[::3] = -1
-    b.ids[1::5] = 3000
+    b.ids[1::5] = V
     b.ids[2::7] = 1 << 40
-    out, ref, _ = run_and_check(b)
+    out, ref, _ = run_and_check(b, bwd=bwd)
     st = cis.read_stats(out["workspace"])
     assert st["n_bad_id"] > 0
-    bad = ((b.ids < 0) | (b.ids >= 3000)) & (b.mask > 0)
-    assert torch.count_nonzero(out["dlogits"][bad]) == 0
+    bad = ((b.ids < 0) | (b.ids >= V)) & (b.mask > 0)
+    if bwd:
+        assert torch.count_nonzero(out["dlogits"][bad]) == 0
 
 
-def test_confident_rows_and_extremes():
-    """p -> 1 (1 - p down to ~1e-30), l_infer = -inf, z_y = -inf, -inf and huge-negative logits."""
-    T, V = 16, 5000
+@pytest.mark.parametrize("V,bwd", [(5000, True), (5000, False), (151936, True), (151936, False)])
+def test_confident_rows_and_extremes(V, bwd):
+    """p -> 1 (1 - p down to ~1e-30), l_infer = -inf, z_y = -inf, -inf and huge-negative logits;
+    fused and forward only, on short rows and on rows of the split forward pass."""
+    T = 16
     b = make_random_batch(T, V, torch.bfloat16, DEV, seed=4, mask_p=1.0)
     z = b.logits
     y = b.ids
@@ -137,7 +148,7 @@ def test_confident_rows_and_extremes():
     z[11, y[11]] = 0.5
     z[12, 7] = -math.inf
     b.logp_infer[13] = 0.0
-    out, ref, rep = run_and_check(b)
+    out, ref, rep = run_and_check(b, bwd=bwd)
     assert out["w"][9].item() == 0.0 and out["trunc"][8].item() == 1
     for t in range(8):
         lt = out["logp_train"][t].item()
