@@ -312,7 +312,8 @@ def bench_lmhead(args, torch, cis):
     lold = b.logp_old if args.decoupled else None
     offs = b.offsets if op.startswith("seq_") else None
     n_seq = 0 if offs is None else offs.numel() - 1
-    ws = torch.empty(cis.lmhead_workspace_bytes(T, V, H, chunk, n_seq, bwd), dtype=torch.uint8,
+    rec = bool(args.recompute)
+    ws = torch.empty(cis.lmhead_workspace_bytes(T, V, H, chunk, n_seq, bwd, rec), dtype=torch.uint8,
                      device="cuda")
     dh = torch.empty(T, H, dtype=torch.float32, device="cuda") if bwd else None
     dw = torch.empty(V, H, dtype=torch.float32, device="cuda") if bwd else None
@@ -321,7 +322,8 @@ def bench_lmhead(args, torch, cis):
         def step():
             return cis.lmhead_loss_bwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
                                        params=prm, logp_old=lold, seq_offsets=offs, chunk=chunk,
-                                       dhidden=dh, dweight=dw, want=want, workspace=ws)
+                                       dhidden=dh, dweight=dw, want=want, workspace=ws,
+                                       recompute=rec)
     else:
         def step():
             return cis.lmhead_loss_fwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
@@ -347,7 +349,7 @@ def bench_lmhead(args, torch, cis):
     avg_call_ms = sum(per_call) / len(per_call)
     stats = cis.read_stats(ws)
     n_valid = stats["n_valid"]
-    flops = (3 if bwd else 1) * 2.0 * T * V * H
+    flops = (3 if bwd else 1) * 2.0 * T * V * H   # algorithmic: the recompute's 4th product is not
     tflops = flops / (avg_call_ms * 1e-3) / 1e12
     line = {
         "metric": f"tokens/sec, CIS loss {'fwd+bwd' if bwd else 'fwd'} through the LM head "
@@ -367,8 +369,11 @@ def bench_lmhead(args, torch, cis):
         "config": {"workload": f"moe-rollout LM head T={T} V={V} H={H} bf16 chunk={chunk} "
                                f"c={args.c:g} {'fused fwd+bwd' if bwd else 'forward only'}"
                                + (f" op={op}" if ext else "")
-                               + (" decoupled PPO-clip (0.2, 0.28)" if args.decoupled else ""),
+                               + (" decoupled PPO-clip (0.2, 0.28)" if args.decoupled else "")
+                               + (" logits recomputed (never stored)" if bwd and rec else "")
+                               + (" logits never stored" if not bwd else ""),
                    "T": T, "V": V, "H": H, "chunk": chunk, "valid_tokens": n_valid,
+                   "recompute": rec if bwd else None,
                    "lambda": b.lam, "kappa": b.kappa, "seed": b.meta["seed"]},
         "roofline": {
             "bound": "mfma",
@@ -377,7 +382,7 @@ def bench_lmhead(args, torch, cis):
             "unit": "TFLOP/s",
             "frac": tflops / MFMA_BF16_PEAK_TFLOPS,
             "traffic": lmhead_traffic() if bwd and chunk == 4096 and H == 2048 and not ext
-            else None,
+            and not rec else None,
             "traffic_scope": "HBM bytes per call, every kernel of the call (rocprofv3 counters)",
             "algorithmic_flops_per_call": flops,
             "avg_call_ms": avg_call_ms,
@@ -417,6 +422,8 @@ def make_parser() -> argparse.ArgumentParser:
                     help="the loss behind the LM head (hidden [T, H] x weight [V, H], bf16)")
     ap.add_argument("--hidden", type=int, default=2048, help="--lmhead: hidden size H")
     ap.add_argument("--chunk", type=int, default=4096, help="--lmhead: rows per chunk")
+    ap.add_argument("--recompute", action="store_true",
+                    help="--lmhead backward: never store the logits (the product is formed twice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-ceiling", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",

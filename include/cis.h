@@ -332,14 +332,23 @@ int cis_loss_bwd_ex(const void* logits, int dtype, int64_t T, int64_t V, int64_t
  *   dL/dh = G W        and        dL/dW = G^T h,        G = dL/dz  (chunk by chunk),
  *
  * with G rounded to bf16 as the operand of those two products (float32 accumulation).
+ *
+ * The forward never stores the logits: the product's epilogue reduces each row's float32
+ * logits to one (max, exp-sum) pair per 64 columns, and a per-row pass folds them. The
+ * backward has two ways to obtain G: by default each chunk's float32 logits are kept in the
+ * workspace (one chunk at a time) and the row kernel turns them into G; with recompute = 1
+ * they are never stored, and the product is formed a second time with an epilogue that writes
+ * G (four products instead of three, and 4 * min(T, chunk) * V bytes less workspace).
  * ========================================================================================= */
 
-/* Workspace bytes for cis_lmhead_loss_fwd (with_grad = 0) or _bwd (with_grad != 0): the loss
- * workspace of cis_workspace_bytes_ex plus the chunk's float32 logits (min(T, chunk) x V) and,
- * with gradients, W^T, the chunk's bf16 dL/dz and the transposed operands of one dL/dW group
- * (about 2*V*H + 2*V*chunk + 2*(V + H)*min(T, group) bytes; group as for cis_lmhead_loss_bwd).
- * Returns 0 for T < 0, V outside [1, 2^22], H outside [1, 2^16], chunk outside [1, 2^16] or
- * n_seq < 0. */
+/* Workspace bytes for cis_lmhead_loss_fwd (with_grad = 0), cis_lmhead_loss_bwd (with_grad = 1)
+ * or cis_lmhead_loss_bwd with recompute (with_grad = 2): the loss workspace of
+ * cis_workspace_bytes_ex plus, per chunk row, 8 bytes per 64 vocabulary columns and 20 bytes
+ * (with_grad = 0 or 2) or the row's float32 logits (with_grad = 1), and with gradients W^T, the
+ * chunk's bf16 dL/dz and the transposed operands of one dL/dW group (about 2*V*H + 2*V*chunk +
+ * 2*(V + H)*min(T, group) bytes; group as for cis_lmhead_loss_bwd). Returns 0 for T < 0, V
+ * outside [1, 2^22], H outside [1, 2^16], chunk outside [1, 2^16], n_seq < 0 or with_grad
+ * outside 0..2. */
 size_t cis_lmhead_workspace_bytes(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_t n_seq,
                                   int with_grad);
 
@@ -351,8 +360,8 @@ size_t cis_lmhead_workspace_bytes(int64_t T, int64_t V, int64_t H, int64_t chunk
  *                           of 8, base 16-byte aligned
  *   weight [V, ld_w] bf16   head weight (row v produces logit v), 1 <= V <= 2^22; H <= ld_w <=
  *                           2^22, a multiple of 8, base 16-byte aligned
- *   chunk                   rows per chunk (1 <= chunk <= 2^16); the workspace holds one
- *                           chunk of float32 logits. Results do not depend on chunk.
+ *   chunk                   rows per chunk (1 <= chunk <= 2^16): rows whose logits are formed
+ *                           by one product. Results do not depend on chunk.
  *   ids, logp_infer, logp_old, adv, mask, seq_offsets, n_seq, params and the per-row outputs
  *                           as for cis_loss_fwd_ex
  *   workspace               >= cis_lmhead_workspace_bytes(T, V, H, chunk, n_seq, 0), 256-byte
@@ -380,9 +389,14 @@ int cis_lmhead_loss_fwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
  *                                partial sums added group by group: a group is
  *                                chunk * floor(16384 / chunk) rows when chunk is a multiple of 8
  *                                below 16384, otherwise chunk rows.
- *   workspace                    >= cis_lmhead_workspace_bytes(T, V, H, chunk, n_seq, 1)
+ *   recompute                    0: keep each chunk's float32 logits in the workspace while
+ *                                its G is formed (faster); 1: never store them and form the
+ *                                logits product twice (less workspace). Results agree to float32
+ *                                rounding of the log-sum-exp (not bit for bit).
+ *   workspace                    >= cis_lmhead_workspace_bytes(T, V, H, chunk, n_seq,
+ *                                1 + recompute)
  * dhidden and dweight must not overlap each other, hidden, weight or the used part of the
- * workspace (CIS_ERR_ALIAS otherwise).
+ * workspace (CIS_ERR_ALIAS otherwise). recompute outside 0..1 is CIS_ERR_PARAM.
  */
 int cis_lmhead_loss_bwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
                         const void* weight, int64_t V, int64_t ld_w,
@@ -390,7 +404,7 @@ int cis_lmhead_loss_bwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
                         const float* adv, const uint8_t* mask, const int64_t* seq_offsets,
                         int64_t n_seq, const cis_params_t* params, int64_t chunk,
                         float* dhidden, int64_t ld_dh, float* dweight, int64_t ld_dw,
-                        int accumulate_dweight,
+                        int accumulate_dweight, int recompute,
                         float* logp_train_out, float* w_out, uint8_t* acted_out,
                         float* loss_terms_out, float* eps_out, float* loss_out,
                         void* workspace, size_t workspace_bytes, hipStream_t stream);

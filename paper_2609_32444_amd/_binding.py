@@ -101,7 +101,7 @@ def load_library() -> ctypes.CDLL:
     lib.cis_lmhead_loss_fwd.restype = _int
     lib.cis_lmhead_loss_bwd.argtypes = [_vp, _i64, _i64, _i64, _vp, _i64, _i64, _vp, _vp, _vp,
                                         _vp, _vp, _vp, _i64, ctypes.POINTER(Params), _i64,
-                                        _vp, _i64, _vp, _i64, _int,
+                                        _vp, _i64, _vp, _i64, _int, _int,
                                         _vp, _vp, _vp, _vp, _vp, _vp, _vp, _size, _vp]
     lib.cis_lmhead_loss_bwd.restype = _int
     _LIB = lib
@@ -121,9 +121,12 @@ def workspace_bytes_ex(T: int, n_seq: int = 0) -> int:
 
 
 def lmhead_workspace_bytes(T: int, V: int, H: int, chunk: int, n_seq: int = 0,
-                           with_grad: bool = True) -> int:
+                           with_grad: bool = True, recompute: bool = False) -> int:
+    """cis_lmhead_workspace_bytes: forward (with_grad=False), backward, or backward with
+    recompute (the logits never stored)."""
+    mode = (2 if recompute else 1) if with_grad else 0
     return int(load_library().cis_lmhead_workspace_bytes(int(T), int(V), int(H), int(chunk),
-                                                         int(n_seq), int(bool(with_grad))))
+                                                         int(n_seq), mode))
 
 
 def lambda_from_logodds(c: float) -> float:
@@ -518,7 +521,7 @@ def _bf16_matrix(name, t, rows, dev):
 
 
 def _lmhead(bwd, hidden, weight, ids, logp_infer, adv, mask, prm, logp_old, seq_offsets, chunk,
-            dhidden, dweight, accumulate, want, workspace):
+            dhidden, dweight, accumulate, want, workspace, recompute=False):
     dev = hidden.device
     T, H = hidden.shape
     V = weight.shape[0]
@@ -532,7 +535,8 @@ def _lmhead(bwd, hidden, weight, ids, logp_infer, adv, mask, prm, logp_old, seq_
     _check_vec("logp_old", logp_old, T, torch.float32, dev, optional=True)
     mask = _check_vec("mask", _mask_u8(mask), T, torch.uint8, dev, optional=True)
     offs, n_seq = _offsets(seq_offsets, T, dev)
-    workspace = _workspace(workspace, lmhead_workspace_bytes(T, V, H, chunk, n_seq, bwd), dev)
+    workspace = _workspace(workspace,
+                           lmhead_workspace_bytes(T, V, H, chunk, n_seq, bwd, recompute), dev)
     out = {}
     for k in want:
         out[k] = torch.empty(T, dtype=torch.uint8 if k == "acted" else torch.float32, device=dev)
@@ -557,7 +561,8 @@ def _lmhead(bwd, hidden, weight, ids, logp_infer, adv, mask, prm, logp_old, seq_
                         or g.shape[0] != rows or g.shape[1] < H or g.stride(1) != 1:
                     raise ValueError(f"{name} must be a float32 [{rows}, >={H}] tensor on {dev}")
             rc = lib.cis_lmhead_loss_bwd(*head, _ptr(dhidden), dhidden.stride(0), _ptr(dweight),
-                                         dweight.stride(0), int(bool(accumulate)), *tail)
+                                         dweight.stride(0), int(bool(accumulate)),
+                                         int(bool(recompute)), *tail)
             fn = "cis_lmhead_loss_bwd"
         else:
             rc = lib.cis_lmhead_loss_fwd(*head, *tail)
@@ -583,9 +588,10 @@ def lmhead_loss_fwd(hidden, weight, ids, logp_infer, adv, mask=None, *, params: 
 
 def lmhead_loss_bwd(hidden, weight, ids, logp_infer, adv, mask=None, *, params: Params,
                     logp_old=None, seq_offsets=None, chunk=LMHEAD_CHUNK, dhidden=None,
-                    dweight=None, accumulate=False, want=_ALL_EX, workspace=None):
+                    dweight=None, accumulate=False, want=_ALL_EX, workspace=None,
+                    recompute=False):
     """Forward and backward through the head (cis_lmhead_loss_bwd): lmhead_loss_fwd's keys plus
     "dhidden" [T, H] and "dweight" [V, H], float32 (dweight accumulated into when
-    accumulate=True)."""
+    accumulate=True). recompute=True never stores the logits (the product is formed twice)."""
     return _lmhead(True, hidden, weight, ids, logp_infer, adv, mask, params, logp_old,
-                   seq_offsets, chunk, dhidden, dweight, accumulate, want, workspace)
+                   seq_offsets, chunk, dhidden, dweight, accumulate, want, workspace, recompute)

@@ -214,18 +214,14 @@ int launch_prepass(const LossCall& c, const Ws& ws, const DeviceInfo& info, hipS
 template <class P>
 P* at(P* p, int64_t t0) { return p ? p + t0 : nullptr; }
 
-// The row kernel over rows [t0, t0 + rows) of the call: `logits` / `dlogits` point at the first
-// of those rows (row strides ld, ld_g elements of c.dtype); per-row arrays are indexed from t0.
-int launch_rows(const LossCall& c, const Ws& ws, const void* logits, void* dlogits, int64_t ld,
-                int64_t ld_g, int64_t t0, int64_t rows, int dev, const DeviceInfo& info,
-                hipStream_t stream) {
-  if (rows <= 0) return CIS_OK;
+// Row-kernel arguments for rows [t0, t0 + rows) of the call: `logits` / `dlogits` point at the
+// first of those rows (row strides ld, ld_g elements of c.dtype); per-row arrays are indexed
+// from t0.
+cis::RowArgs row_args(const LossCall& c, const Ws& ws, const void* logits, void* dlogits,
+                      int64_t ld, int64_t ld_g, int64_t t0, int64_t rows) {
   const int esize = c.dtype == CIS_BF16 ? 2 : 4;
   const int gsize = c.bf16_grad ? 2 : esize;
   const int32_t nvec = (int32_t)((c.V + 16 / esize - 1) / (16 / esize));
-  const cis::RowVariant& var = c.ext
-                                   ? cis::select_row_variant_ext(c.dtype, c.bwd, nvec, c.bf16_grad)
-                                   : cis::select_row_variant(c.dtype, c.bwd, nvec);
   cis::RowArgs ra{};
   ra.logits = logits;
   ra.dlogits = dlogits;
@@ -256,6 +252,31 @@ int launch_rows(const LossCall& c, const Ws& ws, const void* logits, void* dlogi
   ra.eps_out = at(c.eps_out, t0);
   ra.clip_low = c.prm.clip_low;
   ra.clip_high = c.prm.clip_high;
+  return ra;
+}
+
+// cis_combine_kernel over rows [t0, t0 + rows): their pieces (max, exp-sum) folded and the
+// epilogue run.
+int launch_combine(const LossCall& c, cis::RowArgs& ra, cis::SegArgs& sa, int64_t rows,
+                   hipStream_t stream) {
+  void* args[] = {&ra, &sa};
+  const int64_t per = cis::kCombineBlock / 64;
+  return hipLaunchKernel(cis::combine_kernel(c.ext), dim3((unsigned)((rows + per - 1) / per)),
+                         dim3(cis::kCombineBlock), args, 0, stream) == hipSuccess
+             ? CIS_OK
+             : CIS_ERR_LAUNCH;
+}
+
+// The row kernel over rows [t0, t0 + rows) of the call (see row_args).
+int launch_rows(const LossCall& c, const Ws& ws, const void* logits, void* dlogits, int64_t ld,
+                int64_t ld_g, int64_t t0, int64_t rows, int dev, const DeviceInfo& info,
+                hipStream_t stream) {
+  if (rows <= 0) return CIS_OK;
+  cis::RowArgs ra = row_args(c, ws, logits, dlogits, ld, ld_g, t0, rows);
+  const int32_t nvec = ra.nvec;
+  const cis::RowVariant& var = c.ext
+                                   ? cis::select_row_variant_ext(c.dtype, c.bwd, nvec, c.bf16_grad)
+                                   : cis::select_row_variant(c.dtype, c.bwd, nvec);
   // forward pass over long rows: segment kernel + combine (when the workspace has the room)
   const cis::SegVariant* sv =
       (!c.bwd && ws.L.seg) ? cis::select_seg_variant(c.dtype, nvec) : nullptr;
@@ -265,6 +286,7 @@ int launch_rows(const LossCall& c, const Ws& ws, const void* logits, void* dlogi
     sa.nseg = (int32_t)((nvec + sa.segvec - 1) / sa.segvec);
     sa.part = reinterpret_cast<float2*>(ws.base + ws.L.part) + t0 * cis::kSegMax;
     sa.zy = ws.f(ws.L.zy) + t0;
+    sa.stride = cis::kSegMax;
     void* args[] = {&ra, &sa};
     // one short-lived workgroup per (row, segment); the kernel loops only past 2^30 of them
     const int64_t total = rows * sa.nseg;
@@ -272,11 +294,7 @@ int launch_rows(const LossCall& c, const Ws& ws, const void* logits, void* dlogi
     if (hipLaunchKernel(sv->fn, dim3((unsigned)(total < cap ? total : cap)), dim3(sv->block),
                         args, 0, stream) != hipSuccess)
       return CIS_ERR_LAUNCH;
-    const int64_t per = cis::kCombineBlock / 64;
-    return hipLaunchKernel(cis::combine_kernel(c.ext), dim3((unsigned)((rows + per - 1) / per)),
-                           dim3(cis::kCombineBlock), args, 0, stream) == hipSuccess
-               ? CIS_OK
-               : CIS_ERR_LAUNCH;
+    return launch_combine(c, ra, sa, rows, stream);
   }
   const int per_cu = blocks_per_cu(var.fn, var.block, dev);
   const int64_t resident = (int64_t)per_cu * info.num_cu;
@@ -387,6 +405,7 @@ struct LmHeadCall {
   float* dweight;           // [V, ld_dw] float32
   int64_t ld_dh, ld_dw;
   bool accumulate;
+  bool recompute;           // backward: never store the logits (form the product twice)
 };
 
 int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
@@ -406,7 +425,8 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
   if (!aligned(c.workspace, 256)) return CIS_ERR_ALIGN;
   if (!aligned(m.weight, 16) || m.ld_w % 8 != 0) return CIS_ERR_ALIGN;
   if (T > 0 && (!aligned(m.hidden, 16) || m.ld_h % 8 != 0)) return CIS_ERR_ALIGN;
-  const cis::LmLayout LM = cis::lm_layout(T, V, H, m.chunk, n_seq, bwd);
+  // the forward never stores the logits; the backward keeps one chunk of them unless recompute
+  const cis::LmLayout LM = cis::lm_layout(T, V, H, m.chunk, n_seq, bwd, !bwd || m.recompute);
   if (c.workspace_bytes < LM.total) return CIS_ERR_WORKSPACE;
   if (bwd) {  // the gradients may not overlap each other, the operands or the workspace
     const Span dh = span_of(m.dhidden, T, H, m.ld_dh, 4), dw = span_of(m.dweight, V, H, m.ld_dw, 4);
@@ -446,16 +466,43 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
     const int64_t tc = T - t0 < m.chunk ? T - t0 : m.chunk;
     const int64_t g0 = t0 / group * group;  // first row of this chunk's dL/dW group
     const __bf16* hc = hid + t0 * m.ld_h;
-    // Z = h_c W^T (float32 logits of the chunk)
-    if (int rc = ok(cis::launch_gemm_nt(
-            cis::gemm_args(hc, m.weight, Z, tc, V, H, m.ld_h, m.ld_w, LM.ldz), false, nullptr,
-            queue, ncu, stream)))
-      return rc;
-    // loss rows; the backward writes G = dL/dz in bf16 (the operand of dL/dh)
-    if (int rc = launch_rows(c, ws, Z, bwd ? Gb : nullptr, LM.ldz, LM.ldv, t0, tc, dev, info,
-                             stream))
-      return rc;
-    if (!bwd) continue;
+    if (LM.fused) {
+      // the logits h_c W^T are never stored: the product's epilogue leaves per row and
+      // 256-column tile a (max, exp-sum) pair, the combine folds them and runs the loss
+      // epilogue, and the backward forms the product again with an epilogue that writes G
+      cis::GemmArgs ga = cis::gemm_args(hc, m.weight, nullptr, tc, V, H, m.ld_h, m.ld_w, 0);
+      ga.epi = cis::kEpiLse;
+      ga.e.ids = c.ids + t0;
+      ga.e.part = reinterpret_cast<float2*>(base + LM.tpart);
+      ga.e.ldp = LM.ntv;
+      ga.e.zy = reinterpret_cast<float*>(base + LM.tzy);
+      if (int rc = ok(cis::launch_gemm_epi(ga, queue, ncu, stream))) return rc;
+      cis::RowArgs ra = row_args(c, ws, nullptr, nullptr, 0, 0, t0, tc);
+      cis::SegArgs sa{};
+      sa.part = ga.e.part;
+      sa.zy = ga.e.zy;
+      sa.nseg = (int32_t)LM.ntv;
+      sa.stride = LM.ntv;
+      sa.gp = bwd ? reinterpret_cast<cis::GradParams*>(base + LM.tgp) : nullptr;
+      if (int rc = launch_combine(c, ra, sa, tc, stream)) return rc;
+      if (!bwd) continue;
+      ga.epi = cis::kEpiGrad;
+      ga.e.gp = sa.gp;
+      ga.e.G = Gb;
+      ga.e.ldg = LM.ldv;
+      if (int rc = ok(cis::launch_gemm_epi(ga, queue, ncu, stream))) return rc;
+    } else {
+      // Z = h_c W^T (float32 logits of the chunk)
+      if (int rc = ok(cis::launch_gemm_nt(
+              cis::gemm_args(hc, m.weight, Z, tc, V, H, m.ld_h, m.ld_w, LM.ldz), false, nullptr,
+              queue, ncu, stream)))
+        return rc;
+      // loss rows; the backward writes G = dL/dz in bf16 (the operand of dL/dh)
+      if (int rc = launch_rows(c, ws, Z, bwd ? Gb : nullptr, LM.ldz, LM.ldv, t0, tc, dev, info,
+                               stream))
+        return rc;
+      if (!bwd) continue;
+    }
     // G^T and h_c^T (operands of dL/dW) into the group's columns t0 - g0 ..
     if (int rc = ok(cis::launch_transpose(
             cis::TransposeArgs{Gb, Gt + (t0 - g0), nullptr, tc, V, LM.ldv, LM.ldc, 0}, false,
@@ -541,7 +588,8 @@ LmHeadCall lm_call(bool bwd, const void* hidden, int64_t T, int64_t H, int64_t l
                    const float* logp_infer, const float* logp_old, const float* adv,
                    const uint8_t* mask, const int64_t* offsets, int64_t n_seq,
                    const cis_params_t* params, int64_t chunk, float* dhidden, int64_t ld_dh,
-                   float* dweight, int64_t ld_dw, int accumulate, float* logp_train_out,
+                   float* dweight, int64_t ld_dw, int accumulate, int recompute,
+                   float* logp_train_out,
                    float* w_out, uint8_t* acted_out, float* terms_out, float* eps_out,
                    float* loss_out, void* workspace, size_t workspace_bytes) {
   LmHeadCall m{};
@@ -560,6 +608,7 @@ LmHeadCall lm_call(bool bwd, const void* hidden, int64_t T, int64_t H, int64_t l
   m.ld_dh = ld_dh;
   m.ld_dw = ld_dw;
   m.accumulate = accumulate != 0;
+  m.recompute = recompute != 0;
   return m;
 }
 
@@ -571,7 +620,8 @@ size_t cis_lmhead_workspace_bytes(int64_t T, int64_t V, int64_t H, int64_t chunk
                                   int with_grad) {
   if (T < 0 || V < 1 || H < 1 || chunk < 1 || n_seq < 0) return 0;
   if (V > cis::kLmMaxV || H > cis::kLmMaxH || chunk > cis::kLmMaxChunk) return 0;
-  return cis::lm_layout(T, V, H, chunk, n_seq, with_grad != 0).total;
+  if (with_grad < 0 || with_grad > 2) return 0;
+  return cis::lm_layout(T, V, H, chunk, n_seq, with_grad != 0, with_grad != 1).total;
 }
 
 int cis_lmhead_loss_fwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
@@ -585,7 +635,7 @@ int cis_lmhead_loss_fwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
   if (!params) return CIS_ERR_NULL;
   return run_lmhead(lm_call(false, hidden, T, H, ld_h, weight, V, ld_w, ids, logp_infer,
                             logp_old, adv, mask, seq_offsets, n_seq, params, chunk, nullptr, 0,
-                            nullptr, 0, 0, logp_train_out, w_out, acted_out, loss_terms_out,
+                            nullptr, 0, 0, 0, logp_train_out, w_out, acted_out, loss_terms_out,
                             eps_out, loss_out, workspace, workspace_bytes),
                     stream);
 }
@@ -596,13 +646,15 @@ int cis_lmhead_loss_bwd(const void* hidden, int64_t T, int64_t H, int64_t ld_h,
                         const uint8_t* mask, const int64_t* seq_offsets, int64_t n_seq,
                         const cis_params_t* params, int64_t chunk, float* dhidden,
                         int64_t ld_dh, float* dweight, int64_t ld_dw, int accumulate_dweight,
-                        float* logp_train_out, float* w_out, uint8_t* acted_out,
+                        int recompute, float* logp_train_out, float* w_out, uint8_t* acted_out,
                         float* loss_terms_out, float* eps_out, float* loss_out, void* workspace,
                         size_t workspace_bytes, hipStream_t stream) {
   if (!params) return CIS_ERR_NULL;
+  if (recompute != 0 && recompute != 1) return CIS_ERR_PARAM;
   return run_lmhead(lm_call(true, hidden, T, H, ld_h, weight, V, ld_w, ids, logp_infer,
                             logp_old, adv, mask, seq_offsets, n_seq, params, chunk, dhidden,
-                            ld_dh, dweight, ld_dw, accumulate_dweight, logp_train_out, w_out,
+                            ld_dh, dweight, ld_dw, accumulate_dweight, recompute, logp_train_out,
+                            w_out,
                             acted_out, loss_terms_out, eps_out, loss_out, workspace,
                             workspace_bytes),
                     stream);

@@ -4,11 +4,30 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "cis_internal.h"
+
 namespace cis {
 
-// C[M, N] (float32, row stride ldc) = alpha * A[M, K] * B[N, K]^T (+ C when accumulating).
-// A and B are bf16, row-major with K contiguous (row strides lda, ldb: multiples of 8 elements,
-// bases 16-byte aligned). Any M, N, K >= 0. The fields after alpha are set by launch_gemm_nt.
+// Epilogues of the logits product z = h W^T of a row chunk (A = h, B = W), which never store z:
+//   kEpiLse:  per row and 64-column block (4 per 256-column tile tn), the pair (max, sum of
+//             exp(z - max) leaving out the sampled column) into part[row * ldp + 4 tn + wn],
+//             and the sampled logit into zy[row];
+//   kEpiGrad: dL/dz of the row from its GradParams, rounded to bf16, into G[row * ldg + col].
+enum { kEpiStore = 0, kEpiLse = 1, kEpiGrad = 2 };
+struct GemmEpi {
+  const int64_t* ids;       // [M] sampled ids (kEpiLse)
+  float2* part;             // [M, ldp] (kEpiLse)
+  float* zy;                // [M] (kEpiLse)
+  int64_t ldp;
+  const GradParams* gp;     // [M] (kEpiGrad)
+  __bf16* G;                // [M, ldg] (kEpiGrad; ldg a multiple of 4)
+  int64_t ldg;
+};
+
+// C[M, N] (float32, row stride ldc) = alpha * A[M, K] * B[N, K]^T (+ C when accumulating), or
+// one of the row-loss epilogues above instead of C. A and B are bf16, row-major with K
+// contiguous (row strides lda, ldb: multiples of 8 elements, bases 16-byte aligned). Any M, N,
+// K >= 0. The fields after alpha are set by launch_gemm_nt.
 struct GemmArgs {
   const void* A;
   const void* B;
@@ -21,6 +40,8 @@ struct GemmArgs {
   int64_t c_split_stride;   // elements between the splits' partial outputs
   int64_t units;            // tiles x splits
   int* queue;               // kGemmQueues work counters (zero at launch), or null
+  int epi;                  // kEpiStore, kEpiLse or kEpiGrad
+  GemmEpi e;
 };
 
 inline GemmArgs gemm_args(const void* A, const void* B, float* C, int64_t M, int64_t N,
@@ -70,6 +91,9 @@ int64_t gemm_splitk_count(int64_t M, int64_t N, int64_t K, int num_cu);
 // by whichever workgroup takes it.
 hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int* queue, int num_cu,
                           hipStream_t stream);
+// The logits product of a row chunk with a row-loss epilogue (kEpiLse or kEpiGrad; no split-K,
+// no C): M rows of h, N = V columns of W.
+hipError_t launch_gemm_epi(GemmArgs g, int* queue, int num_cu, hipStream_t stream);
 hipError_t launch_transpose(TransposeArgs t, bool in_f32, hipStream_t stream);
 
 }  // namespace cis

@@ -193,12 +193,114 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, const f32x4 (&acc)
   }
 }
 
+constexpr float kLog2e = 1.44269504088896340736f;
+constexpr float kMinRef = -0x1p127f;  // floor of a running max: keeps max * log2(e) finite
+
+// Row-loss epilogue kEpiLse of a logits tile (rows m0.., vocabulary columns n0.., tile column
+// tn): per row and wave, the max over the wave's 64 columns and the sum of exp(z - max) leaving
+// out the sampled column, one pair in part[row * ldp + 4 tn + wn] (the four lanes of a row in a
+// wave combine by shuffles; the combine kernel folds a row's pairs in this order). The lane
+// holding the sampled column stores its logit in zy[row].
+template <bool FULL>
+__device__ __forceinline__ void lse_tile(const GemmArgs& g, const f32x4 (&acc)[kTm][kTn],
+                                         int64_t m0, int64_t n0, int64_t tn,
+                                         const int (&ep_y)[kGemmTile]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / (kGemmTile / kGemmWaveN), wn = wave % (kGemmTile / kGemmWaveN);
+  const int fr = lane & 15, fq = lane >> 4;
+  const int N = (int)g.N;                                   // V <= 2^22
+  const int nb = (int)n0 + wn * kGemmWaveN + 4 * fq;         // this lane's first column
+  const int64_t pidx = tn * (kGemmTile / kGemmWaveN) + wn;
+#pragma unroll
+  for (int i = 0; i < kTm; ++i) {
+    const int64_t m = m0 + wm * kGemmWaveM + i * 16 + fr;
+    const bool row_ok = m < g.M;
+    const int y = ep_y[wm * kGemmWaveM + i * 16 + fr];
+    float mx = kMinRef;
+#pragma unroll
+    for (int j = 0; j < kTn; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (FULL || nb + j * 16 + e < N) mx = fmaxf(mx, acc[i][j][e]);
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mb = mx * kLog2e;
+    float sm = 0.f;
+#pragma unroll
+    for (int j = 0; j < kTn; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int n = nb + j * 16 + e;
+        const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][e], kLog2e, -mb));
+        sm += ((FULL || n < N) && n != y) ? x : 0.f;
+      }
+    sm += __shfl_xor(sm, 16, 64);
+    sm += __shfl_xor(sm, 32, 64);
+    const int dy = y - nb;  // the sampled column in this lane's 4 x 4 columns?
+    if (row_ok && dy >= 0 && dy < kTn * 16 && (dy & 15) < 4) {
+#pragma unroll
+      for (int j = 0; j < kTn; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (dy == j * 16 + e) g.e.zy[m] = acc[i][j][e];
+    }
+    if (row_ok && fq == 0) g.e.part[m * g.e.ldp + pidx] = float2{mx, sm};
+  }
+}
+
+// Row-loss epilogue kEpiGrad: g = -coef exp(z - lse), evaluated as +-exp2(z log2(e) - b2),
+// and coef (1 - p) at the sampled column, rounded to bf16 (nearest even) into G.
+__device__ __forceinline__ void grad_tile(const GemmArgs& g, const f32x4 (&acc)[kTm][kTn],
+                                          int64_t m0, int64_t n0) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / (kGemmTile / kGemmWaveN), wn = wave % (kGemmTile / kGemmWaveN);
+  const int fr = lane & 15, fq = lane >> 4;
+  GradParams ps[kTm];  // every row's parameters requested before the first is used
+#pragma unroll
+  for (int i = 0; i < kTm; ++i) {
+    const int64_t m = m0 + wm * kGemmWaveM + i * 16 + fr;
+    ps[i] = m < g.M ? g.e.gp[m] : GradParams{INFINITY, 0, 0.f, -1};
+  }
+#pragma unroll
+  for (int i = 0; i < kTm; ++i) {
+    const int64_t m = m0 + wm * kGemmWaveM + i * 16 + fr;
+    if (m >= g.M) continue;
+    const GradParams p = ps[i];
+    __bf16* grow = g.e.G + m * g.e.ldg;
+#pragma unroll
+    for (int j = 0; j < kTn; ++j) {
+      const int64_t n = n0 + wn * kGemmWaveN + j * 16 + 4 * fq;
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][e], kLog2e, -p.b2));
+        v[e] = p.y < 0 ? 0.f : ((n + e == p.y) ? p.gy : (p.neg ? -x : x));
+      }
+      const bf16x4 o = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+      if (n + 3 < g.N) {
+        *(bf16x4*)(grow + n) = o;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (n + e < g.N) grow[n + e] = o[e];
+      }
+    }
+  }
+}
+
 // The (tm, tn) tile of C over split `split` of the contraction, by the whole workgroup. The
 // caller puts a barrier between two tiles of one workgroup (the last slab's reads must end
 // before the next tile refills LDS; with an empty K range there is no barrier inside).
-template <bool BETA>
+// The sampled ids of the tile's rows for kEpiLse, loaded into LDS before the contraction (the
+// K loop's barriers make them visible; reading them in the epilogue would put a load latency
+// after every tile).
+struct EpiRows {
+  int y[kGemmTile];            // sampled id, or -1 when outside [0, N)
+};
+
+template <bool BETA, int EPI = kEpiStore>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t tn,
-                                          int64_t split, __bf16 (&lds)[2 * kSlab]) {
+                                          int64_t split, __bf16 (&lds)[2 * kSlab], EpiRows& er) {
   constexpr int BM = kGemmTile, BN = kGemmTile, BK = kGemmBK;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / (BN / kGemmWaveN), wn = wave % (BN / kGemmWaveN);
@@ -258,11 +360,18 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t
 #pragma unroll
     for (int j = 0; j < kTn; ++j) acc[i][j] = f32x4{};
 
+  // the epilogue's per-row inputs: requested now, stored to LDS once the first slab has landed
+  const int64_t mrow = m0 + tid;
+  const bool erow = EPI != kEpiStore && tid < kGemmTile && mrow < g.M;
+  int64_t ey = -1;
+  if (EPI == kEpiLse && erow) ey = g.e.ids[mrow];
   // a fragment row is a multiple of 16 plus lane % 16, so its swizzle is lane & 7
   const int fr = lane & 15, fq = lane >> 4, sw = lane & 7;
   if (nk > 0) issue(0);
   for (int64_t kt = 0; kt < nk; ++kt) {
     wait_vmcnt<0>();  // this wave's part of slab kt is in LDS
+    if (EPI == kEpiLse && kt == 0 && tid < kGemmTile)
+      er.y[tid] = (ey >= 0 && ey < g.N) ? (int)ey : -1;
     lds_barrier();    // every wave's is, and every wave is done with slab kt - 1's buffer
     if (kt + 1 < nk) issue(kt + 1);
     const __bf16* st = lds + (int)(kt & 1) * kSlab;
@@ -272,13 +381,23 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t
               [&](int j, int s) { return lb + j * 16 * BK + ((4 * s + fq) ^ sw) * 8; });
   }
 
-  store_tile<BETA>(g, acc, m0, n0, split);
+  if (EPI == kEpiLse) {
+    if (n0 + kGemmTile <= g.N)
+      lse_tile<true>(g, acc, m0, n0, tn, er.y);
+    else
+      lse_tile<false>(g, acc, m0, n0, tn, er.y);
+  } else if (EPI == kEpiGrad) {
+    grad_tile(g, acc, m0, n0);
+  }
+  else
+    store_tile<BETA>(g, acc, m0, n0, split);
 }
 
-template <bool BETA, bool QUEUED>
+template <bool BETA, bool QUEUED, int EPI = kEpiStore>
 __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(const GemmArgs g) {
   __shared__ __attribute__((aligned(16))) __bf16 lds[2 * kSlab];
   __shared__ int64_t unit;
+  __shared__ EpiRows er;
   const int home = (int)(blockIdx.x % kGemmQueues);
   int tried = 0;
   // one unit per workgroup, or (queued) units until every queue is empty: all threads read the
@@ -295,7 +414,7 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(const GemmArgs g) {
     if (u < 0) break;
     int64_t tm, tn, split;
     unit_tile<kGemmTile, kGemmTile>(g, u, tm, tn, split);
-    gemm_tile<BETA>(g, tm, tn, split, lds);
+    gemm_tile<BETA, EPI>(g, tm, tn, split, lds, er);
     if (!QUEUED) break;
   }
 }
@@ -401,6 +520,32 @@ hipError_t launch_tiles(GemmArgs g, bool beta, int splits, int num_cu, hipStream
 __global__ __launch_bounds__(kGemmQueues) void zero_queue_kernel(int* q) { q[threadIdx.x] = 0; }
 
 }  // namespace
+
+hipError_t launch_gemm_epi(GemmArgs g, int* queue, int num_cu, hipStream_t stream) {
+  if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  g.m_fastest = g.M <= g.N;
+  g.k_split = g.K > 0 ? g.K : 1;
+  g.c_split_stride = 0;
+  g.c_vec = false;
+  const int64_t mt = (g.M + kGemmTile - 1) / kGemmTile, nt = (g.N + kGemmTile - 1) / kGemmTile;
+  g.units = mt * nt;
+  g.queue = g.units > num_cu ? queue : nullptr;
+  if (g.queue) {
+    void* zargs[] = {&g.queue};
+    if (hipError_t e = hipLaunchKernel((const void*)&zero_queue_kernel, dim3(1),
+                                       dim3(kGemmQueues), zargs, 0, stream))
+      return e;
+  }
+  const int64_t grid = g.queue ? num_cu : g.units;
+  const void* fn =
+      g.epi == kEpiLse
+          ? (g.queue ? (const void*)&gemm_bf16_kernel<false, true, kEpiLse>
+                     : (const void*)&gemm_bf16_kernel<false, false, kEpiLse>)
+          : (g.queue ? (const void*)&gemm_bf16_kernel<false, true, kEpiGrad>
+                     : (const void*)&gemm_bf16_kernel<false, false, kEpiGrad>);
+  void* args[] = {&g};
+  return hipLaunchKernel(fn, dim3((unsigned)grid), dim3(kThreads), args, 0, stream);
+}
 
 int64_t gemm_splitk_count(int64_t M, int64_t N, int64_t K, int num_cu) {
   const int64_t tiles = ((M + kGemmTile - 1) / kGemmTile) * ((N + kGemmTile - 1) / kGemmTile);

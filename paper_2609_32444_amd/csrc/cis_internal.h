@@ -25,6 +25,18 @@ namespace cis {
 constexpr size_t kStatsBytes = 256;
 // Segments per row at most in the split forward pass (the partials per row in the workspace).
 constexpr int kSegMax = 32;
+
+// Per-row gradient parameters of the fused LM-head pass (written by the row combine, read by
+// the logits product's gradient epilogue): g_j = s exp2(z_j log2(e) - b2) with s = -1 when neg
+// (coef > 0), else +1; the sampled column y gets gy; y = -1 for a row without gradient
+// (b2 = +inf, gy = 0).
+struct GradParams {
+  float b2;
+  int32_t neg;
+  float gy;
+  int32_t y;
+};
+
 constexpr size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 struct WsLayout {
   size_t terms, logk, excess, wpre, flags, pflags, logK, part, zy, total;
@@ -50,7 +62,10 @@ constexpr size_t ws_bytes(int64_t T) { return ws_layout(T, 0).total; }
 
 // LM-head workspace: the loss workspace above, then (256-byte aligned)
 //   Q   int[kGemmQueues]   the products' work queues (256 bytes)
-//   Z   float[rows, ldz]   the chunk's logits
+//   Z   float[rows, ldz]   the chunk's logits (materialising path only), or, on the fused path
+//                          that never stores them, per row and 64-column block the pair
+//                          (max, exp-sum) (float2[rows, ntv]), the sampled logit (float[rows])
+//                          and the gradient parameters (GradParams[rows])
 //   Wt  bf16[H, ldv]       W^T (backward)
 //   Gt  bf16[V, ldc]       (dL/dz)^T of the rows of a dL/dW group (backward)
 //   Ht  bf16[H, ldc]       their hidden states transposed (backward)
@@ -75,21 +90,36 @@ inline int64_t lm_dw_rows(int64_t chunk) {
 }
 struct LmLayout {
   WsLayout loss;
-  int64_t ldz, ldv, ldc;
+  int64_t ldz, ldv, ldc, ntv;
   size_t z, wt, gt, ht, gb, part, queue, total;
+  size_t tpart, tzy, tgp;  // fused path: tile pairs, sampled logits, gradient parameters
+  bool fused;
 };
 inline LmLayout lm_layout(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_t n_seq,
-                          bool bwd) {
+                          bool bwd, bool fused) {
   LmLayout M;
+  M.fused = fused;
   M.loss = ws_layout(T, n_seq);
   const int64_t rows = T < chunk ? T : chunk;
   M.ldz = (V + 7) / 8 * 8;
   M.ldv = M.ldz;
+  M.ntv = (V + 255) / 256 * 4;  // four 64-column blocks per 256-column tile
   const int64_t grows = T < lm_dw_rows(chunk) ? T : lm_dw_rows(chunk);
   M.ldc = ((grows > 0 ? grows : 1) + 7) / 8 * 8;
   M.queue = align_up(M.loss.total, 256);  // the products' work queues
   M.z = M.queue + 256;
-  size_t end = M.z + align_up((size_t)rows * (size_t)M.ldz * 4, 256);
+  size_t end = M.z;
+  if (fused) {
+    M.tpart = end;
+    end += align_up((size_t)rows * (size_t)M.ntv * 8, 256);
+    M.tzy = end;
+    end += align_up((size_t)rows * 4, 256);
+    M.tgp = end;
+    end += align_up((size_t)rows * sizeof(GradParams), 256);
+  } else {
+    M.tpart = M.tzy = M.tgp = end;
+    end += align_up((size_t)rows * (size_t)M.ldz * 4, 256);
+  }
   M.wt = M.gt = M.ht = M.gb = M.part = end;
   if (bwd) {
     end += align_up((size_t)H * (size_t)M.ldv * 2, 256);
@@ -146,12 +176,15 @@ struct RowArgs {
   float clip_low, clip_high;
 };
 
-// Split forward pass (cis_seg_kernel, cis_combine_kernel).
+// Rows whose (max, exp-sum) comes in pieces: the split forward pass (cis_seg_kernel) and the
+// fused LM-head pass (the logits product's epilogue), folded by cis_combine_kernel.
 struct SegArgs {
-  float2* part;    // [T * kSegMax] (max, exp-sum without the sampled logit) per segment
-  float* zy;       // [T] the sampled logit
-  int32_t nseg;    // segments per row (<= kSegMax)
-  int32_t segvec;  // 16-byte vectors per segment (kSegBlock * K)
+  float2* part;     // [T * stride] (max, exp-sum without the sampled logit) per piece
+  float* zy;        // [T] the sampled logit
+  int32_t nseg;     // pieces per row (<= stride)
+  int32_t segvec;   // 16-byte vectors per segment (split forward pass)
+  int64_t stride;   // pieces per row in `part`
+  GradParams* gp;   // [T] nullable: gradient parameters for the fused LM-head pass
 };
 constexpr int kCombineBlock = 256;
 // A compiled segment kernel: `block` threads with K 16-byte vectors each, so block * K vectors

@@ -83,7 +83,7 @@ __global__ __launch_bounds__(BLOCK) void cis_seg_kernel(const RowArgs a, const S
     wave_lse_reduce(m, s);
     if (y_mine) g.zy[row] = zy_mine;
     if (NW == 1) {
-      if (tid == 0) g.part[row * kSegMax + seg] = float2{m, s};
+      if (tid == 0) g.part[row * g.stride + seg] = float2{m, s};
       continue;
     }
     const int wid = tid >> 6;
@@ -96,7 +96,7 @@ __global__ __launch_bounds__(BLOCK) void cis_seg_kernel(const RowArgs a, const S
       float M = sh_m[0], S = sh_s[0];
 #pragma unroll
       for (int w = 1; w < NW; ++w) lse_combine(M, S, sh_m[w], sh_s[w]);
-      g.part[row * kSegMax + seg] = float2{M, S};
+      g.part[row * g.stride + seg] = float2{M, S};
     }
     __syncthreads();  // sh_m / sh_s are reused by the next segment of this workgroup
   }
@@ -111,17 +111,26 @@ __global__ __launch_bounds__(kCombineBlock) void cis_combine_kernel(const RowArg
   if (row >= a.T) return;  // whole waves leave together; no barrier follows
   const RowScalars rsc = fetch_row_scalars<EXT>(a, row);
   if (!rsc.valid(a.V)) {
-    if (lane == 0) row_invalid<EXT>(a, rsc, row);
+    if (lane == 0) {
+      row_invalid<EXT>(a, rsc, row);
+      if (g.gp) g.gp[row] = GradParams{INFINITY, 0, 0.f, -1};
+    }
     return;
   }
   float m = kMinRef, s = 0.f;
   for (int k = lane; k < g.nseg; k += 64) {
-    const float2 p = g.part[row * kSegMax + k];
+    const float2 p = g.part[row * g.stride + k];
     lse_combine(m, s, p.x, p.y);
   }
   wave_lse_reduce(m, s);
   const float zy = g.zy[row];
-  row_epilogue<EXT>(a, rsc, row, m, s, zy, lane == 0);
+  const RowResult rr = row_epilogue<EXT>(a, rsc, row, m, s, zy, lane == 0);
+  if (g.gp && lane == 0) {
+    // the row kernel's gradient: -coef exp(z - lse) = s exp2(z log2(e) - b2), coef (1 - p) at y
+    const float coef = rr.coef;
+    const float b2 = coef != 0.f ? (rr.lse - logf(fabsf(coef))) * kLog2e : INFINITY;
+    g.gp[row] = GradParams{b2, coef > 0.f ? 1 : 0, coef * rr.one_m_p, (int32_t)rsc.y};
+  }
 }
 
 }  // namespace cis

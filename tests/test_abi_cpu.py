@@ -203,10 +203,13 @@ def test_lmhead_workspace_bytes():
     T, V, H = 16384, 151936, 2048
     fwd, bwd = f(T, V, H, 4096, 0, False), f(T, V, H, 4096, 0, True)
     loss = 256 + 18 * T
-    # the loss rows' scratch plus one float32 chunk of logits; the backward adds W^T and the
-    # two transposed chunk operands
-    assert fwd >= loss + 4 * 4096 * V and fwd % 256 == 0
-    assert bwd >= fwd + 2 * V * H + 2 * (V + H) * 4096
+    # the loss rows' scratch plus, per chunk row, one (max, exp-sum) pair per 256 columns, the
+    # sampled logit and the gradient parameters: the logits themselves are never stored
+    ntv = (V + 255) // 256 * 4
+    assert fwd >= loss + 4096 * (8 * ntv + 4 + 16) and fwd % 256 == 0
+    assert fwd < 4096 * V                       # far less than one float32 chunk of logits
+    # the backward adds W^T, the chunk's bf16 gradient and the two transposed operands
+    assert bwd >= fwd + 2 * V * H + 2 * 4096 * V + 2 * (V + H) * 4096
     # a chunk larger than the batch only needs the batch's rows
     assert f(100, 1000, 64, 4096, 0, True) == f(100, 1000, 64, 100, 0, True)
     assert f(T, V, H, 4096, 10, True) >= bwd
@@ -214,6 +217,11 @@ def test_lmhead_workspace_bytes():
                 (T, V, 1 << 17, 1), (T, V, H, 1 << 17)):
         assert f(*bad, 0, True) == 0, bad
     assert f(T, V, H, 64, -1, True) == 0
+    # the backward that never stores the logits needs the forward's pairs, not a chunk of logits
+    rec = cis.lmhead_workspace_bytes(T, V, H, 4096, 0, True, recompute=True)
+    assert rec < bwd - 4 * 4096 * V + 4096 * (8 * ntv + 20) + 256 * 4
+    assert rec >= fwd + 2 * V * H + 2 * 4096 * V
+    assert cis.load_library().cis_lmhead_workspace_bytes(T, V, H, 4096, 0, 3) == 0
 
 
 # distinct fake buffers for the LM-head calls, 4 GiB apart (never dereferenced)
@@ -223,7 +231,7 @@ LM_H, LM_W, LM_DH, LM_DW, LM_WS = (k << 32 for k in range(1, 6))
 def _lm(bwd=True, **kw):
     a = dict(hidden=LM_H, T=4, H=64, ld_h=64, weight=LM_W, V=1000, ld_w=64, ids=FAKE, linf=FAKE,
              lold=NULL, adv=FAKE, mask=NULL, offs=NULL, nseq=0, prm=_prm(), chunk=4096,
-             dh=LM_DH, ld_dh=64, dw=LM_DW, ld_dw=64, ws=LM_WS, wsb=1 << 30)
+             dh=LM_DH, ld_dh=64, dw=LM_DW, ld_dw=64, ws=LM_WS, wsb=1 << 30, recompute=0)
     a.update(kw)
     pp = ctypes.byref(a["prm"]) if a["prm"] is not None else None
     lib = cis.load_library()
@@ -231,7 +239,8 @@ def _lm(bwd=True, **kw):
             a["linf"], a["lold"], a["adv"], a["mask"], a["offs"], a["nseq"], pp, a["chunk"])
     tail = (NULL, NULL, NULL, NULL, NULL, NULL, a["ws"], a["wsb"], NULL)
     if bwd:
-        return lib.cis_lmhead_loss_bwd(*head, a["dh"], a["ld_dh"], a["dw"], a["ld_dw"], 0, *tail)
+        return lib.cis_lmhead_loss_bwd(*head, a["dh"], a["ld_dh"], a["dw"], a["ld_dw"], 0,
+                                       a["recompute"], *tail)
     return lib.cis_lmhead_loss_fwd(*head, *tail)
 
 
@@ -244,6 +253,7 @@ def _lm(bwd=True, **kw):
     (dict(V=(1 << 22) + 1), -2), (dict(ld_h=(1 << 22) + 8), -2), (dict(ld_w=(1 << 22) + 8), -2),
     (dict(ld_h=68, H=60), -5), (dict(ld_w=68, H=60), -5), (dict(hidden=LM_H + 8), -5),
     (dict(weight=LM_W + 8), -5), (dict(ws=LM_WS + 16), -5), (dict(wsb=1000), -7),
+    (dict(recompute=2), -4), (dict(recompute=-1), -4),
     (dict(prm=None), -1), (dict(lold=FAKE, prm=None), -1),
 ])
 def test_lmhead_argument_errors(kw, code):

@@ -81,14 +81,19 @@ def ref_dict(res):
             "rho": res.rho, "gate": res.gate}
 
 
-def run_case(name, b, op=X.OP_CIS, kw=None, chunk=4096, decoupled=False, seq=False, bwd=True):
+def run_case(name, b, op=X.OP_CIS, kw=None, chunk=4096, decoupled=False, seq=False, bwd=True,
+             recompute=False):
     kw = dict(lam=b.lam, kappa=b.kappa) if kw is None and op == X.OP_CIS else (kw or {})
     prm_dev, prm_ref = make_params(op, kw, b.scale)
     lold = b.logp_old if decoupled else None
     offs = b.offsets if seq else None
-    fn = cis.lmhead_loss_bwd if bwd else cis.lmhead_loss_fwd
-    out = fn(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask, params=prm_dev,
-             logp_old=lold, seq_offsets=offs, chunk=chunk)
+    if bwd:
+        out = cis.lmhead_loss_bwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
+                                  params=prm_dev, logp_old=lold, seq_offsets=offs, chunk=chunk,
+                                  recompute=recompute)
+    else:
+        out = cis.lmhead_loss_fwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
+                                  params=prm_dev, logp_old=lold, seq_offsets=offs, chunk=chunk)
     torch.cuda.synchronize()
     h, W = host(b)
     res = L.lmhead_cis_loss(h, W, b.ids.cpu().numpy(), b.logp_infer.cpu().double().numpy(),
@@ -134,10 +139,13 @@ SMALL = [
 ]
 
 
+@pytest.mark.parametrize("recompute", [False, True], ids=["chunked_logits", "recompute"])
 @pytest.mark.parametrize("name,T,V,H,chunk,gen", SMALL, ids=[c[0] for c in SMALL])
-def test_lmhead_parity_small(name, T, V, H, chunk, gen):
+def test_lmhead_parity_small(name, T, V, H, chunk, gen, recompute):
+    """Both backward modes: each chunk's float32 logits kept while G is formed, and the product
+    formed again with an epilogue that writes G (the logits never stored)."""
     b = make_lmhead_batch(T, V, H, device=DEV, seed=11, min_len=16, max_len=96, **gen)
-    run_case(name, b, chunk=chunk)
+    run_case(name, b, chunk=chunk, recompute=recompute)
 
 
 # ------------------------------------------------------------------------------------------
@@ -157,8 +165,9 @@ GENERAL = [
 ]
 
 
+@pytest.mark.parametrize("recompute", [False, True], ids=["chunked_logits", "recompute"])
 @pytest.mark.parametrize("name,T,V,H,chunk", GENERAL, ids=[g[0] for g in GENERAL])
-def test_lmhead_general_bf16_inputs(name, T, V, H, chunk):
+def test_lmhead_general_bf16_inputs(name, T, V, H, chunk, recompute):
     """Hidden states N(0, 1) and head weights N(0, 4/(H-1)) rounded once to bf16, so the
     float32 logits h W^T carry their own dot-product rounding. The bounds follow from it:
 
@@ -177,7 +186,7 @@ def test_lmhead_general_bf16_inputs(name, T, V, H, chunk):
     b = make_lmhead_batch(T, V, H, device=DEV, seed=23, min_len=16, max_len=96, exact=False)
     prm_dev, prm_ref = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
     out = cis.lmhead_loss_bwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
-                              params=prm_dev, chunk=chunk)
+                              params=prm_dev, chunk=chunk, recompute=recompute)
     torch.cuda.synchronize()
     h, W = host(b)
     ids = b.ids.cpu().numpy()
@@ -229,7 +238,7 @@ def test_lmhead_general_bf16_inputs(name, T, V, H, chunk):
     rep["dhidden"] = check_grad("dhidden", dh, res.dhidden,
                                 ch[:, None] * (G @ np.abs(W)) + 1e-30)
     rep["dweight"] = check_grad("dweight", dW, res.dW, (cw[:, None] * G).T @ np.abs(h) + 1e-30)
-    _dump(f"general_{name}", rep)
+    _dump(f"general_{name}_{'recompute' if recompute else 'chunked'}", rep)
     print(rep, flush=True)
 
 
@@ -248,12 +257,14 @@ def test_lmhead_products_with_more_tiles_than_cus():
         assert torch.equal(out[k], again[k]), k
 
 
-def test_lmhead_largest_vocabulary():
+@pytest.mark.parametrize("recompute", [False, True], ids=["chunked_logits", "recompute"])
+def test_lmhead_largest_vocabulary(recompute):
     """V = 2^22, the largest vocabulary the LM-head calls accept: float32 logit rows of 16 MB
-    through the streamed row path, a logits product of 16384 tiles, dL/dh split along V into
-    2^19-long contractions and dL/dW over all 2^22 rows, every output against the oracle."""
+    through the streamed row path (or 65536 pairs per row folded by the combine), a logits
+    product of 16384 tiles, dL/dh split along V into 2^19-long contractions and dL/dW over all
+    2^22 rows, every output against the oracle."""
     b = make_lmhead_batch(64, 1 << 22, 64, device=DEV, seed=17, min_len=16, max_len=32)
-    run_case("max_vocab", b, chunk=64)
+    run_case("max_vocab", b, chunk=64, recompute=recompute)
 
 
 def test_lmhead_largest_chunk():
@@ -317,10 +328,11 @@ def test_lmhead_operators(name, op, kw):
     ("ppo_icepop", X.OP_ICEPOP, dict(lo=0.5, hi=5.0), False),
     ("ppo_seq_tis", X.OP_SEQ_TIS, dict(hi=2.0), True),
 ])
-def test_lmhead_decoupled(name, op, kw, seq):
+@pytest.mark.parametrize("recompute", [False, True], ids=["chunked_logits", "recompute"])
+def test_lmhead_decoupled(name, op, kw, seq, recompute):
     b = make_lmhead_batch(300, 2001, 64, device=DEV, seed=31, min_len=16, max_len=80,
                           delta_sd=0.3, old_sd=0.2)
-    run_case(name, b, op=op, kw=kw, chunk=128, decoupled=True, seq=seq)
+    run_case(name, b, op=op, kw=kw, chunk=128, decoupled=True, seq=seq, recompute=recompute)
 
 
 def test_lmhead_forward_only_parity():
@@ -379,15 +391,17 @@ def test_lmhead_empty_batch_zero_dweight_from_work_queues():
 FULL_T, FULL_V, FULL_H, FULL_CHUNK = 16384, 151936, 2048, cis.LMHEAD_CHUNK
 
 
-def test_lmhead_full_size_sampled():
-    """T = 16384, V = 151936, H = 2048 in chunks of 4096 rows: sampled rows against the oracle
+@pytest.mark.parametrize("recompute", [False, True], ids=["chunked_logits", "recompute"])
+def test_lmhead_full_size_sampled(recompute):
+    """T = 16384, V = 151936, H = 2048 in chunks of 4096 rows, both backward modes: sampled rows
+    against the oracle
     (per-row outputs and dL/dh rows), and for dL/dW the properties that hold at any size:
     <dW, W> = sum_t <dh_t, h_t> (both are sum_t <G_t, z_t> for the same bf16 G), and each
     column of dW sums to sum_t (sum_v G_tv) h_t with sum_v G_tv = 0 up to G's bf16 rounding."""
     b = make_lmhead_batch(FULL_T, FULL_V, FULL_H, device=DEV, seed=2, c=1.0)
     prm_dev, prm_ref = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
     out = cis.lmhead_loss_bwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
-                              params=prm_dev, chunk=FULL_CHUNK)
+                              params=prm_dev, chunk=FULL_CHUNK, recompute=recompute)
     torch.cuda.synchronize()
     stats = cis.read_stats(out["workspace"])
     assert stats["n_valid"] == FULL_T and stats["n_bad_id"] == 0 and stats["n_nonfinite"] == 0
@@ -425,7 +439,7 @@ def test_lmhead_full_size_sampled():
     assert torch.all(col.abs() <= cbound)
     rep.update(trace_lhs=lhs, trace_rhs=rhs, trace_bound=bound,
                colsum_max_over_bound=float((col.abs() / cbound).max()))
-    _dump("full_size", rep)
+    _dump(f"full_size_{'recompute' if recompute else 'chunked'}", rep)
 
 
 def test_lmhead_full_size_few_valid_rows_dweight():
