@@ -118,9 +118,9 @@ def test_config4_wide_vocab_fwd_and_bwd():
     out_b = _run(b, bwd=True)
     rep = _check_full("cfg4_bwd", b, out_b, grad_rows=grows, z=z, ref=ref)
     assert rep["grad_rows"] >= 1024
-    # Both passes also agree with each other to float32 rounding. (Not bit for bit: on rows
-    # this long the fused pass keeps part of the row in LDS, the forward pass streams it, so
-    # the exp-sum is accumulated in a different order.)
+    # Both passes also agree with each other to float32 rounding. (Not bit for bit: the fused
+    # pass sums a row in one workgroup, the forward pass in 16 KiB segments that are combined
+    # afterwards, so the exp-sum is accumulated in a different order.)
     for k in ("logp_train", "w", "terms"):
         f, g = out_f[k].double(), out_b[k].double()
         assert torch.all((f - g).abs() <= 1e-5 * f.abs() + 1e-7), k
