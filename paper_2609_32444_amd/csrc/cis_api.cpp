@@ -252,6 +252,7 @@ cis::RowArgs row_args(const LossCall& c, const Ws& ws, const void* logits, void*
   ra.eps_out = at(c.eps_out, t0);
   ra.clip_low = c.prm.clip_low;
   ra.clip_high = c.prm.clip_high;
+  ra.queue = reinterpret_cast<unsigned long long*>(ws.base + cis::kQueueOff);
   return ra;
 }
 
@@ -299,6 +300,12 @@ int launch_rows(const LossCall& c, const Ws& ws, const void* logits, void* dlogi
   const int per_cu = blocks_per_cu(var.fn, var.block, dev);
   const int64_t resident = (int64_t)per_cu * info.num_cu;
   const int grid = (int)(rows < resident ? rows : resident);
+  if (c.bwd) {  // the fused pass takes its rows from a queue (see cis_row_kernel)
+    void* qargs[] = {&ra.queue};
+    if (hipLaunchKernel(cis::queue_reset_kernel(), dim3(1), dim3(64), qargs, 0, stream) !=
+        hipSuccess)
+      return CIS_ERR_LAUNCH;
+  }
   return launch(var.fn, grid, var.block, &ra, stream);
 }
 

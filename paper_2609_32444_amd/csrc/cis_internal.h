@@ -23,6 +23,9 @@ namespace cis {
 // The last two exist only in the layout of the forward entry points (`seg`); the fused pass and
 // the LM-head path do not use them.
 constexpr size_t kStatsBytes = 256;
+// The row queue counter (8 bytes) sits in the stats block, after the cis_stats_t.
+constexpr size_t kQueueOff = 128;
+static_assert(sizeof(cis_stats_t) <= kQueueOff, "the row queue counter follows the statistics");
 // Segments per row at most in the split forward pass (the partials per row in the workspace).
 constexpr int kSegMax = 32;
 
@@ -174,6 +177,10 @@ struct RowArgs {
   const uint8_t* pflags_ws; // pre-pass acted bits[T]
   float* eps_out;           // nullable; rate-1 path only (the pre-pass writes it otherwise)
   float clip_low, clip_high;
+  // row queue of the row kernel: a workgroup's first two rows are blockIdx.x and
+  // blockIdx.x + gridDim.x, later ones 2*gridDim.x + the counter's old value. Cleared by
+  // queue_reset_kernel before every launch.
+  unsigned long long* queue;
 };
 
 // Rows whose (max, exp-sum) comes in pieces: the split forward pass (cis_seg_kernel) and the
@@ -272,6 +279,7 @@ const RowVariant& select_row_variant_ext(int dtype, bool bwd, int32_t nvec,
                                          bool bf16_grad = false);
 
 const void* finalize_kernel();
+const void* queue_reset_kernel();
 const void* weights_kernel();
 const void* seq_sum_kernel();
 const void* prepass_kernel();

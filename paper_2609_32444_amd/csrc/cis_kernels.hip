@@ -151,7 +151,14 @@ const void* combine_kernel(bool ext) {
   return ext ? combine_kernel_ext() : (const void*)&cis_combine_kernel<false>;
 }
 
+// Clears the row kernel's queue counter ahead of each launch: a kernel rather than a memset, so
+// a captured call holds no memset node.
+__global__ __launch_bounds__(64) void cis_queue_reset_kernel(unsigned long long* q) {
+  if (threadIdx.x == 0) *q = 0ull;
+}
+
 const void* finalize_kernel() { return (const void*)&cis_finalize_kernel; }
+const void* queue_reset_kernel() { return (const void*)&cis_queue_reset_kernel; }
 const void* weights_kernel() { return (const void*)&cis_weights_kernel; }
 
 }  // namespace cis

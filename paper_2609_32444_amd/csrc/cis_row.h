@@ -648,6 +648,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
   __shared__ float sh_m[2][NW];
   __shared__ float sh_s[2][NW];
   __shared__ float sh_zy[2];
+  __shared__ unsigned long long sh_q[2];
   // slot NV+k of thread tid at lds_row[k*BLOCK + tid]; each wave fills and reads its own part
   __shared__ u32x4 lds_row[NL > 0 ? NL * BLOCK : 1];
 
@@ -707,7 +708,15 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
   }
 
   RowScalars cur = fetch_row_scalars<EXT>(a, blockIdx.x);
-  for (int64_t row = blockIdx.x; row < a.T; row += gridDim.x) {
+  // The fused pass takes rows from a queue, so that workgroups that meet cheap rows (masked
+  // ones) or run on a faster part of the chip take more of them: the first two rows of a
+  // workgroup are fixed, every later one is drawn one row ahead of its use (the next row is
+  // needed at the top of a row, for its scalars and, with PF, its loads). The forward pass
+  // keeps the fixed stride: its long rows go to the split kernels, whose short-lived
+  // workgroups balance by themselves.
+  constexpr bool kQueue = BWD;
+  int64_t nrow = (int64_t)blockIdx.x + gridDim.x;
+  for (int64_t row = blockIdx.x; row < a.T;) {
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
     const int wid = __builtin_amdgcn_readfirstlane(tid) >> 6;
@@ -715,8 +724,10 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     uint32_t voff = (uint32_t)tid * 16u;
 
     const RowScalars rsc = cur;
-    const int64_t nrow = row + gridDim.x;
     cur = fetch_row_scalars<EXT>(a, nrow);  // the next row's, for the next iteration
+    // the row after the next one: thread 0 draws it now and publishes it at the reduction
+    unsigned long long tk = 0ull;
+    if (kQueue && tid == 0) tk = atomicAdd(a.queue, 1ull);
     const bool valid = rsc.valid(V);
     const int y = valid ? (int)rsc.y : 0;
     const int vy = y / EPV, ey = y % EPV;
@@ -828,6 +839,22 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 
     // ---- block reduction and epilogue: l_train, 1 - p, weight (Algorithm 1), loss term -----
     float coef = 0.f, b2 = INFINITY, one_m_p = 0.f;
+    // (one barrier per row, valid or not, so that the double-buffered shared values of row n
+    // are read before row n + 2 writes them)
+    if (kQueue && NW > 1 && tid == 0) sh_q[buf] = tk;
+    auto drawn = [&]() -> int64_t {
+      if (!kQueue) return nrow + gridDim.x;
+      unsigned long long q;
+      if (NW > 1) {
+        q = sh_q[buf];
+      } else {
+        const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)tk);
+        const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(tk >> 32));
+        q = ((unsigned long long)hi << 32) | lo;
+      }
+      return (int64_t)q + 2 * (int64_t)gridDim.x;
+    };
+    int64_t nn;
     if (valid) {
       wave_lse_reduce(m, s);
       if ((tid & 63) == 0) {
@@ -840,6 +867,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 #pragma unroll
       for (int w = 1; w < NW; ++w) lse_combine(M, sr, sh_m[buf][w], sh_s[buf][w]);
       const float zy = sh_zy[buf];
+      nn = drawn();
       buf ^= 1;
       // M: max over the row (sampled element included); sr: sum_{j != y} exp(z_j - M).
       const RowResult rr = row_epilogue<EXT>(a, rsc, row, M, sr, zy, tid == 0);
@@ -849,8 +877,11 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
       // and b2 = (lse - ln|coef|) * log2e; coef = 0 keeps b2 = +inf, which gives an all-zero
       // row. The float32 offset is accurate to a few 1e-6 relative, far inside bf16 rounding.
       if (BWD && coef != 0.f) b2 = (rr.lse - logf(fabsf(coef))) * kLog2e;
-    } else if (tid == 0) {
-      row_invalid<EXT>(a, rsc, row);
+    } else {
+      if (kQueue && NW > 1) __syncthreads();
+      nn = drawn();
+      buf ^= 1;
+      if (tid == 0) row_invalid<EXT>(a, rsc, row);
     }
 
     // ---- sweep 2: gradient ----------------------------------------------------------------
@@ -905,6 +936,8 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
       }
       if (valid && y_mine) EO::store_elem(grow, y, EO::bits_of(coef * one_m_p));
     }
+    row = nrow;
+    nrow = nn;
   }
 }
 

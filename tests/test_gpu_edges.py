@@ -71,6 +71,27 @@ def test_long_rows_many_per_workgroup(V, dtype):
     run_and_check(b)
 
 
+# Fused-pass rows come from a queue once every workgroup has had two rows. The row counts put
+# thousands of rows in the queue for the one-wave, 256-thread, 1024-thread and LDS variants
+# (resident grids of up to 7168, 1024, 256 and 256 workgroups).
+@pytest.mark.parametrize("V,T", [(1000, 20000), (32768, 4096), (151936, 1500), (250001, 700)])
+def test_row_queue_and_stale_workspace(V, T):
+    """The workspace starts as all 0xFF bytes: as the row queue's counter that would hand out
+    no queued row at all, so the call must clear it itself. Every row (15% masked) against the
+    oracle, then a second call on the same workspace gives identical bits."""
+    b = make_random_batch(T, V, torch.bfloat16, DEV, seed=V + 11, ld=((V + 7) // 8) * 8,
+                          mask_p=0.85)
+    ws = torch.full((cis.workspace_bytes(T),), 255, dtype=torch.uint8, device=DEV)
+    out, _, _ = run_and_check(b, workspace=ws)
+    g1 = out["dlogits"].clone()
+    t1 = out["terms"].clone()
+    out2 = cis.loss_bwd(b.logits, b.ids, b.logp_infer, b.adv, b.mask, lam=b.lam, kappa=b.kappa,
+                        scale=b.scale, V=b.V, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(out2["dlogits"].view(torch.int16), g1.view(torch.int16))
+    assert torch.equal(out2["terms"], t1)
+
+
 # Forward pass: rows of fewer than 2048 16-byte vectors go through the row kernel (capacities
 # 128, 256, 512, 1024, 2048 vectors); rows of 2048 up to 131072 vectors through the split
 # kernels (segments of 1024, 2048 or 4096 vectors, at most 32 per row); longer rows through the
