@@ -123,7 +123,7 @@ def bandwidth_ceilings(rows: int, row_bytes: int, torch) -> dict:
     n = rows * row_bytes
     src = torch.ones(n, dtype=torch.uint8, device="cuda")
     dst = torch.empty(n, dtype=torch.uint8, device="cuda")
-    sink = torch.zeros(1024, dtype=torch.int32, device="cuda")
+    sink = torch.zeros(1026, dtype=torch.int32, device="cuda")  # 1024 words + queue counter
     stream = torch.cuda.current_stream().cuda_stream
     grid = torch.cuda.get_device_properties(0).multi_processor_count
     out = {}

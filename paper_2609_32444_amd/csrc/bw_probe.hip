@@ -1,7 +1,8 @@
 // Bandwidth probes for the roofline: plain HBM copy, read and write kernels shaped like the
 // row kernel's traffic (one 1024-thread workgroup per row, 16-byte buffer accesses, every
-// vector of a row in flight at once, non-temporal). They measure what this device achieves for
-// pure reads, pure writes and an equal mix; they are not part of the loss.
+// vector of a row in flight at once, non-temporal, rows taken from a queue as the fused pass
+// takes them). They measure what this device achieves for pure reads, pure writes and an equal
+// mix; they are not part of the loss.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -19,12 +20,20 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, kRsrcWord3);
 }
 
-// mode 0: copy, 1: read only, 2: write only
+// mode 0: copy, 1: read only, 2: write only. A workgroup's first row is blockIdx.x; thread 0
+// draws the next one from the counter at sink[kSinkWords] while the row is in flight, and the
+// other waves read it after the row's barrier (double-buffered: one barrier per row).
+constexpr int kSinkWords = 1024;
 template <int MODE>
 __global__ __launch_bounds__(kBlock) void probe_kernel(const void* src, void* dst, int64_t rows,
                                                        uint32_t row_bytes, uint32_t* sink) {
+  __shared__ unsigned long long next[2];
+  unsigned long long* const queue = reinterpret_cast<unsigned long long*>(sink + kSinkWords);
   uint32_t acc = 0;
-  for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
+  int buf = 0;
+  for (int64_t r = blockIdx.x; r < rows;) {
+    unsigned long long tk = 0ull;
+    if (threadIdx.x == 0) tk = atomicAdd(queue, 1ull);
     const __amdgpu_buffer_rsrc_t rs = rsrc((const char*)src + r * row_bytes, row_bytes);
     const __amdgpu_buffer_rsrc_t ws = rsrc((char*)dst + r * row_bytes, row_bytes);
     u32x4 v[kSlots];
@@ -41,8 +50,16 @@ __global__ __launch_bounds__(kBlock) void probe_kernel(const void* src, void* ds
       else
         __builtin_amdgcn_raw_buffer_store_b128(v[k], ws, o, 0, kAuxNT);
     }
+    if (threadIdx.x == 0) next[buf] = tk;
+    __syncthreads();
+    r = (int64_t)gridDim.x + (int64_t)next[buf];
+    buf ^= 1;
   }
   if (MODE == 1 && acc == 0x9E3779B9u) sink[threadIdx.x] = acc;  // keeps the loads alive
+}
+
+__global__ __launch_bounds__(64) void probe_queue_reset(uint32_t* sink) {
+  if (threadIdx.x == 0) *reinterpret_cast<unsigned long long*>(sink + kSinkWords) = 0ull;
 }
 
 // Mode 3: the fastest equal read/write stream found on this part. Short-lived 128-thread
@@ -108,7 +125,12 @@ extern "C" int cis_probe_bandwidth(int mode, const void* src, void* dst, int64_t
   if (mode < 0 || mode > 2 || rows < 0 || grid < 1) return -4;
   if (row_bytes <= 0 || row_bytes % 16 != 0 || row_bytes > (int64_t)kSlots * kBlock * 16)
     return -2;
-  if ((mode != 2 && !src) || (mode != 1 && !dst) || (mode == 1 && !sink)) return -1;
+  if ((mode != 2 && !src) || (mode != 1 && !dst) || !sink) return -1;
+  if (reinterpret_cast<uintptr_t>(sink) % 8 != 0) return -2;
+  void* qargs[] = {&sink};
+  if (hipLaunchKernel((const void*)&probe_queue_reset, dim3(1), dim3(64), qargs, 0, stream) !=
+      hipSuccess)
+    return -6;
   void* args[] = {&src, &dst, &rows, &row_bytes, &sink};
   uint32_t rb = (uint32_t)row_bytes;
   args[3] = &rb;

@@ -744,95 +744,151 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 
     if (!PF) load_row(rs, g, voff, wid);
 
-    // ---- sweep 1a: max ------------------------------------------------------------------
-    float m = kMinRef;
-    if (valid) {
-      static_for<NV>([&](auto I) {
-        constexpr int i = I;
-        if (i < g.nres) {
-          float f[EPV];
-          E::unpack(r[i], f);
-#pragma unroll
-          for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
-        }
-        slot_fence();
-      });
-      // Entries of rp that are not logits of this row become -inf: lanes past the last
-      // vector and the padding after V in a ragged last vector.
-      rp = g.rp_mine ? rp : E::neg_inf_vec();
-      if (g.ragged && g.last_mine) rp = E::mask_tail(rp, g.tail);
-      if (g.has_rp) {
-        float f[EPV];
-        E::unpack(rp, f);
-#pragma unroll
-        for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
-      }
-      if (NL > 0 && g.nlds > 0) {
-        lds_fill_wait();
-        static_for<NL>([&](auto K) {
-          constexpr int k = K;
-          if (k < g.nlds) {
-            float f[EPV];
-            lds_vec(k, g, tid, f);
-#pragma unroll
-            for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
-          }
-        });
-      }
-    }
-    opaque(r);
-
-    // ---- streamed slots NV..L (rows longer than the registers hold): one online pass for
-    // max and exp-sum, the next vector's load in flight while the current one is summed ------
-    float s = 0.f, zy_mine = 0.f;
-    if (valid && !g.has_rp) stream_lse<E, BLOCK, !PF>(rs, g, voff, V, y, m, s, zy_mine);
-
-    // ---- sweep 1b: exp-sum excluding the sampled id ---------------------------------------
-    // (forward only with PF: the row's last sweep, so each register is refilled with the next
-    // row's vector right after it has been read)
+    // (Forward only with PF: sweep 1 is the row's last sweep, so each register is refilled with
+    // the next row's vector right after it has been read.)
     constexpr bool kRefill1 = PF && !BWD;
-    {
-      const float mb = m * kLog2e;
-      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    float m = kMinRef, s = 0.f, zy_mine = 0.f;
+    if constexpr (NL == 0) {
+      // ---- sweep 1: max and exp-sum in one online pass -------------------------------------
+      // Each vector is folded into the lane's running (max m, exp-sum s) as soon as its load
+      // has landed, so little of the sum is left once the row's last load arrives: the max
+      // includes the sampled logit, the sum leaves it out, and s is rescaled when the max
+      // grows. (The LDS variants below keep two passes: this one's extra registers spill
+      // there.)
+      auto fold_vec = [&](const float (&f)[EPV], bool has_y) {
+        float mv = m;
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) mv = fmaxf(mv, f[e]);
+        const float mb = mv * kLog2e;
+        float a0 = s * fast_exp2((m - mv) * kLog2e), a1 = 0.f;
+        if (has_y) {
+          asm volatile("");  // keeps the caller's uniform branch a branch
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) {
+            const bool hit = y_mine && e == ey;
+            zy_mine = hit ? f[e] : zy_mine;
+            const float x = hit ? 0.f : fast_exp2(__builtin_fmaf(f[e], kLog2e, -mb));
+            if (e & 1) a1 += x; else a0 += x;
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) {
+            const float x = fast_exp2(__builtin_fmaf(f[e], kLog2e, -mb));
+            if (e & 1) a1 += x; else a0 += x;
+          }
+        }
+        s = a0 + a1;
+        m = mv;
+      };
       static_for<NV>([&](auto I) {
         constexpr int i = I;
         float f[EPV];
         E::unpack(r[i], f);
         if (kRefill1)
           r[i] = bload(nrs, slot_off<BLOCK>(i, g, voff) + after(f[0], f[EPV / 4], f[EPV / 2], f[EPV - 1]), 0u);
-        if (valid && i < g.nres) {
-          if (i == slot_y)
-            accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
-          else
-            accum_vec<E>(f, mb, acc);
-        }
+        if (valid && i < g.nres) fold_vec(f, i == slot_y);
         slot_fence();
       });
+      if (valid) {
+        // Entries of rp that are not logits of this row become -inf: lanes past the last
+        // vector and the padding after V in a ragged last vector.
+        rp = g.rp_mine ? rp : E::neg_inf_vec();
+        if (g.ragged && g.last_mine) rp = E::mask_tail(rp, g.tail);
+      }
       {
         float f[EPV];
         E::unpack(rp, f);
         if (kRefill1) rp = bload(nrs, rp_off(BLOCK, g, voff) + after(f[0], f[EPV / 4], f[EPV / 2], f[EPV - 1]), 0u);
-        if (valid && g.has_rp) {
-          if (slot_y == g.L)
-            accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
-          else
-            accum_vec<E>(f, mb, acc);
+        if (valid && g.has_rp) fold_vec(f, slot_y == g.L);
+      }
+      // streamed slots NV..L (rows longer than the registers hold): the same online pass, the
+      // next vector's load in flight while the current one is summed
+      if (valid && !g.has_rp) stream_lse<E, BLOCK, !PF>(rs, g, voff, V, y, m, s, zy_mine);
+    } else {
+      // LDS variants (fused pass, rows beyond the registers): two passes over the resident
+      // slots, max first, then the exp-sum relative to it.
+      // ---- sweep 1a: max ------------------------------------------------------------------
+      if (valid) {
+        static_for<NV>([&](auto I) {
+          constexpr int i = I;
+          if (i < g.nres) {
+            float f[EPV];
+            E::unpack(r[i], f);
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
+          }
+          slot_fence();
+        });
+        // Entries of rp that are not logits of this row become -inf: lanes past the last
+        // vector and the padding after V in a ragged last vector.
+        rp = g.rp_mine ? rp : E::neg_inf_vec();
+        if (g.ragged && g.last_mine) rp = E::mask_tail(rp, g.tail);
+        if (g.has_rp) {
+          float f[EPV];
+          E::unpack(rp, f);
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
+        }
+        if (NL > 0 && g.nlds > 0) {
+          lds_fill_wait();
+          static_for<NL>([&](auto K) {
+            constexpr int k = K;
+            if (k < g.nlds) {
+              float f[EPV];
+              lds_vec(k, g, tid, f);
+#pragma unroll
+              for (int e = 0; e < EPV; ++e) m = fmaxf(m, f[e]);
+            }
+          });
         }
       }
-      if (NL > 0 && valid) {
-        static_for<NL>([&](auto K) {
-          constexpr int k = K;
-          if (k < g.nlds) {
-            float f[EPV];
-            lds_vec(k, g, tid, f);
-            if (NV + k == slot_y)
+      opaque(r);
+
+      // ---- streamed slots NV..L: one online pass for max and exp-sum, the next vector's load
+      // in flight while the current one is summed -------------------------------------------
+      if (valid && !g.has_rp) stream_lse<E, BLOCK, !PF>(rs, g, voff, V, y, m, s, zy_mine);
+
+      // ---- sweep 1b: exp-sum excluding the sampled id -------------------------------------
+      {
+        const float mb = m * kLog2e;
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        static_for<NV>([&](auto I) {
+          constexpr int i = I;
+          float f[EPV];
+          E::unpack(r[i], f);
+          if (valid && i < g.nres) {
+            if (i == slot_y)
               accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
             else
               accum_vec<E>(f, mb, acc);
           }
+          slot_fence();
         });
+        {
+          float f[EPV];
+          E::unpack(rp, f);
+          if (valid && g.has_rp) {
+            if (slot_y == g.L)
+              accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
+            else
+              accum_vec<E>(f, mb, acc);
+          }
+        }
+        if (NL > 0 && valid) {
+          static_for<NL>([&](auto K) {
+            constexpr int k = K;
+            if (k < g.nlds) {
+              float f[EPV];
+              lds_vec(k, g, tid, f);
+              if (NV + k == slot_y)
+                accum_vec_skip<E>(f, mb, acc, y_mine, ey, zy_mine);
+              else
+                accum_vec<E>(f, mb, acc);
+            }
+          });
+        }
+        s += (acc[0] + acc[1]) + (acc[2] + acc[3]);
       }
-      s += (acc[0] + acc[1]) + (acc[2] + acc[3]);
     }
     if (BWD) opaque(r);
     asm volatile("" : "+v"(voff));
