@@ -211,13 +211,18 @@ __device__ __forceinline__ void lse_combine(float& m, float& s, float m2, float 
   m = mn;
 }
 
+// Wave-wide (m, s): the max first, then each lane's sum rescaled to it once and added up, so
+// the exponentials are independent rather than a chain of pairwise combines. The xor tree
+// gives every lane the same bits (each step adds the same two values in either order).
 __device__ __forceinline__ void wave_lse_reduce(float& m, float& s) {
+  float M = m;
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float m2 = __shfl_xor(m, off, 64);
-    const float s2 = __shfl_xor(s, off, 64);
-    lse_combine(m, s, m2, s2);
-  }
+  for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
+  float t = s * fast_exp2((m - M) * kLog2e);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) t += __shfl_xor(t, off, 64);
+  m = M;
+  s = t;
 }
 
 // Optimisation barrier: the register-resident row is "redefined" here, so the compiler cannot
@@ -919,9 +924,13 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
       }
       if (y_mine) sh_zy[buf] = zy_mine;
       __syncthreads();
-      float M = sh_m[buf][0], sr = sh_s[buf][0];
+      // the waves' pairs: max, then the rescaled sums in wave order (independent exponentials)
+      float M = sh_m[buf][0];
 #pragma unroll
-      for (int w = 1; w < NW; ++w) lse_combine(M, sr, sh_m[buf][w], sh_s[buf][w]);
+      for (int w = 1; w < NW; ++w) M = fmaxf(M, sh_m[buf][w]);
+      float sr = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) sr += sh_s[buf][w] * fast_exp2((sh_m[buf][w] - M) * kLog2e);
       const float zy = sh_zy[buf];
       nn = drawn();
       buf ^= 1;
