@@ -276,12 +276,6 @@ struct RowGeom {
   int sbeg;          // first streamed slot (streaming covers sbeg..L)
 };
 
-// Offset of slot i for this thread, or an out-of-range offset when slot i is not resident (its
-// loads then return zeros and move no data, its stores are dropped).
-template <int BLOCK>
-__device__ __forceinline__ uint32_t slot_off(int i, const RowGeom& g, uint32_t voff) {
-  return i < g.nres ? voff + (uint32_t)(i * BLOCK * 16) : kOutOfRange;
-}
 __device__ __forceinline__ uint32_t rp_off(int BLOCK, const RowGeom& g, uint32_t voff) {
   return (g.has_rp && g.rp_mine) ? voff + (uint32_t)(g.L * BLOCK * 16) : kOutOfRange;
 }
@@ -686,8 +680,15 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     return make_rsrc((const char*)a.logits + (valid ? row : 0) * a.row_bytes,
                      valid ? (uint32_t)g.nvec * 16u : 0u);
   };
-  auto load_row = [&](__amdgpu_buffer_rsrc_t rs, const RowGeom& g, uint32_t voff, int wid) {
-    static_for<NV>([&](auto I) { r[I] = bload(rs, slot_off<BLOCK>(I, g, voff), 0u); });
+  // The same for the register slots only (slots 0..nres-1, all complete): their accesses need
+  // no per-slot test, the range check drops the slots a shorter row does not have.
+  auto reg_rsrc = [&](int64_t row, bool valid, const RowGeom& g) {
+    return make_rsrc((const char*)a.logits + (valid ? row : 0) * a.row_bytes,
+                     valid ? (uint32_t)(g.nres * BLOCK * 16) : 0u);
+  };
+  auto load_row = [&](__amdgpu_buffer_rsrc_t rs, __amdgpu_buffer_rsrc_t rr, const RowGeom& g,
+                      uint32_t voff, int wid) {
+    static_for<NV>([&](auto I) { r[I] = bload(rr, voff + (uint32_t)(I * BLOCK * 16), 0u); });
     rp = bload(rs, rp_off(BLOCK, g, voff), 0u);
     // (unused LDS slots get out-of-range offsets rather than a branch, so every row issues
     // the same loads and the compiler's wait counts stay exact)
@@ -709,7 +710,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     const RowGeom g = geometry(tid);
     const int64_t row = blockIdx.x;
     const bool v0 = fetch_row_scalars<EXT>(a, row).valid(V);
-    load_row(row_rsrc(row, v0, g), g, (uint32_t)tid * 16u, 0);
+    load_row(row_rsrc(row, v0, g), reg_rsrc(row, v0, g), g, (uint32_t)tid * 16u, 0);
   }
 
   RowScalars cur = fetch_row_scalars<EXT>(a, blockIdx.x);
@@ -739,15 +740,19 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     const int slot_y = vy / BLOCK;
     const bool y_mine = (vy % BLOCK) == tid;
     const __amdgpu_buffer_rsrc_t rs = row_rsrc(row, valid, g);
+    const __amdgpu_buffer_rsrc_t rr = reg_rsrc(row, valid, g);
     void* grow = BWD ? (void*)((char*)a.dlogits + row * a.grow_bytes) : nullptr;
     // write descriptor: complete vectors only
     const __amdgpu_buffer_rsrc_t ws = make_rsrc(
         grow, BWD ? ((uint32_t)(g.nvec - (g.ragged ? 1 : 0)) * 16u) >> GO::kShift : 0u);
+    const __amdgpu_buffer_rsrc_t wr =
+        make_rsrc(grow, BWD ? (uint32_t)(g.nres * BLOCK * 16) >> GO::kShift : 0u);
     // the next row of this workgroup (prefetched during this row's last sweep)
     const bool nvalid = PF && cur.valid(V);
     const __amdgpu_buffer_rsrc_t nrs = row_rsrc(nrow, nvalid, g);
+    const __amdgpu_buffer_rsrc_t nrr = reg_rsrc(nrow, nvalid, g);
 
-    if (!PF) load_row(rs, g, voff, wid);
+    if (!PF) load_row(rs, rr, g, voff, wid);
 
     // (Forward only with PF: sweep 1 is the row's last sweep, so each register is refilled with
     // the next row's vector right after it has been read.)
@@ -790,7 +795,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
         float f[EPV];
         E::unpack(r[i], f);
         if (kRefill1)
-          r[i] = bload(nrs, slot_off<BLOCK>(i, g, voff) + after(f[0], f[EPV / 4], f[EPV / 2], f[EPV - 1]), 0u);
+          r[i] = bload(nrr, voff + (uint32_t)(i * BLOCK * 16) + after(f[0], f[EPV / 4], f[EPV / 2], f[EPV - 1]), 0u);
         if (valid && i < g.nres) fold_vec(f, i == slot_y);
         slot_fence();
       });
@@ -953,22 +958,22 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     // Every vector is stored through the write descriptor (which drops the partial last vector
     // and out-of-range lanes); the partial last vector is then written element by element, and
     // finally the sampled element is overwritten with coef*(1-p) by the thread that stored its
-    // vector (same-thread program order). Invalid rows store zeros.
+    // vector (same-thread program order). Invalid rows store zeros: their register slots and
+    // rp were loaded through empty descriptors (zeros) and their b2 is +inf, so the same
+    // arithmetic gives exp2(-inf) = 0 without a branch.
     if (BWD) {
       const uint32_t sgn = coef > 0.f ? GO::kSign : 0u;
       static_for<NV>([&](auto I) {
         constexpr int i = I;
-        const uint32_t o = slot_off<BLOCK>(i, g, voff);
-        typename GO::vec out = GO::zero();
-        if (valid) out = GO::make(r[i], b2, sgn);
-        if (PF) r[i] = bload(nrs, o + after(out), 0u);
-        GO::store(out, ws, o);
+        const uint32_t o = voff + (uint32_t)(i * BLOCK * 16);
+        const typename GO::vec out = GO::make(r[i], b2, sgn);
+        if (PF) r[i] = bload(nrr, o + after(out), 0u);
+        GO::store(out, wr, o);
         slot_fence();
       });
       {
         const uint32_t o = rp_off(BLOCK, g, voff);
-        typename GO::vec out = GO::zero();
-        if (valid) out = GO::make(rp, b2, sgn);
+        const typename GO::vec out = GO::make(rp, b2, sgn);
         if (PF) rp = bload(nrs, o + after(out), 0u);
         GO::store(out, ws, o);
       }
