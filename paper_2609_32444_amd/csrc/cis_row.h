@@ -1027,11 +1027,13 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 // fewer slots per thread than the forward pass, prefetches the next row during the gradient
 // sweep only on short rows (on long ones it costs more than it hides), and adds 9 LDS slots
 // (144 KiB) for rows beyond its registers. The fp32 forward kernel stops at 15 slots (18
-// would spill the prefetched row to scratch).
+// would spill the prefetched row to scratch). Once the fused pass took its rows from a queue,
+// 512 x 7 overtook 256 x 15 for rows of up to 4096 vectors (V = 32768 in bf16: 0.676 against
+// 0.684 ms; 1024 x 3: 0.747).
 #define CIS_BWD_TABLE_OUT(E, EO)                                                            \
   {CIS_VO(E, EO, 64, 1, 0, true),     CIS_VO(E, EO, 64, 3, 0, true),                        \
    CIS_VO(E, EO, 64, 7, 0, true),     CIS_VO(E, EO, 64, 15, 0, true),                       \
-   CIS_VO(E, EO, 512, 3, 0, false),   CIS_VO(E, EO, 256, 15, 0, true),                      \
+   CIS_VO(E, EO, 512, 3, 0, false),   CIS_VO(E, EO, 512, 7, 0, true),                       \
    CIS_VO(E, EO, 1024, 7, 0, false),  CIS_VO(E, EO, 1024, 11, 0, false),                    \
    CIS_VO(E, EO, 1024, 15, 0, false), CIS_VO(E, EO, 1024, 18, 0, false),                    \
    CIS_VO(E, EO, 1024, 18, 9, false)}
