@@ -74,39 +74,39 @@ def _check_full(name, b, out, grad_rows=None, scalar_rows=None, z=None, ref=None
     return report
 
 
-def test_config0_tiny_all_rows():
+def test_tiny_fp32_all_rows():
     b = make_batch(0, device="cuda")
-    _check_full("cfg0", b, _run(b))
+    _check_full("tiny", b, _run(b))
 
 
-def test_config1_small_bf16_all_rows():
+def test_small_bf16_all_rows():
     b = make_batch(1, device="cuda")
-    _check_full("cfg1", b, _run(b))
+    _check_full("small", b, _run(b))
 
 
 @pytest.mark.parametrize("c", [0.5, 1.0, 2.0])
-def test_config2_moe_full_size(c):
+def test_moe_rollout_full_size(c):
     """Every row of the MoE-rollout batch: per-token outputs, loss and all 2.5e9 gradient
     elements against the oracle."""
     b = make_batch(2, device="cuda", c=c)
     out = _run(b)
-    rep = _check_full(f"cfg2_c{c}", b, out)
+    rep = _check_full(f"moe_rollout_c{c}", b, out)
     assert rep["grad"]["n_rows"] == b.T
 
 
 @pytest.mark.parametrize("chunk", range(8))
-def test_config3_long_chunk(chunk):
+def test_long_response_chunk(chunk):
     """One 65536-row chunk of the long-response workload: every row's per-token outputs and
     the chunk's loss, and the gradients of 4096 seeded rows plus the first, last and
     heavy-tail rows."""
     b = make_batch(3, device="cuda", chunk=chunk)
     out = _run(b)
     grows = _sample_rows(b.T, 4096, seed=200 + chunk, extra=b.meta["outlier_rows"])
-    rep = _check_full(f"cfg3_chunk{chunk}", b, out, grad_rows=grows)
+    rep = _check_full(f"long_response_chunk{chunk}", b, out, grad_rows=grows)
     assert rep["trunc"] > 0 and rep["grad_rows"] >= 4096
 
 
-def test_config4_wide_vocab_fwd_and_bwd():
+def test_wide_vocab_fwd_and_bwd():
     """Wide vocabulary, forward only and fused: every row's per-token outputs and the loss,
     and the fused pass's gradients on 1024 seeded rows plus the first and last rows."""
     b = make_batch(4, device="cuda")
@@ -114,9 +114,9 @@ def test_config4_wide_vocab_fwd_and_bwd():
     z = P.host_logits(b.logits)
     ref = P.oracle_for_batch(b, with_grad=False, z=z)
     out_f = _run(b, bwd=False)
-    _check_full("cfg4_fwd", b, out_f, z=z, ref=ref)
+    _check_full("wide_vocab_fwd", b, out_f, z=z, ref=ref)
     out_b = _run(b, bwd=True)
-    rep = _check_full("cfg4_bwd", b, out_b, grad_rows=grows, z=z, ref=ref)
+    rep = _check_full("wide_vocab_bwd", b, out_b, grad_rows=grows, z=z, ref=ref)
     assert rep["grad_rows"] >= 1024
     # Both passes also agree with each other to float32 rounding. (Not bit for bit: the fused
     # pass sums a row in one workgroup, the forward pass in 16 KiB segments that are combined
@@ -127,7 +127,7 @@ def test_config4_wide_vocab_fwd_and_bwd():
     assert abs(out_f["loss"].item() - out_b["loss"].item()) <= 1e-5 * abs(out_f["loss"].item())
 
 
-def test_determinism_config2():
+def test_determinism_moe_rollout():
     b = make_batch(2, device="cuda", c=1.0, rows=2048)
     o1 = _run(b)
     g1 = o1["dlogits"].clone()

@@ -1,8 +1,8 @@
 """Calibrates the peak offsets used by workloads.synth (run once; prints the constants).
 
-Targets, from the workload descriptions: config 1 has a mean sampled-token training
-confidence of about 0.8; config 3 has about 80% of its tokens with sampled training
-probability above 0.95. The training probability of a sampled id is read off torch.softmax of
+Targets, from the workload descriptions: the small workload (T = 32768, V = 32768) has a mean
+sampled-token training confidence of about 0.8; the long-response workload (V = 151936) has
+about 80% of its tokens with sampled training probability above 0.95. The training probability of a sampled id is read off torch.softmax of
 the pilot rows (a library routine; this script is not part of the loss path).
 
     python -m workloads.calibrate

@@ -42,9 +42,9 @@ from dataclasses import dataclass, field
 import torch
 
 # Peak offsets, calibrated by workloads/calibrate.py (see that script for the targets).
-PEAK_1 = 4.69            # config 1: mean sampled training probability ~ 0.80
-PEAK_3 = 9.0             # config 3: peaked rows have training probability of the peak > 0.99
-PEAK_3_FRACTION = 0.81   # config 3: ~80% of tokens with sampled training probability > 0.95
+PEAK_1 = 4.69            # small workload: mean sampled training probability ~ 0.80
+PEAK_3 = 9.0             # long response: peaked rows have training probability of the peak > 0.99
+PEAK_3_FRACTION = 0.81   # long response: ~80% of tokens with sampled training probability > 0.95
 
 KAPPA = 5e-3
 
@@ -137,7 +137,7 @@ def _fill_rows(batch_logits, ids, lq, r0, z, delta, g, store_dtype):
 def make_batch(cfg: int, device="cuda", seed: int | None = None, chunk: int = 0,
                c: float | None = None, rows: int | None = None,
                rows_per_step: int = 1024) -> Batch:
-    """Builds the inputs of configuration `cfg` (chunk `chunk` of the chunked config 3).
+    """Builds the inputs of workload `cfg` (chunk `chunk` of the chunked long-response workload).
 
     Every per-row quantity of the full batch (advantages, masks, outlier and peak rows) is
     drawn first and the logits afterwards, `rows_per_step` rows at a time; `rows` keeps only
