@@ -72,8 +72,8 @@ def test_long_rows_many_per_workgroup(V, dtype):
 
 
 # Fused-pass rows come from a queue once every workgroup has had two rows. The row counts put
-# thousands of rows in the queue for the one-wave, 256-thread, 1024-thread and LDS variants
-# (resident grids of up to 7168, 1024, 256 and 256 workgroups).
+# thousands of rows in the queue for the one-wave, 512-thread, 1024-thread and LDS variants
+# (resident grids of up to 7168, 768, 256 and 256 workgroups).
 @pytest.mark.parametrize("V,T", [(1000, 20000), (32768, 4096), (151936, 1500), (250001, 700)])
 def test_row_queue_and_stale_workspace(V, T):
     """The workspace starts as all 0xFF bytes: as the row queue's counter that would hand out
