@@ -50,7 +50,7 @@ def kernel_source_hash(extra=()) -> str:
     for f in ("paper_2609_32444_amd/csrc/cis_row.h", "paper_2609_32444_amd/csrc/cis_kernels.hip",
               "paper_2609_32444_amd/csrc/cis_kernels_ext.hip",
               "paper_2609_32444_amd/csrc/cis_api.cpp", "paper_2609_32444_amd/csrc/cis_internal.h",
-              *extra):
+              "paper_2609_32444_amd/csrc/cis_seg.h", *extra):
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -1,14 +1,15 @@
 // Row kernel of the CIS token loss (gfx950), shared by the base and the extended kernels.
-// Row kernel design (one persistent workgroup per row at a time):
+// Row kernel design (one persistent workgroup per row at a time; the fused pass takes its rows
+// from a queue):
 //   * Each thread owns the 16-byte vectors v = tid, tid + BLOCK, ... of the row. The first
 //     NV of them stay in VGPRs from the load to the gradient store, so a row that fits in
 //     NV*BLOCK vectors is read from HBM exactly once. Long rows park the next NL slots in
 //     LDS (filled by buffer loads that write LDS directly, no register round trip); vectors
 //     beyond that are streamed: read once for the exp-sum and, with the gradient, once more.
-//   * Sweep 1: per-lane max over the resident vectors, an online (max, exp-sum) pass over the
-//     streamed ones, then the exp-sum of the resident vectors; the sampled id is left out of
-//     the sum. Lanes combine across the wave with shuffles and across waves through LDS in a
-//     fixed order (deterministic).
+//   * Sweep 1: an online (max, exp-sum) pass per lane, each vector folded in as its load
+//     lands (the LDS variants take the max of the resident vectors first and their exp-sum
+//     after); the sampled id is left out of the sum. Lanes combine across the wave with
+//     shuffles and across waves through LDS in a fixed order (deterministic).
 //   * Epilogue: l_train, 1 - p (complement mass), the weight (Algorithm 1, or an operator of
 //     the family, or the pre-pass weight with the clipped update ratio of Eq. (1)) and the
 //     loss term, all computed redundantly by every thread from the same LDS values.
@@ -263,7 +264,8 @@ __device__ __forceinline__ uint32_t after(float a, float b, float c, float d) {
 // Row geometry shared by the sweeps. Vector v = i*BLOCK + tid of the row is "slot i" of thread
 // tid; slot L = (nvec-1)/BLOCK holds the last vector. When L <= NV, slots 0..L-1 (all complete)
 // live in r[0..L-1] and slot L (possibly partial, possibly ending in padding) in one extra
-// register vector rp; otherwise r holds slots 0..NV-1 and slots NV..L are streamed twice.
+// register vector rp; otherwise r holds slots 0..NV-1, the next nlds slots sit in LDS and the
+// rest up to L are streamed twice.
 struct RowGeom {
   int nvec, tail;
   int L;             // slot of the last vector
