@@ -650,6 +650,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
   __shared__ float sh_s[2][NW];
   __shared__ float sh_zy[2];
   __shared__ unsigned long long sh_q[2];
+  __shared__ float sh_ep[2][3];  // wave 0's epilogue for the other waves: coef, b2, 1 - p
   // slot NV+k of thread tid at lds_row[k*BLOCK + tid]; each wave fills and reads its own part
   __shared__ u32x4 lds_row[NL > 0 ? NL * BLOCK : 1];
 
@@ -907,8 +908,8 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 
     // ---- block reduction and epilogue: l_train, 1 - p, weight (Algorithm 1), loss term -----
     float coef = 0.f, b2 = INFINITY, one_m_p = 0.f;
-    // (one barrier per row, valid or not, so that the double-buffered shared values of row n
-    // are read before row n + 2 writes them)
+    // (at least one barrier per row, valid or not, so that the double-buffered shared values
+    // of row n are read before row n + 2 writes them)
     if (kQueue && NW > 1 && tid == 0) sh_q[buf] = tk;
     auto drawn = [&]() -> int64_t {
       if (!kQueue) return nrow + gridDim.x;
@@ -931,24 +932,40 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
       }
       if (y_mine) sh_zy[buf] = zy_mine;
       __syncthreads();
-      // the waves' pairs: max, then the rescaled sums in wave order (independent exponentials)
-      float M = sh_m[buf][0];
-#pragma unroll
-      for (int w = 1; w < NW; ++w) M = fmaxf(M, sh_m[buf][w]);
-      float sr = 0.f;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) sr += sh_s[buf][w] * fast_exp2((sh_m[buf][w] - M) * kLog2e);
-      const float zy = sh_zy[buf];
       nn = drawn();
+      // Wave 0 alone combines the waves' pairs and runs the epilogue (a few hundred serial
+      // instructions); the other waves wait at the next barrier and read its result from LDS.
+      // Alone on its SIMD, wave 0 finishes sooner than sixteen waves doing the same work.
+      if (NW == 1 || wid == 0) {
+        // the waves' pairs: max, then the rescaled sums in wave order (independent exponentials)
+        float M = sh_m[buf][0];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) M = fmaxf(M, sh_m[buf][w]);
+        float sr = 0.f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) sr += sh_s[buf][w] * fast_exp2((sh_m[buf][w] - M) * kLog2e);
+        const float zy = sh_zy[buf];
+        // M: max over the row (sampled element included); sr: sum_{j != y} exp(z_j - M).
+        const RowResult rr = row_epilogue<EXT>(a, rsc, row, M, sr, zy, tid == 0);
+        coef = rr.coef;
+        one_m_p = rr.one_m_p;
+        // g_j = -coef * exp(z_j - lse) = sign * exp2(z_j*log2e - b2) with sign = -sign(coef)
+        // and b2 = (lse - ln|coef|) * log2e; coef = 0 keeps b2 = +inf, which gives an all-zero
+        // row. The float32 offset is accurate to a few 1e-6 relative, far inside bf16 rounding.
+        if (BWD && coef != 0.f) b2 = (rr.lse - logf(fabsf(coef))) * kLog2e;
+        if (NW > 1 && tid == 0) {
+          sh_ep[buf][0] = coef;
+          sh_ep[buf][1] = b2;
+          sh_ep[buf][2] = one_m_p;
+        }
+      }
+      if (NW > 1) {
+        __syncthreads();
+        coef = sh_ep[buf][0];
+        b2 = sh_ep[buf][1];
+        one_m_p = sh_ep[buf][2];
+      }
       buf ^= 1;
-      // M: max over the row (sampled element included); sr: sum_{j != y} exp(z_j - M).
-      const RowResult rr = row_epilogue<EXT>(a, rsc, row, M, sr, zy, tid == 0);
-      coef = rr.coef;
-      one_m_p = rr.one_m_p;
-      // g_j = -coef * exp(z_j - lse) = sign * exp2(z_j*log2e - b2) with sign = -sign(coef)
-      // and b2 = (lse - ln|coef|) * log2e; coef = 0 keeps b2 = +inf, which gives an all-zero
-      // row. The float32 offset is accurate to a few 1e-6 relative, far inside bf16 rounding.
-      if (BWD && coef != 0.f) b2 = (rr.lse - logf(fabsf(coef))) * kLog2e;
     } else {
       if (kQueue && NW > 1) __syncthreads();
       nn = drawn();
