@@ -261,8 +261,9 @@ cis::RowArgs row_args(const LossCall& c, const Ws& ws, const void* logits, void*
 int launch_combine(const LossCall& c, cis::RowArgs& ra, cis::SegArgs& sa, int64_t rows,
                    hipStream_t stream) {
   void* args[] = {&ra, &sa};
-  const int64_t per = cis::kCombineBlock / 64;
-  return hipLaunchKernel(cis::combine_kernel(c.ext), dim3((unsigned)((rows + per - 1) / per)),
+  const bool lane = sa.nseg <= cis::kSegMax;  // one lane per row, else one wave per row
+  const int64_t per = lane ? cis::kCombineBlock : cis::kCombineBlock / 64;
+  return hipLaunchKernel(cis::combine_kernel(c.ext, lane), dim3((unsigned)((rows + per - 1) / per)),
                          dim3(cis::kCombineBlock), args, 0, stream) == hipSuccess
              ? CIS_OK
              : CIS_ERR_LAUNCH;

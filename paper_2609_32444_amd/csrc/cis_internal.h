@@ -203,8 +203,9 @@ struct SegVariant {
 // The segment kernel for rows of `nvec` vectors, or nullptr when the row kernel serves them
 // better (short rows) or they need more than kSegMax segments of the largest variant.
 const SegVariant* select_seg_variant(int dtype, int32_t nvec);
-const void* combine_kernel(bool ext);
-const void* combine_kernel_ext();
+// lane: one lane per row (rows of at most kSegMax pieces), else one wave per row
+const void* combine_kernel(bool ext, bool lane);
+const void* combine_kernel_ext(bool lane);
 
 struct FinalizeArgs {
   const float* terms_ws;

@@ -147,8 +147,9 @@ const SegVariant* select_seg_variant(int dtype, int32_t nvec) {
   return nullptr;
 }
 
-const void* combine_kernel(bool ext) {
-  return ext ? combine_kernel_ext() : (const void*)&cis_combine_kernel<false>;
+const void* combine_kernel(bool ext, bool lane) {
+  if (ext) return combine_kernel_ext(lane);
+  return lane ? (const void*)&cis_combine_lane_kernel<false> : (const void*)&cis_combine_kernel<false>;
 }
 
 // Clears the row kernel's queue counter ahead of each launch: a kernel rather than a memset, so

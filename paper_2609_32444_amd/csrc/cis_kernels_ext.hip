@@ -121,7 +121,9 @@ __global__ __launch_bounds__(kWeightsBlock) void cis_prepass_kernel(const Prepas
 }
 
 const void* seq_sum_kernel() { return (const void*)&cis_seq_sum_kernel; }
-const void* combine_kernel_ext() { return (const void*)&cis_combine_kernel<true>; }
+const void* combine_kernel_ext(bool lane) {
+  return lane ? (const void*)&cis_combine_lane_kernel<true> : (const void*)&cis_combine_kernel<true>;
+}
 const void* prepass_kernel() { return (const void*)&cis_prepass_kernel; }
 
 }  // namespace cis

@@ -454,6 +454,22 @@ __device__ __forceinline__ RowScalars fetch_row_scalars(const RowArgs& a, int64_
   return s;
 }
 
+// The same inputs through vector loads, for kernels whose lanes take different rows.
+template <bool EXT>
+__device__ __forceinline__ RowScalars fetch_row_scalars_lane(const RowArgs& a, int64_t row) {
+  RowScalars s{0, 0.f, 0.f, 0.f, 0.f, false, false};
+  s.y = a.ids[row];
+  s.on = a.mask ? (a.mask[row] != 0) : true;
+  s.logp_infer = a.logp_infer[row];
+  s.adv = a.adv[row];
+  if (EXT && a.logp_old) {
+    s.logp_old = a.logp_old[row];
+    s.wpre = a.wpre_ws[row];
+    s.pacted = (a.pflags_ws[row] & kFlagTrunc) != 0;
+  }
+  return s;
+}
+
 // ------------------------------------------------------------------------------------------
 // The operator family (App. C.1 "Operators", Table tab:baselines): the weight on the token
 // loss from the training-side log-probability lp (and 1 - p), the inference-side lq, with

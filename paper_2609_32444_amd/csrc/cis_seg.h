@@ -9,9 +9,12 @@
 //     stores it. Invalid rows are not read. The workgroups are short-lived: a persistent grid
 //     whose workgroups walk segment after segment, with the next segment's loads in flight,
 //     measured 10-30% slower.
-//   * cis_combine_kernel: one wave per row folds the row's partials in segment order (lane l
-//     takes partials l, l + 64, ..., then a fixed xor tree), so the result does not depend on
-//     which segment finished first, and runs the row kernel's epilogue.
+//   * cis_combine_kernel: folds each row's partials in a fixed order, so the result does not
+//     depend on which segment finished first, and runs the row kernel's epilogue. Rows of at
+//     most kSegMax partials (every split row) take one lane each: the max of the partials, then
+//     their rescaled sums in segment order, and the epilogue by that lane alone. Rows of more
+//     partials (the LM head's 64-column pieces) take one wave each: lane l takes partials
+//     l, l + 64, ..., then a fixed xor tree.
 //
 // A row's logits are read once, like the register-resident row kernel; the difference is the
 // traffic pattern: many small independent reads per CU instead of one row-sized working set,
@@ -102,6 +105,37 @@ __global__ __launch_bounds__(BLOCK) void cis_seg_kernel(const RowArgs a, const S
   }
 }
 
+// GradParams of a row for the fused LM-head pass: the row kernel's gradient
+// -coef exp(z - lse) = s exp2(z log2(e) - b2), and coef (1 - p) at y.
+__device__ __forceinline__ GradParams grad_params(const RowResult& rr, int64_t y) {
+  const float coef = rr.coef;
+  const float b2 = coef != 0.f ? (rr.lse - logf(fabsf(coef))) * kLog2e : INFINITY;
+  return GradParams{b2, coef > 0.f ? 1 : 0, coef * rr.one_m_p, (int32_t)y};
+}
+
+template <bool EXT>
+__global__ __launch_bounds__(kCombineBlock) void cis_combine_lane_kernel(const RowArgs a,
+                                                                         const SegArgs g) {
+  const int64_t row = (int64_t)blockIdx.x * kCombineBlock + threadIdx.x;
+  if (row >= a.T) return;  // no barrier follows
+  const RowScalars rsc = fetch_row_scalars_lane<EXT>(a, row);
+  if (!rsc.valid(a.V)) {
+    row_invalid<EXT>(a, rsc, row);
+    if (g.gp) g.gp[row] = GradParams{INFINITY, 0, 0.f, -1};
+    return;
+  }
+  const float2* pr = g.part + row * g.stride;
+  float M = kMinRef;
+  for (int k = 0; k < g.nseg; ++k) M = fmaxf(M, pr[k].x);
+  float s = 0.f;
+  for (int k = 0; k < g.nseg; ++k) {
+    const float2 p = pr[k];
+    s += p.y * fast_exp2((p.x - M) * kLog2e);
+  }
+  const RowResult rr = row_epilogue<EXT>(a, rsc, row, M, s, g.zy[row], true);
+  if (g.gp) g.gp[row] = grad_params(rr, rsc.y);
+}
+
 template <bool EXT>
 __global__ __launch_bounds__(kCombineBlock) void cis_combine_kernel(const RowArgs a,
                                                                     const SegArgs g) {
@@ -125,12 +159,7 @@ __global__ __launch_bounds__(kCombineBlock) void cis_combine_kernel(const RowArg
   wave_lse_reduce(m, s);
   const float zy = g.zy[row];
   const RowResult rr = row_epilogue<EXT>(a, rsc, row, m, s, zy, lane == 0);
-  if (g.gp && lane == 0) {
-    // the row kernel's gradient: -coef exp(z - lse) = s exp2(z log2(e) - b2), coef (1 - p) at y
-    const float coef = rr.coef;
-    const float b2 = coef != 0.f ? (rr.lse - logf(fabsf(coef))) * kLog2e : INFINITY;
-    g.gp[row] = GradParams{b2, coef > 0.f ? 1 : 0, coef * rr.one_m_p, (int32_t)rsc.y};
-  }
+  if (g.gp && lane == 0) g.gp[row] = grad_params(rr, rsc.y);
 }
 
 }  // namespace cis
