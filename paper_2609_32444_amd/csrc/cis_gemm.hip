@@ -225,19 +225,30 @@ __device__ __forceinline__ void lse_tile(const GemmArgs& g, const f32x4 (&acc)[k
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float mb = mx * kLog2e;
+    const int dy = y - nb;  // the sampled column in this lane's 4 x 4 columns?
+    const bool has_y = dy >= 0 && dy < kTn * 16 && (dy & 15) < 4;
     float sm = 0.f;
+    if (has_y) {  // the one lane of the row that holds y leaves it out element by element
 #pragma unroll
-    for (int j = 0; j < kTn; ++j)
+      for (int j = 0; j < kTn; ++j)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int n = nb + j * 16 + e;
-        const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][e], kLog2e, -mb));
-        sm += ((FULL || n < N) && n != y) ? x : 0.f;
-      }
+        for (int e = 0; e < 4; ++e) {
+          const int n = nb + j * 16 + e;
+          const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][e], kLog2e, -mb));
+          sm += ((FULL || n < N) && n != y) ? x : 0.f;
+        }
+    } else {
+#pragma unroll
+      for (int j = 0; j < kTn; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][e], kLog2e, -mb));
+          sm += (FULL || nb + j * 16 + e < N) ? x : 0.f;
+        }
+    }
     sm += __shfl_xor(sm, 16, 64);
     sm += __shfl_xor(sm, 32, 64);
-    const int dy = y - nb;  // the sampled column in this lane's 4 x 4 columns?
-    if (row_ok && dy >= 0 && dy < kTn * 16 && (dy & 15) < 4) {
+    if (row_ok && has_y) {
 #pragma unroll
       for (int j = 0; j < kTn; ++j)
 #pragma unroll
