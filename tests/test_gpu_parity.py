@@ -108,16 +108,15 @@ def test_long_response_chunk(chunk):
 
 def test_wide_vocab_fwd_and_bwd():
     """Wide vocabulary, forward only and fused: every row's per-token outputs and the loss,
-    and the fused pass's gradients on 1024 seeded rows plus the first and last rows."""
+    and the fused pass's gradient on every row."""
     b = make_batch(4, device="cuda")
-    grows = _sample_rows(b.T, 1024, seed=401)
     z = P.host_logits(b.logits)
     ref = P.oracle_for_batch(b, with_grad=False, z=z)
     out_f = _run(b, bwd=False)
     _check_full("wide_vocab_fwd", b, out_f, z=z, ref=ref)
     out_b = _run(b, bwd=True)
-    rep = _check_full("wide_vocab_bwd", b, out_b, grad_rows=grows, z=z, ref=ref)
-    assert rep["grad_rows"] >= 1024
+    rep = _check_full("wide_vocab_bwd", b, out_b, z=z)
+    assert rep["grad_rows"] == b.T
     # Both passes also agree with each other to float32 rounding. (Not bit for bit: the fused
     # pass sums a row in one workgroup, the forward pass in 16 KiB segments that are combined
     # afterwards, so the exp-sum is accumulated in a different order.)
