@@ -212,18 +212,46 @@ __device__ __forceinline__ void lse_combine(float& m, float& s, float m2, float 
   m = mn;
 }
 
+// Lane x of the lane's row of 16 after a DPP permutation within that row (CTRL: quad_perm,
+// row_mirror or row_half_mirror; no lane leaves its row).
+template <int CTRL>
+__device__ __forceinline__ float dpp16(float x) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float lane_value(float x, int lane) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), lane));
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E;              // quad_perm [1,0,3,2], [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141, kDppRowMirror = 0x140;  // lane i <-> 7-i, i <-> 15-i
+// Max / sum over each row of 16 lanes (butterfly steps within the row); the row's result is
+// taken from one of its lanes.
+__device__ __forceinline__ float row16_max(float x) {
+  x = fmaxf(x, dpp16<kDppXor1>(x));
+  x = fmaxf(x, dpp16<kDppXor2>(x));
+  x = fmaxf(x, dpp16<kDppHalfMirror>(x));
+  return fmaxf(x, dpp16<kDppRowMirror>(x));
+}
+__device__ __forceinline__ float row16_sum(float x) {
+  x += dpp16<kDppXor1>(x);
+  x += dpp16<kDppXor2>(x);
+  x += dpp16<kDppHalfMirror>(x);
+  return x + dpp16<kDppRowMirror>(x);
+}
+
 // Wave-wide (m, s): the max first, then each lane's sum rescaled to it once and added up, so
-// the exponentials are independent rather than a chain of pairwise combines. The xor tree
-// gives every lane the same bits (each step adds the same two values in either order).
+// the exponentials are independent rather than a chain of pairwise combines. Rows of 16 lanes
+// reduce through DPP (a few cycles a step, where a cross-lane shuffle through the LDS crossbar
+// costs an LDS round trip); the first lanes of the four rows are read as wave-uniform values
+// and combined in a fixed order, so every lane returns the same bits. All 64 lanes must be
+// active.
 __device__ __forceinline__ void wave_lse_reduce(float& m, float& s) {
-  float M = m;
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
-  float t = s * fast_exp2((m - M) * kLog2e);
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) t += __shfl_xor(t, off, 64);
+  const float rm = row16_max(m);
+  const float M = fmaxf(fmaxf(lane_value(rm, 0), lane_value(rm, 16)),
+                        fmaxf(lane_value(rm, 32), lane_value(rm, 48)));
+  const float rs = row16_sum(s * fast_exp2((m - M) * kLog2e));
+  s = (lane_value(rs, 0) + lane_value(rs, 16)) + (lane_value(rs, 32) + lane_value(rs, 48));
   m = M;
-  s = t;
 }
 
 // Optimisation barrier: the register-resident row is "redefined" here, so the compiler cannot
@@ -707,7 +735,13 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
   };
   auto load_row = [&](__amdgpu_buffer_rsrc_t rs, __amdgpu_buffer_rsrc_t rr, const RowGeom& g,
                       uint32_t voff, int wid) {
-    static_for<NV>([&](auto I) { r[I] = bload(rr, voff + (uint32_t)(I * BLOCK * 16), 0u); });
+    // Issued in slot order (the fences keep the scheduler from sinking slot 0's load, whose
+    // address needs no add, below the others): loads return in order, so sweep 1 can fold
+    // slot i as soon as the first i+1 loads have landed instead of waiting for the whole row.
+    static_for<NV>([&](auto I) {
+      r[I] = bload(rr, voff + (uint32_t)(I * BLOCK * 16), 0u);
+      slot_fence();
+    });
     rp = bload(rs, rp_off(BLOCK, g, voff), 0u);
     // (unused LDS slots get out-of-range offsets rather than a branch, so every row issues
     // the same loads and the compiler's wait counts stay exact)
@@ -750,9 +784,6 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 
     const RowScalars rsc = cur;
     cur = fetch_row_scalars<EXT>(a, nrow);  // the next row's, for the next iteration
-    // the row after the next one: thread 0 draws it now and publishes it at the reduction
-    unsigned long long tk = 0ull;
-    if (kQueue && tid == 0) tk = atomicAdd(a.queue, 1ull);
     const bool valid = rsc.valid(V);
     const int y = valid ? (int)rsc.y : 0;
     const int vy = y / EPV, ey = y % EPV;
@@ -772,6 +803,17 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     const __amdgpu_buffer_rsrc_t nrr = reg_rsrc(nrow, nvalid, g);
 
     if (!PF) load_row(rs, rr, g, voff, wid);
+    // The row after the next one: thread 0 draws it now, behind the row's loads, and publishes
+    // it at the reduction. The queue pointer goes through a VGPR so that the compiler's atomic
+    // optimizer (which turns a uniform-address atomic into a wave scan and waits for its
+    // result on the spot, i.e. for every older store and load of the wave) leaves it alone:
+    // the result is first needed at the reduction, after the row's loads have landed anyway.
+    unsigned long long tk = 0ull;
+    if (kQueue && tid == 0) {
+      auto* q = (__attribute__((address_space(1))) unsigned long long*)a.queue;
+      asm volatile("" : "+v"(q));
+      tk = __hip_atomic_fetch_add(q, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
 
     // (Forward only with PF: sweep 1 is the row's last sweep, so each register is refilled with
     // the next row's vector right after it has been read.)
