@@ -10,7 +10,8 @@
 namespace cis {
 
 // Workspace layout (bytes), every array 256-byte aligned:
-//   [0, 256)  cis_stats_t
+//   [0, 256)     cis_stats_t
+//   [256, 1280)  the fused pass's row-queue counters, one per 128-byte line
 //   terms  float[T]   per-row loss term
 //   logk   float[T]   per-row log k (diagnostics)
 //   excess float[T]   per-row k - w (diagnostics)
@@ -23,9 +24,16 @@ namespace cis {
 // The last two exist only in the layout of the forward entry points (`seg`); the fused pass and
 // the LM-head path do not use them.
 constexpr size_t kStatsBytes = 256;
-// The row queue counter (8 bytes) sits in the stats block, after the cis_stats_t.
-constexpr size_t kQueueOff = 128;
-static_assert(sizeof(cis_stats_t) <= kQueueOff, "the row queue counter follows the statistics");
+static_assert(sizeof(cis_stats_t) <= kStatsBytes, "the statistics fit their block");
+// The row queue: up to kRowQueues counters of 8 bytes, each on a 128-byte line of its own.
+// Returning atomics on one line are served one at a time, about 80 M per second on this part,
+// which short rows approach (one draw per row); counters on separate lines are served in
+// parallel. Short rows use all of them, long rows one (with eight, the long-row workloads ran
+// 2-3% slower).
+constexpr int kRowQueues = 8;
+constexpr size_t kQueueOff = kStatsBytes;
+constexpr size_t kQueueStride = 128;
+constexpr size_t kHeadBytes = kQueueOff + kRowQueues * kQueueStride;
 // Segments per row at most in the split forward pass (the partials per row in the workspace).
 constexpr int kSegMax = 32;
 
@@ -48,7 +56,7 @@ struct WsLayout {
 constexpr WsLayout ws_layout(int64_t T, int64_t n_seq, bool seg = false) {
   const size_t f = align_up(4 * (size_t)T, 256), b = align_up((size_t)T, 256);
   WsLayout L{};
-  L.terms = kStatsBytes;
+  L.terms = kHeadBytes;
   L.logk = L.terms + f;
   L.excess = L.logk + f;
   L.wpre = L.excess + f;
@@ -177,9 +185,10 @@ struct RowArgs {
   const uint8_t* pflags_ws; // pre-pass acted bits[T]
   float* eps_out;           // nullable; rate-1 path only (the pre-pass writes it otherwise)
   float clip_low, clip_high;
-  // row queue of the row kernel: a workgroup's first two rows are blockIdx.x and
-  // blockIdx.x + gridDim.x, later ones 2*gridDim.x + the counter's old value. Cleared by
-  // queue_reset_kernel before every launch.
+  // row queue of the row kernel (up to kRowQueues counters, kQueueStride bytes apart): a
+  // workgroup's first two rows are blockIdx.x and blockIdx.x + gridDim.x; with n counters in
+  // use (kRowQueues for blocks of up to 512 threads, else 1), counter c hands out the later rows
+  // 2*gridDim.x + c + n*q, q = 0, 1, ... Cleared by queue_reset_kernel before every launch.
   unsigned long long* queue;
 };
 

@@ -152,10 +152,10 @@ const void* combine_kernel(bool ext, bool lane) {
   return lane ? (const void*)&cis_combine_lane_kernel<false> : (const void*)&cis_combine_kernel<false>;
 }
 
-// Clears the row kernel's queue counter ahead of each launch: a kernel rather than a memset, so
-// a captured call holds no memset node.
+// Clears the row kernel's queue counters ahead of each launch: a kernel rather than a memset,
+// so a captured call holds no memset node.
 __global__ __launch_bounds__(64) void cis_queue_reset_kernel(unsigned long long* q) {
-  if (threadIdx.x == 0) *q = 0ull;
+  if (threadIdx.x < kRowQueues) q[threadIdx.x * (kQueueStride / sizeof(*q))] = 0ull;
 }
 
 const void* finalize_kernel() { return (const void*)&cis_finalize_kernel; }

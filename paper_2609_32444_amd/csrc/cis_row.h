@@ -770,11 +770,33 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
   // The fused pass takes rows from a queue, so that workgroups that meet cheap rows (masked
   // ones) or run on a faster part of the chip take more of them: the first two rows of a
   // workgroup are fixed, every later one is drawn one row ahead of its use (the next row is
-  // needed at the top of a row, for its scalars and, with PF, its loads). The forward pass
-  // keeps the fixed stride: its long rows go to the split kernels, whose short-lived
-  // workgroups balance by themselves.
+  // needed at the top of a row, for its scalars and, with PF, its loads). Blocks of up to 512
+  // threads (short rows, one draw per row each) use kRowQueues counters on separate cache
+  // lines, since one counter serialises every draw; counter c hands out the rows congruent to
+  // c modulo kRowQueues in increasing order, workgroup b starts on counter b mod kRowQueues
+  // and, once its counter has run dry, moves on to the next. Longer rows draw from one counter
+  // (eight measured 0.5-3% slower there). The forward pass keeps the fixed stride: its long
+  // rows go to the split kernels, whose short-lived workgroups balance by themselves.
   constexpr bool kQueue = BWD;
   int64_t nrow = (int64_t)blockIdx.x + gridDim.x;
+  constexpr uint32_t qshift = BLOCK <= 512 ? 3 : 0;
+  static_assert((1 << 3) == kRowQueues, "short rows use every counter");
+  constexpr uint64_t qmask = (1ull << qshift) - 1;
+  // thread 0's counter, kept 64-bit: with a 32-bit index, the 64-bit ticket arithmetic below
+  // was compiled with an uninitialised high half for it
+  uint64_t qc = blockIdx.x & qmask;
+  auto draw = [&](uint64_t c) -> unsigned long long {
+    // The pointer goes through a VGPR so that the compiler's atomic optimizer (which turns a
+    // uniform-address atomic into a wave scan and waits for its result on the spot, i.e. for
+    // every older load and store of the wave) leaves it alone.
+    auto* q = (__attribute__((address_space(1))) unsigned long long*)a.queue +
+              c * (kQueueStride / sizeof(unsigned long long));
+    asm volatile("" : "+v"(q));
+    return __hip_atomic_fetch_add(q, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  };
+  auto ticket_row = [&](unsigned long long t, uint64_t c) -> int64_t {
+    return (int64_t)(2 * (uint64_t)gridDim.x + c + (t << qshift));
+  };
   for (int64_t row = blockIdx.x; row < a.T;) {
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
@@ -803,17 +825,11 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     const __amdgpu_buffer_rsrc_t nrr = reg_rsrc(nrow, nvalid, g);
 
     if (!PF) load_row(rs, rr, g, voff, wid);
-    // The row after the next one: thread 0 draws it now, behind the row's loads, and publishes
-    // it at the reduction. The queue pointer goes through a VGPR so that the compiler's atomic
-    // optimizer (which turns a uniform-address atomic into a wave scan and waits for its
-    // result on the spot, i.e. for every older store and load of the wave) leaves it alone:
-    // the result is first needed at the reduction, after the row's loads have landed anyway.
+    // The row after the next one: thread 0 draws a ticket now, behind the row's loads, and
+    // publishes its row at the reduction (the result is first needed there, after the row's
+    // loads have landed anyway).
     unsigned long long tk = 0ull;
-    if (kQueue && tid == 0) {
-      auto* q = (__attribute__((address_space(1))) unsigned long long*)a.queue;
-      asm volatile("" : "+v"(q));
-      tk = __hip_atomic_fetch_add(q, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    if (kQueue && tid == 0) tk = draw(qc);
 
     // (Forward only with PF: sweep 1 is the row's last sweep, so each register is refilled with
     // the next row's vector right after it has been read.)
@@ -968,18 +984,25 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     float coef = 0.f, b2 = INFINITY, one_m_p = 0.f;
     // (at least one barrier per row, valid or not, so that the double-buffered shared values
     // of row n are read before row n + 2 writes them)
-    if (kQueue && NW > 1 && tid == 0) sh_q[buf] = tk;
+    // The drawn row; a counter that has run dry sends thread 0 to the next one (a draw waited
+    // for at once, at the end of the pass only). A row >= T after every counter ends the loop.
+    uint64_t nq = 0;
+    if (kQueue && tid == 0) {
+      asm volatile("" : "+v"(tk));  // keeps the arithmetic on the ticket (and its wait) here
+      int64_t r = ticket_row(tk, qc);
+      for (uint64_t k = 1; k <= qmask && r >= a.T; ++k) {
+        qc = (qc + 1) & qmask;
+        r = ticket_row(draw(qc), qc);
+      }
+      nq = (uint64_t)r;
+      if (NW > 1) sh_q[buf] = nq;
+    }
     auto drawn = [&]() -> int64_t {
       if (!kQueue) return nrow + gridDim.x;
-      unsigned long long q;
-      if (NW > 1) {
-        q = sh_q[buf];
-      } else {
-        const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)tk);
-        const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(tk >> 32));
-        q = ((unsigned long long)hi << 32) | lo;
-      }
-      return (int64_t)q + 2 * (int64_t)gridDim.x;
+      if (NW > 1) return (int64_t)sh_q[buf];
+      const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)nq);
+      const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(nq >> 32));
+      return (int64_t)(((uint64_t)hi << 32) | lo);
     };
     int64_t nn;
     if (valid) {

@@ -73,8 +73,11 @@ def test_long_rows_many_per_workgroup(V, dtype):
 
 # Fused-pass rows come from a queue once every workgroup has had two rows. The row counts put
 # thousands of rows in the queue for the one-wave, 512-thread, 1024-thread and LDS variants
-# (resident grids of up to 7168, 768, 256 and 256 workgroups).
-@pytest.mark.parametrize("V,T", [(1000, 20000), (32768, 4096), (151936, 1500), (250001, 700)])
+# (resident grids of up to 7168, 768, 256 and 256 workgroups). The queue is eight counters, each
+# handing out every eighth row; 515 and 517 rows of 151936 leave 3 and 5 queued rows on a grid
+# of 256, so most counters are empty from the start and the workgroups on them must move on.
+@pytest.mark.parametrize("V,T", [(1000, 20000), (32768, 4096), (151936, 1500), (250001, 700),
+                                 (151936, 515), (151936, 517)])
 def test_row_queue_and_stale_workspace(V, T):
     """The workspace starts as all 0xFF bytes: as the row queue's counter that would hand out
     no queued row at all, so the call must clear it itself. Every row (15% masked) against the
