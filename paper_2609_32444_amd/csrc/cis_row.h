@@ -768,9 +768,13 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 
   RowScalars cur = fetch_row_scalars<EXT>(a, blockIdx.x);
   // The fused pass takes rows from a queue, so that workgroups that meet cheap rows (masked
-  // ones) or run on a faster part of the chip take more of them: the first two rows of a
-  // workgroup are fixed, every later one is drawn one row ahead of its use (the next row is
-  // needed at the top of a row, for its scalars and, with PF, its loads). Blocks of up to 512
+  // ones) or run on a faster part of the chip take more of them: the first three rows of a
+  // workgroup are fixed, every later one is drawn as a ticket at the start of the gradient
+  // sweep two rows before its use and turned into a row at the next row's reduction (the next
+  // row is needed at the top of a row, for its scalars and, with PF, its loads). gfx9 counts
+  // loads, stores and atomics in one in-order vmcnt, so waiting for a ticket also waits for
+  // every memory operation issued before it: drawn ahead of the row's stores, it lets a masked
+  // row (stores only) proceed while the previous row's stores are still in flight. Blocks of up to 512
   // threads (short rows, one draw per row each) use kRowQueues counters on separate cache
   // lines, since one counter serialises every draw; counter c hands out the rows congruent to
   // c modulo kRowQueues in increasing order, workgroup b starts on counter b mod kRowQueues
@@ -779,6 +783,8 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
   // rows go to the split kernels, whose short-lived workgroups balance by themselves.
   constexpr bool kQueue = BWD;
   int64_t nrow = (int64_t)blockIdx.x + gridDim.x;
+  bool first = true;             // the first row publishes the workgroup's third, fixed row
+  unsigned long long tk = 0ull;  // thread 0's ticket, drawn in the previous row's gradient sweep
   constexpr uint32_t qshift = BLOCK <= 512 ? 3 : 0;
   static_assert((1 << 3) == kRowQueues, "short rows use every counter");
   constexpr uint64_t qmask = (1ull << qshift) - 1;
@@ -795,7 +801,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     return __hip_atomic_fetch_add(q, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   };
   auto ticket_row = [&](unsigned long long t, uint64_t c) -> int64_t {
-    return (int64_t)(2 * (uint64_t)gridDim.x + c + (t << qshift));
+    return (int64_t)(3 * (uint64_t)gridDim.x + c + (t << qshift));
   };
   for (int64_t row = blockIdx.x; row < a.T;) {
     int tid = threadIdx.x;
@@ -825,11 +831,6 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     const __amdgpu_buffer_rsrc_t nrr = reg_rsrc(nrow, nvalid, g);
 
     if (!PF) load_row(rs, rr, g, voff, wid);
-    // The row after the next one: thread 0 draws a ticket now, behind the row's loads, and
-    // publishes its row at the reduction (the result is first needed there, after the row's
-    // loads have landed anyway).
-    unsigned long long tk = 0ull;
-    if (kQueue && tid == 0) tk = draw(qc);
 
     // (Forward only with PF: sweep 1 is the row's last sweep, so each register is refilled with
     // the next row's vector right after it has been read.)
@@ -984,15 +985,20 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     float coef = 0.f, b2 = INFINITY, one_m_p = 0.f;
     // (at least one barrier per row, valid or not, so that the double-buffered shared values
     // of row n are read before row n + 2 writes them)
-    // The drawn row; a counter that has run dry sends thread 0 to the next one (a draw waited
-    // for at once, at the end of the pass only). A row >= T after every counter ends the loop.
+    // The row after the next one: the workgroup's third row, or the row of the ticket drawn
+    // in the previous row's gradient sweep; a counter that has run dry sends thread 0 to the
+    // next one (a draw waited for at once, at the end of the pass only). A row >= T after
+    // every counter ends the loop.
     uint64_t nq = 0;
     if (kQueue && tid == 0) {
-      asm volatile("" : "+v"(tk));  // keeps the arithmetic on the ticket (and its wait) here
-      int64_t r = ticket_row(tk, qc);
-      for (uint64_t k = 1; k <= qmask && r >= a.T; ++k) {
-        qc = (qc + 1) & qmask;
-        r = ticket_row(draw(qc), qc);
+      int64_t r = (int64_t)blockIdx.x + 2 * (int64_t)gridDim.x;
+      if (!first) {
+        asm volatile("" : "+v"(tk));  // keeps the arithmetic on the ticket (and its wait) here
+        r = ticket_row(tk, qc);
+        for (uint64_t k = 1; k <= qmask && r >= a.T; ++k) {
+          qc = (qc + 1) & qmask;
+          r = ticket_row(draw(qc), qc);
+        }
       }
       nq = (uint64_t)r;
       if (NW > 1) sh_q[buf] = nq;
@@ -1058,24 +1064,38 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     // Every vector is stored through the write descriptor (which drops the partial last vector
     // and out-of-range lanes); the partial last vector is then written element by element, and
     // finally the sampled element is overwritten with coef*(1-p) by the thread that stored its
-    // vector (same-thread program order). Invalid rows store zeros: their register slots and
-    // rp were loaded through empty descriptors (zeros) and their b2 is +inf, so the same
-    // arithmetic gives exp2(-inf) = 0 without a branch.
+    // vector (same-thread program order). Invalid rows store zeros without reading their
+    // register slots, so their stores wait for no load (nor, through the in-order vmcnt, for
+    // the previous row's stores).
     if (BWD) {
+      // the ticket of the row after next, drawn ahead of this row's stores
+      if (kQueue && tid == 0) tk = draw(qc);
+      slot_fence();
       const uint32_t sgn = coef > 0.f ? GO::kSign : 0u;
-      static_for<NV>([&](auto I) {
-        constexpr int i = I;
-        const uint32_t o = voff + (uint32_t)(i * BLOCK * 16);
-        const typename GO::vec out = GO::make(r[i], b2, sgn);
-        if (PF) r[i] = bload(nrr, o + after(out), 0u);
-        GO::store(out, wr, o);
-        slot_fence();
-      });
-      {
+      if (valid) {
+        static_for<NV>([&](auto I) {
+          constexpr int i = I;
+          const uint32_t o = voff + (uint32_t)(i * BLOCK * 16);
+          const typename GO::vec out = GO::make(r[i], b2, sgn);
+          if (PF) r[i] = bload(nrr, o + after(out), 0u);
+          GO::store(out, wr, o);
+          slot_fence();
+        });
         const uint32_t o = rp_off(BLOCK, g, voff);
         const typename GO::vec out = GO::make(rp, b2, sgn);
         if (PF) rp = bload(nrs, o + after(out), 0u);
         GO::store(out, ws, o);
+      } else {
+        static_for<NV>([&](auto I) {
+          constexpr int i = I;
+          const uint32_t o = voff + (uint32_t)(i * BLOCK * 16);
+          if (PF) r[i] = bload(nrr, o, 0u);
+          GO::store(GO::zero(), wr, o);
+          slot_fence();
+        });
+        const uint32_t o = rp_off(BLOCK, g, voff);
+        if (PF) rp = bload(nrs, o, 0u);
+        GO::store(GO::zero(), ws, o);
       }
       static_for<NL>([&](auto K) {
         constexpr int k = K;
@@ -1108,6 +1128,7 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     }
     row = nrow;
     nrow = nn;
+    first = false;
   }
 }
 
