@@ -774,18 +774,19 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
   // row is needed at the top of a row, for its scalars and, with PF, its loads). gfx9 counts
   // loads, stores and atomics in one in-order vmcnt, so waiting for a ticket also waits for
   // every memory operation issued before it: drawn ahead of the row's stores, it lets a masked
-  // row (stores only) proceed while the previous row's stores are still in flight. Blocks of up to 512
-  // threads (short rows, one draw per row each) use kRowQueues counters on separate cache
-  // lines, since one counter serialises every draw; counter c hands out the rows congruent to
-  // c modulo kRowQueues in increasing order, workgroup b starts on counter b mod kRowQueues
-  // and, once its counter has run dry, moves on to the next. Longer rows draw from one counter
-  // (eight measured 0.5-3% slower there). The forward pass keeps the fixed stride: its long
-  // rows go to the split kernels, whose short-lived workgroups balance by themselves.
+  // row (stores only) proceed while the previous row's stores are still in flight. Short rows
+  // (blocks of up to 512 threads, or up to 4 slots per thread) draw at a high rate and use
+  // kRowQueues counters on separate cache lines, since one counter serialises every draw;
+  // counter c hands out the rows congruent to c modulo kRowQueues in increasing order,
+  // workgroup b starts on counter b mod kRowQueues and, once its counter has run dry, moves on
+  // to the next. Longer rows draw from one counter (eight measured 0.5-3.5% slower there). The
+  // forward pass keeps the fixed stride: its long rows go to the split kernels, whose
+  // short-lived workgroups balance by themselves.
   constexpr bool kQueue = BWD;
   int64_t nrow = (int64_t)blockIdx.x + gridDim.x;
   bool first = true;             // the first row publishes the workgroup's third, fixed row
   unsigned long long tk = 0ull;  // thread 0's ticket, drawn in the previous row's gradient sweep
-  constexpr uint32_t qshift = BLOCK <= 512 ? 3 : 0;
+  constexpr uint32_t qshift = (BLOCK <= 512 || NV <= 3) ? 3 : 0;
   static_assert((1 << 3) == kRowQueues, "short rows use every counter");
   constexpr uint64_t qmask = (1ull << qshift) - 1;
   // thread 0's counter, kept 64-bit: with a 32-bit index, the 64-bit ticket arithmetic below
@@ -1148,13 +1149,14 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 // fewer slots per thread than the forward pass, prefetches the next row during the gradient
 // sweep only on short rows (on long ones it costs more than it hides), and adds 9 LDS slots
 // (144 KiB) for rows beyond its registers. The fp32 forward kernel stops at 15 slots (18
-// would spill the prefetched row to scratch). Once the fused pass took its rows from a queue,
-// 512 x 7 overtook 256 x 15 for rows of up to 4096 vectors (V = 32768 in bf16: 0.676 against
-// 0.684 ms; 1024 x 3: 0.747).
+// would spill the prefetched row to scratch). For rows of up to 4096 vectors (V = 32768 in
+// bf16) 1024 x 3 without the prefetch took over once loads were issued in slot order and the
+// queue tickets were drawn ahead of the stores: 0.625 ms against 0.635 for 512 x 7 without and
+// 0.657 with the prefetch, 0.658 for 256 x 15 with it and 0.677 without.
 #define CIS_BWD_TABLE_OUT(E, EO)                                                            \
   {CIS_VO(E, EO, 64, 1, 0, true),     CIS_VO(E, EO, 64, 3, 0, true),                        \
    CIS_VO(E, EO, 64, 7, 0, true),     CIS_VO(E, EO, 64, 15, 0, true),                       \
-   CIS_VO(E, EO, 512, 3, 0, false),   CIS_VO(E, EO, 512, 7, 0, true),                       \
+   CIS_VO(E, EO, 512, 3, 0, false),   CIS_VO(E, EO, 1024, 3, 0, false),                    \
    CIS_VO(E, EO, 1024, 7, 0, false),  CIS_VO(E, EO, 1024, 11, 0, false),                    \
    CIS_VO(E, EO, 1024, 15, 0, false), CIS_VO(E, EO, 1024, 18, 0, false),                    \
    CIS_VO(E, EO, 1024, 18, 9, false)}
