@@ -97,7 +97,7 @@ typedef struct cis_stats {
 } cis_stats_t;
 
 /* Bytes of device workspace cis_loss_fwd/_bwd and cis_weights_ex (without sequence
- * operators) need for T rows (T >= 0). The workspace holds the cis_stats_t, the counter of
+ * operators) need for T rows (T >= 0). The workspace holds the cis_stats_t, the counters of
  * the fused pass's row queue (which each call clears with a kernel of its own before the rows
  * start) and per-row scratch: loss terms, flags and diagnostics, and for the forward pass the
  * partial sums of up to 32 segments per row (274 bytes per row in all); its previous contents
