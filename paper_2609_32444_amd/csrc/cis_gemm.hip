@@ -379,10 +379,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t
   // a fragment row is a multiple of 16 plus lane % 16, so its swizzle is lane & 7
   const int fr = lane & 15, fq = lane >> 4, sw = lane & 7;
   if (nk > 0) issue(0);
+  // (the ids were requested before the first slab, so this waits for them alone; the first
+  // slab's barrier makes them visible, and a loop free of first-iteration code keeps the
+  // compiler from peeling it into a copy that spills)
+  if (EPI == kEpiLse && tid < kGemmTile) er.y[tid] = (ey >= 0 && ey < g.N) ? (int)ey : -1;
   for (int64_t kt = 0; kt < nk; ++kt) {
     wait_vmcnt<0>();  // this wave's part of slab kt is in LDS
-    if (EPI == kEpiLse && kt == 0 && tid < kGemmTile)
-      er.y[tid] = (ey >= 0 && ey < g.N) ? (int)ey : -1;
     lds_barrier();    // every wave's is, and every wave is done with slab kt - 1's buffer
     if (kt + 1 < nk) issue(kt + 1);
     const __bf16* st = lds + (int)(kt & 1) * kSlab;
