@@ -144,7 +144,6 @@ int launch_seq_sum(const float* lp, const float* lq, const uint8_t* mask, const 
 // family / decoupled path); the base entry points pass the CIS operator with ext = false.
 struct LossCall {
   bool bwd, ext;
-  bool bf16_grad;           // float32 logits, bf16 gradient (LM-head path)
   const void* logits;
   int dtype;
   int64_t T, V, ld;
@@ -220,13 +219,12 @@ P* at(P* p, int64_t t0) { return p ? p + t0 : nullptr; }
 cis::RowArgs row_args(const LossCall& c, const Ws& ws, const void* logits, void* dlogits,
                       int64_t ld, int64_t ld_g, int64_t t0, int64_t rows) {
   const int esize = c.dtype == CIS_BF16 ? 2 : 4;
-  const int gsize = c.bf16_grad ? 2 : esize;
   const int32_t nvec = (int32_t)((c.V + 16 / esize - 1) / (16 / esize));
   cis::RowArgs ra{};
   ra.logits = logits;
   ra.dlogits = dlogits;
   ra.row_bytes = ld * esize;
-  ra.grow_bytes = c.bwd ? ld_g * gsize : 0;
+  ra.grow_bytes = c.bwd ? ld_g * esize : 0;
   ra.ids = c.ids + t0;
   ra.logp_infer = c.logp_infer + t0;
   ra.adv = c.adv + t0;
@@ -276,9 +274,8 @@ int launch_rows(const LossCall& c, const Ws& ws, const void* logits, void* dlogi
   if (rows <= 0) return CIS_OK;
   cis::RowArgs ra = row_args(c, ws, logits, dlogits, ld, ld_g, t0, rows);
   const int32_t nvec = ra.nvec;
-  const cis::RowVariant& var = c.ext
-                                   ? cis::select_row_variant_ext(c.dtype, c.bwd, nvec, c.bf16_grad)
-                                   : cis::select_row_variant(c.dtype, c.bwd, nvec);
+  const cis::RowVariant& var = c.ext ? cis::select_row_variant_ext(c.dtype, c.bwd, nvec)
+                                     : cis::select_row_variant(c.dtype, c.bwd, nvec);
   // forward pass over long rows: segment kernel + combine (when the workspace has the room)
   const cis::SegVariant* sv =
       (!c.bwd && ws.L.seg) ? cis::select_seg_variant(c.dtype, nvec) : nullptr;
@@ -463,7 +460,8 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
 
   if (bwd && T > 0) {  // W^T once: the operand of dL/dh = G W with V as the contracted axis
     if (int rc = ok(cis::launch_transpose(
-            cis::TransposeArgs{m.weight, Wt, nullptr, V, H, m.ld_w, LM.ldv, 0}, false, stream)))
+            cis::TransposeArgs{m.weight, Wt, nullptr, V, H, m.ld_w, LM.ldv, 0, nullptr}, false,
+            stream)))
       return rc;
   }
   if (T > 0 && c.logp_old) {
@@ -474,51 +472,52 @@ int run_lmhead(const LmHeadCall& m, hipStream_t stream) {
     const int64_t tc = T - t0 < m.chunk ? T - t0 : m.chunk;
     const int64_t g0 = t0 / group * group;  // first row of this chunk's dL/dW group
     const __bf16* hc = hid + t0 * m.ld_h;
+    // The logits product's epilogue leaves per row and 64-column block a (max, exp-sum) pair
+    // (and the sampled logit); the combine folds a row's pairs in column order, runs the loss
+    // epilogue and, for the backward, writes the row's gradient parameters. The default
+    // backward also stores the chunk's logits in float32 and forms G and G^T from them in one
+    // tiled pass; the forward, and the backward with `recompute`, never store them (the
+    // backward forms the product a second time, with an epilogue that writes G).
+    cis::GemmArgs ga = cis::gemm_args(hc, m.weight, LM.fused ? nullptr : Z, tc, V, H, m.ld_h,
+                                      m.ld_w, LM.fused ? 0 : LM.ldz);
+    ga.epi = LM.fused ? cis::kEpiLse : cis::kEpiLseStore;
+    ga.e.ids = c.ids + t0;
+    ga.e.part = reinterpret_cast<float2*>(base + LM.tpart);
+    ga.e.ldp = LM.ntv;
+    ga.e.zy = reinterpret_cast<float*>(base + LM.tzy);
+    if (int rc = ok(cis::launch_gemm_epi(ga, queue, ncu, stream))) return rc;
+    cis::RowArgs ra = row_args(c, ws, nullptr, nullptr, 0, 0, t0, tc);
+    cis::SegArgs sa{};
+    sa.part = ga.e.part;
+    sa.zy = ga.e.zy;
+    sa.nseg = (int32_t)LM.ntv;
+    sa.stride = LM.ntv;
+    sa.gp = bwd ? reinterpret_cast<cis::GradParams*>(base + LM.tgp) : nullptr;
+    if (int rc = launch_combine(c, ra, sa, tc, stream)) return rc;
+    if (!bwd) continue;
     if (LM.fused) {
-      // the logits h_c W^T are never stored: the product's epilogue leaves per row and
-      // 256-column tile a (max, exp-sum) pair, the combine folds them and runs the loss
-      // epilogue, and the backward forms the product again with an epilogue that writes G
-      cis::GemmArgs ga = cis::gemm_args(hc, m.weight, nullptr, tc, V, H, m.ld_h, m.ld_w, 0);
-      ga.epi = cis::kEpiLse;
-      ga.e.ids = c.ids + t0;
-      ga.e.part = reinterpret_cast<float2*>(base + LM.tpart);
-      ga.e.ldp = LM.ntv;
-      ga.e.zy = reinterpret_cast<float*>(base + LM.tzy);
-      if (int rc = ok(cis::launch_gemm_epi(ga, queue, ncu, stream))) return rc;
-      cis::RowArgs ra = row_args(c, ws, nullptr, nullptr, 0, 0, t0, tc);
-      cis::SegArgs sa{};
-      sa.part = ga.e.part;
-      sa.zy = ga.e.zy;
-      sa.nseg = (int32_t)LM.ntv;
-      sa.stride = LM.ntv;
-      sa.gp = bwd ? reinterpret_cast<cis::GradParams*>(base + LM.tgp) : nullptr;
-      if (int rc = launch_combine(c, ra, sa, tc, stream)) return rc;
-      if (!bwd) continue;
       ga.epi = cis::kEpiGrad;
       ga.e.gp = sa.gp;
       ga.e.G = Gb;
       ga.e.ldg = LM.ldv;
       if (int rc = ok(cis::launch_gemm_epi(ga, queue, ncu, stream))) return rc;
+      // G^T (operand of dL/dW) into the group's columns t0 - g0 ..
+      if (int rc = ok(cis::launch_transpose(
+              cis::TransposeArgs{Gb, Gt + (t0 - g0), nullptr, tc, V, LM.ldv, LM.ldc, 0, nullptr},
+              false, stream)))
+        return rc;
     } else {
-      // Z = h_c W^T (float32 logits of the chunk)
-      if (int rc = ok(cis::launch_gemm_nt(
-              cis::gemm_args(hc, m.weight, Z, tc, V, H, m.ld_h, m.ld_w, LM.ldz), false, nullptr,
-              queue, ncu, stream)))
+      // G = dL/dz in bf16 (operand of dL/dh) and G^T (operand of dL/dW, the group's columns
+      // t0 - g0 ..) from the stored logits
+      if (int rc = ok(cis::launch_transpose(
+              cis::TransposeArgs{Z, Gt + (t0 - g0), Gb, tc, V, LM.ldz, LM.ldc, LM.ldv, sa.gp},
+              true, stream)))
         return rc;
-      // loss rows; the backward writes G = dL/dz in bf16 (the operand of dL/dh)
-      if (int rc = launch_rows(c, ws, Z, bwd ? Gb : nullptr, LM.ldz, LM.ldv, t0, tc, dev, info,
-                               stream))
-        return rc;
-      if (!bwd) continue;
     }
-    // G^T and h_c^T (operands of dL/dW) into the group's columns t0 - g0 ..
+    // h_c^T (operand of dL/dW)
     if (int rc = ok(cis::launch_transpose(
-            cis::TransposeArgs{Gb, Gt + (t0 - g0), nullptr, tc, V, LM.ldv, LM.ldc, 0}, false,
-            stream)))
-      return rc;
-    if (int rc = ok(cis::launch_transpose(
-            cis::TransposeArgs{hc, Ht + (t0 - g0), nullptr, tc, H, m.ld_h, LM.ldc, 0}, false,
-            stream)))
+            cis::TransposeArgs{hc, Ht + (t0 - g0), nullptr, tc, H, m.ld_h, LM.ldc, 0, nullptr},
+            false, stream)))
       return rc;
     // dL/dh_c = G W = G (W^T)^T
     if (int rc = ok(cis::launch_gemm_nt(
@@ -604,7 +603,6 @@ LmHeadCall lm_call(bool bwd, const void* hidden, int64_t T, int64_t H, int64_t l
   m.loss = ext_call(bwd, nullptr, CIS_F32, T, V, 0, ids, logp_infer, logp_old, adv, mask, offsets,
                     n_seq, params, nullptr, 0, logp_train_out, w_out, acted_out, terms_out,
                     eps_out, loss_out, workspace, workspace_bytes);
-  m.loss.bf16_grad = true;
   m.hidden = hidden;
   m.weight = weight;
   m.H = H;

@@ -8,12 +8,15 @@
 
 namespace cis {
 
-// Epilogues of the logits product z = h W^T of a row chunk (A = h, B = W), which never store z:
-//   kEpiLse:  per row and 64-column block (4 per 256-column tile tn), the pair (max, sum of
-//             exp(z - max) leaving out the sampled column) into part[row * ldp + 4 tn + wn],
-//             and the sampled logit into zy[row];
-//   kEpiGrad: dL/dz of the row from its GradParams, rounded to bf16, into G[row * ldg + col].
-enum { kEpiStore = 0, kEpiLse = 1, kEpiGrad = 2 };
+// Epilogues of the logits product z = h W^T of a row chunk (A = h, B = W):
+//   kEpiLse:      per row and 64-column block (4 per 256-column tile tn), the pair (max, sum
+//                 of exp(z - max) leaving out the sampled column) into
+//                 part[row * ldp + 4 tn + wn], and the sampled logit into zy[row]; z itself
+//                 is not stored;
+//   kEpiGrad:     dL/dz of the row from its GradParams, rounded to bf16, into
+//                 G[row * ldg + col];
+//   kEpiLseStore: kEpiLse, and z into C (float32) as kEpiStore does.
+enum { kEpiStore = 0, kEpiLse = 1, kEpiGrad = 2, kEpiLseStore = 3 };
 struct GemmEpi {
   const int64_t* ids;       // [M] sampled ids (kEpiLse)
   float2* part;             // [M, ldp] (kEpiLse)
@@ -60,14 +63,17 @@ inline GemmArgs gemm_args(const void* A, const void* B, float* C, int64_t M, int
   return g;
 }
 
-// out[c][r] = bf16(in[r][c]), in R x C (float32 or bf16, row stride ldi), out C x R (ldo);
-// out_n (nullable) receives bf16(in) in the input's layout (row stride ldn). Row strides are
-// multiples of 4 elements and bases 16-byte aligned.
+// out[c][r] = bf16(f(in[r][c])), in R x C (float32 or bf16, row stride ldi), out C x R (ldo);
+// out_n (nullable) receives bf16(f(in)) in the input's layout (row stride ldn). f is the
+// identity, or with gp (float32 input only) the loss gradient of logit in[r][c] from row r's
+// GradParams (the kEpiGrad formula). Row strides are multiples of 4 elements and bases
+// 16-byte aligned.
 struct TransposeArgs {
   const void* in;
   void* out;
   void* out_n;
   int64_t R, C, ldi, ldo, ldn;
+  const GradParams* gp;
 };
 
 constexpr int kGemmTile = 256;      // C tile per workgroup (rows and columns)
@@ -91,8 +97,8 @@ int64_t gemm_splitk_count(int64_t M, int64_t N, int64_t K, int num_cu);
 // by whichever workgroup takes it.
 hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int* queue, int num_cu,
                           hipStream_t stream);
-// The logits product of a row chunk with a row-loss epilogue (kEpiLse or kEpiGrad; no split-K,
-// no C): M rows of h, N = V columns of W.
+// The logits product of a row chunk with a row-loss epilogue (kEpiLse, kEpiGrad or
+// kEpiLseStore; no split-K; C only with kEpiLseStore): M rows of h, N = V columns of W.
 hipError_t launch_gemm_epi(GemmArgs g, int* queue, int num_cu, hipStream_t stream);
 hipError_t launch_transpose(TransposeArgs t, bool in_f32, hipStream_t stream);
 

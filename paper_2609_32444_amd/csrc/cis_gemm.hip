@@ -259,8 +259,15 @@ __device__ __forceinline__ void lse_tile(const GemmArgs& g, const f32x4 (&acc)[k
   }
 }
 
-// Row-loss epilogue kEpiGrad: g = -coef exp(z - lse), evaluated as +-exp2(z log2(e) - b2),
-// and coef (1 - p) at the sampled column, rounded to bf16 (nearest even) into G.
+// dL/dz of logit z in column n of a row with parameters p: -coef exp(z - lse), evaluated as
+// +-exp2(z log2(e) - b2), and coef (1 - p) at the sampled column; 0 for a row without gradient.
+__device__ __forceinline__ float grad_value(const GradParams& p, float z, int64_t n) {
+  const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(z, kLog2e, -p.b2));
+  return p.y < 0 ? 0.f : ((n == p.y) ? p.gy : (p.neg ? -x : x));
+}
+
+// Row-loss epilogue kEpiGrad: grad_value of every logit of the tile, rounded to bf16 (nearest
+// even) into G.
 __device__ __forceinline__ void grad_tile(const GemmArgs& g, const f32x4 (&acc)[kTm][kTn],
                                           int64_t m0, int64_t n0) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -283,10 +290,7 @@ __device__ __forceinline__ void grad_tile(const GemmArgs& g, const f32x4 (&acc)[
       const int64_t n = n0 + wn * kGemmWaveN + j * 16 + 4 * fq;
       float v[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][e], kLog2e, -p.b2));
-        v[e] = p.y < 0 ? 0.f : ((n + e == p.y) ? p.gy : (p.neg ? -x : x));
-      }
+      for (int e = 0; e < 4; ++e) v[e] = grad_value(p, acc[i][j][e], n + e);
       const bf16x4 o = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
       if (n + 3 < g.N) {
         *(bf16x4*)(grow + n) = o;
@@ -373,16 +377,17 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t
 
   // the epilogue's per-row inputs: requested now, stored to LDS once the first slab has landed
   const int64_t mrow = m0 + tid;
-  const bool erow = EPI != kEpiStore && tid < kGemmTile && mrow < g.M;
+  constexpr bool kLse = EPI == kEpiLse || EPI == kEpiLseStore;
+  const bool erow = kLse && tid < kGemmTile && mrow < g.M;
   int64_t ey = -1;
-  if (EPI == kEpiLse && erow) ey = g.e.ids[mrow];
+  if (erow) ey = g.e.ids[mrow];
   // a fragment row is a multiple of 16 plus lane % 16, so its swizzle is lane & 7
   const int fr = lane & 15, fq = lane >> 4, sw = lane & 7;
   if (nk > 0) issue(0);
   // (the ids were requested before the first slab, so this waits for them alone; the first
   // slab's barrier makes them visible, and a loop free of first-iteration code keeps the
   // compiler from peeling it into a copy that spills)
-  if (EPI == kEpiLse && tid < kGemmTile) er.y[tid] = (ey >= 0 && ey < g.N) ? (int)ey : -1;
+  if (kLse && tid < kGemmTile) er.y[tid] = (ey >= 0 && ey < g.N) ? (int)ey : -1;
   for (int64_t kt = 0; kt < nk; ++kt) {
     wait_vmcnt<0>();  // this wave's part of slab kt is in LDS
     lds_barrier();    // every wave's is, and every wave is done with slab kt - 1's buffer
@@ -394,15 +399,15 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t
               [&](int j, int s) { return lb + j * 16 * BK + ((4 * s + fq) ^ sw) * 8; });
   }
 
-  if (EPI == kEpiLse) {
+  if (kLse) {
     if (n0 + kGemmTile <= g.N)
       lse_tile<true>(g, acc, m0, n0, tn, er.y);
     else
       lse_tile<false>(g, acc, m0, n0, tn, er.y);
-  } else if (EPI == kEpiGrad) {
-    grad_tile(g, acc, m0, n0);
   }
-  else
+  if (EPI == kEpiGrad)
+    grad_tile(g, acc, m0, n0);
+  else if (EPI == kEpiStore || EPI == kEpiLseStore)
     store_tile<BETA>(g, acc, m0, n0, split);
 }
 
@@ -454,10 +459,11 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const ReduceArgs r) 
   }
 }
 
-// out[c][r] = bf16(in[r][c]) for an R x C matrix (row strides ldi, ldo), and optionally
-// out_n[r][c] = bf16(in[r][c]) (row stride ldn): 64 x 64 tiles through LDS, every global access
-// row-contiguous (four elements per thread).
-template <class TI>
+// out[c][r] = bf16(f(in[r][c])) for an R x C matrix (row strides ldi, ldo), and optionally
+// out_n[r][c] = bf16(f(in[r][c])) (row stride ldn): 64 x 64 tiles through LDS, every global
+// access row-contiguous (four elements per thread). GRAD: f is grad_value with row r's
+// GradParams (the loss gradient of stored float32 logits), else the identity.
+template <class TI, bool GRAD = false>
 __global__ __launch_bounds__(256) void transpose_kernel(const TransposeArgs t) {
   __shared__ float tile[64][65];
   const TI* in = static_cast<const TI*>(t.in);
@@ -484,6 +490,11 @@ __global__ __launch_bounds__(256) void transpose_kernel(const TransposeArgs t) {
       } else {
         for (int e = 0; e < 4; ++e)
           if (c + e < t.C) v[e] = (float)src[e];
+      }
+      if constexpr (GRAD) {
+        const GradParams gp = t.gp[r];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = grad_value(gp, v[e], c + e);
       }
       if (outn) {
         __bf16* dst = outn + r * t.ldn + c;
@@ -539,7 +550,7 @@ hipError_t launch_gemm_epi(GemmArgs g, int* queue, int num_cu, hipStream_t strea
   g.m_fastest = g.M <= g.N;
   g.k_split = g.K > 0 ? g.K : 1;
   g.c_split_stride = 0;
-  g.c_vec = false;
+  g.c_vec = g.epi == kEpiLseStore && ((uintptr_t)g.C % 16 == 0) && g.ldc % 4 == 0;
   const int64_t mt = (g.M + kGemmTile - 1) / kGemmTile, nt = (g.N + kGemmTile - 1) / kGemmTile;
   g.units = mt * nt;
   g.queue = g.units > num_cu ? queue : nullptr;
@@ -550,12 +561,23 @@ hipError_t launch_gemm_epi(GemmArgs g, int* queue, int num_cu, hipStream_t strea
       return e;
   }
   const int64_t grid = g.queue ? num_cu : g.units;
-  const void* fn =
-      g.epi == kEpiLse
-          ? (g.queue ? (const void*)&gemm_bf16_kernel<false, true, kEpiLse>
-                     : (const void*)&gemm_bf16_kernel<false, false, kEpiLse>)
-          : (g.queue ? (const void*)&gemm_bf16_kernel<false, true, kEpiGrad>
-                     : (const void*)&gemm_bf16_kernel<false, false, kEpiGrad>);
+  const void* fn;
+  switch (g.epi) {
+    case kEpiLse:
+      fn = g.queue ? (const void*)&gemm_bf16_kernel<false, true, kEpiLse>
+                   : (const void*)&gemm_bf16_kernel<false, false, kEpiLse>;
+      break;
+    case kEpiGrad:
+      fn = g.queue ? (const void*)&gemm_bf16_kernel<false, true, kEpiGrad>
+                   : (const void*)&gemm_bf16_kernel<false, false, kEpiGrad>;
+      break;
+    case kEpiLseStore:
+      fn = g.queue ? (const void*)&gemm_bf16_kernel<false, true, kEpiLseStore>
+                   : (const void*)&gemm_bf16_kernel<false, false, kEpiLseStore>;
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
   void* args[] = {&g};
   return hipLaunchKernel(fn, dim3((unsigned)grid), dim3(kThreads), args, 0, stream);
 }
@@ -612,10 +634,12 @@ hipError_t launch_gemm_nt(GemmArgs g, bool beta, float* partial, int* queue, int
 
 hipError_t launch_transpose(TransposeArgs t, bool in_f32, hipStream_t stream) {
   if (t.R <= 0 || t.C <= 0) return hipSuccess;
+  if (t.gp && !in_f32) return hipErrorInvalidValue;
   const int64_t tiles = ((t.C + kTransposeTile - 1) / kTransposeTile) *
                         ((t.R + kTransposeTile - 1) / kTransposeTile);
-  const void* fn =
-      in_f32 ? (const void*)&transpose_kernel<float> : (const void*)&transpose_kernel<__bf16>;
+  const void* fn = t.gp    ? (const void*)&transpose_kernel<float, true>
+                   : in_f32 ? (const void*)&transpose_kernel<float>
+                            : (const void*)&transpose_kernel<__bf16>;
   void* args[] = {&t};
   return hipLaunchKernel(fn, dim3((unsigned)tiles), dim3(256), args, 0, stream);
 }

@@ -103,7 +103,8 @@ struct LmLayout {
   WsLayout loss;
   int64_t ldz, ldv, ldc, ntv;
   size_t z, wt, gt, ht, gb, part, queue, total;
-  size_t tpart, tzy, tgp;  // fused path: tile pairs, sampled logits, gradient parameters
+  size_t tpart, tzy, tgp;  // the product's (max, exp-sum) pairs, sampled logits, gradient
+                           // parameters of the chunk's rows
   bool fused;
 };
 inline LmLayout lm_layout(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_t n_seq,
@@ -120,17 +121,13 @@ inline LmLayout lm_layout(int64_t T, int64_t V, int64_t H, int64_t chunk, int64_
   M.queue = align_up(M.loss.total, 256);  // the products' work queues
   M.z = M.queue + 256;
   size_t end = M.z;
-  if (fused) {
-    M.tpart = end;
-    end += align_up((size_t)rows * (size_t)M.ntv * 8, 256);
-    M.tzy = end;
-    end += align_up((size_t)rows * 4, 256);
-    M.tgp = end;
-    end += align_up((size_t)rows * sizeof(GradParams), 256);
-  } else {
-    M.tpart = M.tzy = M.tgp = end;
-    end += align_up((size_t)rows * (size_t)M.ldz * 4, 256);
-  }
+  if (!fused) end += align_up((size_t)rows * (size_t)M.ldz * 4, 256);  // the chunk's logits
+  M.tpart = end;
+  end += align_up((size_t)rows * (size_t)M.ntv * 8, 256);
+  M.tzy = end;
+  end += align_up((size_t)rows * 4, 256);
+  M.tgp = end;
+  end += align_up((size_t)rows * sizeof(GradParams), 256);
   M.wt = M.gt = M.ht = M.gb = M.part = end;
   if (bwd) {
     end += align_up((size_t)H * (size_t)M.ldv * 2, 256);
@@ -282,11 +279,9 @@ struct RowVariant {
 };
 
 // Picks the variant for `nvec` 16-byte vectors per row; dtype is CIS_BF16 or CIS_F32. The
-// extended variants carry the operator family and the decoupled path in their epilogue;
-// bf16_grad selects, for float32 logits, a fused pass that writes the gradient in bf16.
+// extended variants carry the operator family and the decoupled path in their epilogue.
 const RowVariant& select_row_variant(int dtype, bool bwd, int32_t nvec);
-const RowVariant& select_row_variant_ext(int dtype, bool bwd, int32_t nvec,
-                                         bool bf16_grad = false);
+const RowVariant& select_row_variant_ext(int dtype, bool bwd, int32_t nvec);
 
 const void* finalize_kernel();
 const void* queue_reset_kernel();

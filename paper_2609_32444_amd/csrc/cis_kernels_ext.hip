@@ -12,16 +12,9 @@ static const RowVariant kBf16BwdExt[] = CIS_BWD_TABLE(Bf16);
 static const RowVariant kBf16FwdExt[] = CIS_FWD_TABLE(Bf16, 18);
 static const RowVariant kF32BwdExt[] = CIS_BWD_TABLE(F32);
 static const RowVariant kF32FwdExt[] = CIS_FWD_TABLE(F32, 15);
-// float32 logits with bf16 gradients (the LM-head path, whose rows are long): a short ladder
-static const RowVariant kF32Bf16BwdExt[] = {
-    CIS_VO(F32, Bf16, 64, 7, 0, true), CIS_VO(F32, Bf16, 256, 15, 0, true),
-    CIS_VO(F32, Bf16, 1024, 15, 0, false), CIS_VO(F32, Bf16, 1024, 18, 9, false)};
-
-const RowVariant& select_row_variant_ext(int dtype, bool bwd, int32_t nvec, bool bf16_grad) {
+const RowVariant& select_row_variant_ext(int dtype, bool bwd, int32_t nvec) {
   constexpr int nb = sizeof(kBf16BwdExt) / sizeof(kBf16BwdExt[0]);
   constexpr int nf = sizeof(kBf16FwdExt) / sizeof(kBf16FwdExt[0]);
-  constexpr int nn = sizeof(kF32Bf16BwdExt) / sizeof(kF32Bf16BwdExt[0]);
-  if (bwd && bf16_grad && dtype == CIS_F32) return pick_variant(kF32Bf16BwdExt, nn, nvec);
   const RowVariant* t = dtype == CIS_BF16 ? (bwd ? kBf16BwdExt : kBf16FwdExt)
                                           : (bwd ? kF32BwdExt : kF32FwdExt);
   return pick_variant(t, bwd ? nb : nf, nvec);

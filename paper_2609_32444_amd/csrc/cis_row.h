@@ -321,14 +321,10 @@ __device__ __forceinline__ u32x4 grad_vec(u32x4 zv, float b2, uint32_t sgn) {
   return E::pack(f) ^ u32x4{sgn, sgn, sgn, sgn};
 }
 
-// Gradient output of one 16-byte vector of logits. By default it has the logits' format and
-// position. GradOut<F32, Bf16> (float32 logits, bf16 gradient: the LM-head path) packs the four
-// values into 8 bytes at half the byte offset, in a separate gradient buffer.
-template <class E, class EO>
+// Gradient output of one 16-byte vector of logits, in the logits' format and position.
+template <class E>
 struct GradOut {
-  static_assert(__is_same(E, EO), "bf16 gradients of fp32 logits: GradOut<F32, Bf16>");
   typedef u32x4 vec;
-  static constexpr int kShift = 0;  // output byte offset = input byte offset >> kShift
   static constexpr uint32_t kSign = E::kSignMask;
   __device__ static __forceinline__ vec zero() { return u32x4{0u, 0u, 0u, 0u}; }
   __device__ static __forceinline__ vec make(u32x4 zv, float b2, uint32_t sgn) {
@@ -339,29 +335,6 @@ struct GradOut {
   }
   __device__ static __forceinline__ uint32_t elem(vec v, int e) { return E::elem_bits(v, e); }
 };
-template <class E>
-struct GradOutNarrow {
-  typedef u32x2 vec;
-  static constexpr int kShift = 1;
-  static constexpr uint32_t kSign = Bf16::kSignMask;
-  __device__ static __forceinline__ vec zero() { return u32x2{0u, 0u}; }
-  __device__ static __forceinline__ vec make(u32x4 zv, float b2, uint32_t sgn) {
-    float f[4];
-    F32::unpack(zv, f);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) f[e] = fast_exp2(__builtin_fmaf(f[e], kLog2e, -b2));
-    const bf16x2 lo = {(__bf16)f[0], (__bf16)f[1]}, hi = {(__bf16)f[2], (__bf16)f[3]};
-    return u32x2{__builtin_bit_cast(uint32_t, lo) ^ sgn, __builtin_bit_cast(uint32_t, hi) ^ sgn};
-  }
-  __device__ static __forceinline__ void store(vec v, __amdgpu_buffer_rsrc_t r, uint32_t o) {
-    __builtin_amdgcn_raw_buffer_store_b64(v, r, o >> 1, 0u, kAuxNT);
-  }
-  __device__ static __forceinline__ uint32_t elem(vec v, int e) {
-    return (v[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-  }
-};
-template <>
-struct GradOut<F32, Bf16> : GradOutNarrow<F32> {};
 
 // Exp-sum of one vector relative to mb = max*log2e, optionally leaving out element `skip`.
 template <class E>
@@ -684,10 +657,10 @@ __device__ __forceinline__ void row_invalid(const RowArgs& a, const RowScalars& 
 //   EXT: the epilogue also carries the operator family (rate-1 path, any token operator) and
 //        the decoupled PPO-clip path (weight from the pre-pass, clipped update ratio). The base
 //        kernels compute the CIS weight only, which keeps their registers for the row.
-template <class E, int BLOCK, int NV, int NL, bool BWD, bool PF, bool EXT, class EO = E>
+template <class E, int BLOCK, int NV, int NL, bool BWD, bool PF, bool EXT>
 __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
   static_assert(NL == 0 || (BWD && !PF), "LDS slots are for the fused pass");
-  using GO = GradOut<E, EO>;
+  using GO = GradOut<E>;
   constexpr int EPV = E::kPerVec;
   constexpr int NW = BLOCK / 64;
   __shared__ float sh_m[2][NW];
@@ -823,9 +796,9 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
     void* grow = BWD ? (void*)((char*)a.dlogits + row * a.grow_bytes) : nullptr;
     // write descriptor: complete vectors only
     const __amdgpu_buffer_rsrc_t ws = make_rsrc(
-        grow, BWD ? ((uint32_t)(g.nvec - (g.ragged ? 1 : 0)) * 16u) >> GO::kShift : 0u);
+        grow, BWD ? (uint32_t)(g.nvec - (g.ragged ? 1 : 0)) * 16u : 0u);
     const __amdgpu_buffer_rsrc_t wr =
-        make_rsrc(grow, BWD ? (uint32_t)(g.nres * BLOCK * 16) >> GO::kShift : 0u);
+        make_rsrc(grow, BWD ? (uint32_t)(g.nres * BLOCK * 16) : 0u);
     // the next row of this workgroup (prefetched during this row's last sweep)
     const bool nvalid = PF && cur.valid(V);
     const __amdgpu_buffer_rsrc_t nrs = row_rsrc(nrow, nvalid, g);
@@ -1123,9 +1096,9 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
         typename GO::vec out = GO::zero();
         if (valid) out = GO::make(bload(rs, (uint32_t)(g.nvec - 1) * 16u, 0u), b2, sgn);
         for (int e = 0; e < g.tail; ++e)
-          EO::store_elem(grow, (g.nvec - 1) * EPV + e, GO::elem(out, e));
+          E::store_elem(grow, (g.nvec - 1) * EPV + e, GO::elem(out, e));
       }
-      if (valid && y_mine) EO::store_elem(grow, y, EO::bits_of(coef * one_m_p));
+      if (valid && y_mine) E::store_elem(grow, y, E::bits_of(coef * one_m_p));
     }
     row = nrow;
     nrow = nn;
@@ -1138,9 +1111,6 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 // ------------------------------------------------------------------------------------------
 #define CIS_V(E, B, N, L, BWD, PF) \
   RowVariant{B, N, L, (const void*)&cis_row_kernel<E, B, N, L, BWD, PF, CIS_EXT>}
-// fused-pass variant with a gradient format other than the logits' (GradOut<E, EO>)
-#define CIS_VO(E, EO, B, N, L, PF) \
-  RowVariant{B, N, L, (const void*)&cis_row_kernel<E, B, N, L, true, PF, CIS_EXT, EO>}
 
 // Row capacity of a variant: block*(nv+1) vectors (block*(nv+nl) with LDS slots); a row goes
 // to the first variant that holds it. The ladders were chosen by timing every (block, nv)
@@ -1153,14 +1123,13 @@ __global__ __launch_bounds__(BLOCK) void cis_row_kernel(const RowArgs a) {
 // bf16) 1024 x 3 without the prefetch took over once loads were issued in slot order and the
 // queue tickets were drawn ahead of the stores: 0.625 ms against 0.635 for 512 x 7 without and
 // 0.657 with the prefetch, 0.658 for 256 x 15 with it and 0.677 without.
-#define CIS_BWD_TABLE_OUT(E, EO)                                                            \
-  {CIS_VO(E, EO, 64, 1, 0, true),     CIS_VO(E, EO, 64, 3, 0, true),                        \
-   CIS_VO(E, EO, 64, 7, 0, true),     CIS_VO(E, EO, 64, 15, 0, true),                       \
-   CIS_VO(E, EO, 512, 3, 0, false),   CIS_VO(E, EO, 1024, 3, 0, false),                    \
-   CIS_VO(E, EO, 1024, 7, 0, false),  CIS_VO(E, EO, 1024, 11, 0, false),                    \
-   CIS_VO(E, EO, 1024, 15, 0, false), CIS_VO(E, EO, 1024, 18, 0, false),                    \
-   CIS_VO(E, EO, 1024, 18, 9, false)}
-#define CIS_BWD_TABLE(E) CIS_BWD_TABLE_OUT(E, E)
+#define CIS_BWD_TABLE(E)                                                                    \
+  {CIS_V(E, 64, 1, 0, true, true),     CIS_V(E, 64, 3, 0, true, true),                      \
+   CIS_V(E, 64, 7, 0, true, true),     CIS_V(E, 64, 15, 0, true, true),                     \
+   CIS_V(E, 512, 3, 0, true, false),   CIS_V(E, 1024, 3, 0, true, false),                   \
+   CIS_V(E, 1024, 7, 0, true, false),  CIS_V(E, 1024, 11, 0, true, false),                  \
+   CIS_V(E, 1024, 15, 0, true, false), CIS_V(E, 1024, 18, 0, true, false),                  \
+   CIS_V(E, 1024, 18, 9, true, false)}
 #define CIS_FWD_TABLE(E, LAST)                                                              \
   {CIS_V(E, 64, 1, 0, false, true),    CIS_V(E, 64, 3, 0, false, true),                     \
    CIS_V(E, 64, 7, 0, false, true),    CIS_V(E, 64, 15, 0, false, true),                    \
