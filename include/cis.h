@@ -338,15 +338,16 @@ int cis_loss_bwd_ex(const void* logits, int dtype, int64_t T, int64_t V, int64_t
  * The forward never stores the logits: the product's epilogue reduces each row's float32
  * logits to one (max, exp-sum) pair per 64 columns, and a per-row pass folds them. The
  * backward has two ways to obtain G: by default each chunk's float32 logits are kept in the
- * workspace (one chunk at a time) and the row kernel turns them into G; with recompute = 1
- * they are never stored, and the product is formed a second time with an epilogue that writes
- * G (four products instead of three, and 4 * min(T, chunk) * V bytes less workspace).
+ * workspace (one chunk at a time) beside the pairs, and one tiled pass over them writes G and
+ * its transpose; with recompute = 1 they are never stored, and the product is formed a second
+ * time with an epilogue that writes G (four products instead of three, and
+ * 4 * min(T, chunk) * V bytes less workspace).
  * ========================================================================================= */
 
 /* Workspace bytes for cis_lmhead_loss_fwd (with_grad = 0), cis_lmhead_loss_bwd (with_grad = 1)
  * or cis_lmhead_loss_bwd with recompute (with_grad = 2): the loss workspace of
- * cis_workspace_bytes_ex plus, per chunk row, 8 bytes per 64 vocabulary columns and 20 bytes
- * (with_grad = 0 or 2) or the row's float32 logits (with_grad = 1), and with gradients W^T, the
+ * cis_workspace_bytes_ex plus, per chunk row, 8 bytes per 64 vocabulary columns and 20 bytes,
+ * and the row's float32 logits (with_grad = 1), and with gradients W^T, the
  * chunk's bf16 dL/dz and the transposed operands of one dL/dW group (about 2*V*H + 2*V*chunk +
  * 2*(V + H)*min(T, group) bytes; group as for cis_lmhead_loss_bwd). Returns 0 for T < 0, V
  * outside [1, 2^22], H outside [1, 2^16], chunk outside [1, 2^16], n_seq < 0 or with_grad

@@ -73,14 +73,13 @@ constexpr size_t ws_bytes(int64_t T) { return ws_layout(T, 0).total; }
 
 // LM-head workspace: the loss workspace above, then (256-byte aligned)
 //   Q   int[kGemmQueues]   the products' work queues (256 bytes)
-//   Z   float[rows, ldz]   the chunk's logits (materialising path only), or, on the fused path
-//                          that never stores them, per row and 64-column block the pair
-//                          (max, exp-sum) (float2[rows, ntv]), the sampled logit (float[rows])
-//                          and the gradient parameters (GradParams[rows])
+//   Z   float[rows, ldz]   the chunk's logits (the default backward only)
+//   then per row and 64-column block the pair (max, exp-sum) (float2[rows, ntv]), the sampled
+//   logit (float[rows]) and the gradient parameters (GradParams[rows])
 //   Wt  bf16[H, ldv]       W^T (backward)
 //   Gt  bf16[V, ldc]       (dL/dz)^T of the rows of a dL/dW group (backward)
 //   Ht  bf16[H, ldc]       their hidden states transposed (backward)
-//   Gb  bf16[rows, ldv]    dL/dz of the chunk in bf16, written by the loss rows (backward)
+//   Gb  bf16[rows, ldv]    dL/dz of the chunk in bf16 (backward)
 //   P   float[kLmSplits, rows, H]  split-K partials of dL/dh (backward)
 // with rows = min(T, chunk), ldc = min(T, lm_dw_rows(chunk)) and row strides rounded up to 8
 // elements.

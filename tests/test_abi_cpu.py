@@ -203,13 +203,14 @@ def test_lmhead_workspace_bytes():
     T, V, H = 16384, 151936, 2048
     fwd, bwd = f(T, V, H, 4096, 0, False), f(T, V, H, 4096, 0, True)
     loss = 256 + 18 * T
-    # the loss rows' scratch plus, per chunk row, one (max, exp-sum) pair per 256 columns, the
+    # the loss rows' scratch plus, per chunk row, one (max, exp-sum) pair per 64 columns, the
     # sampled logit and the gradient parameters: the logits themselves are never stored
     ntv = (V + 255) // 256 * 4
     assert fwd >= loss + 4096 * (8 * ntv + 4 + 16) and fwd % 256 == 0
     assert fwd < 4096 * V                       # far less than one float32 chunk of logits
-    # the backward adds W^T, the chunk's bf16 gradient and the two transposed operands
-    assert bwd >= fwd + 2 * V * H + 2 * 4096 * V + 2 * (V + H) * 4096
+    # the backward adds the chunk's float32 logits, W^T, the chunk's bf16 gradient and the two
+    # transposed operands
+    assert bwd >= fwd + 4 * 4096 * V + 2 * V * H + 2 * 4096 * V + 2 * (V + H) * 4096
     # a chunk larger than the batch only needs the batch's rows
     assert f(100, 1000, 64, 4096, 0, True) == f(100, 1000, 64, 100, 0, True)
     assert f(T, V, H, 4096, 10, True) >= bwd
@@ -217,9 +218,9 @@ def test_lmhead_workspace_bytes():
                 (T, V, 1 << 17, 1), (T, V, H, 1 << 17)):
         assert f(*bad, 0, True) == 0, bad
     assert f(T, V, H, 64, -1, True) == 0
-    # the backward that never stores the logits needs the forward's pairs, not a chunk of logits
+    # the backward that never stores the logits needs exactly one float32 chunk less
     rec = cis.lmhead_workspace_bytes(T, V, H, 4096, 0, True, recompute=True)
-    assert rec < bwd - 4 * 4096 * V + 4096 * (8 * ntv + 20) + 256 * 4
+    assert 4 * 4096 * V <= bwd - rec <= 4 * 4096 * (V + 8) + 256
     assert rec >= fwd + 2 * V * H + 2 * 4096 * V
     assert cis.load_library().cis_lmhead_workspace_bytes(T, V, H, 4096, 0, 3) == 0
 
