@@ -130,34 +130,71 @@ static_assert(kGemmBK == 64 && kThreads * 8 / 64 * kALoads == kGemmTile,
               "a slab row is 8 chunks; each load covers 64 rows");
 
 // One slab of MFMAs for a wave's kTm x kTn blocks: two 32-steps, the fragments of the second
-// read from LDS while the first is multiplied. Each step's 12 reads have landed before the next
-// step's are issued: the LDS counter tracks at most 15, and with 24 in flight the compiler
-// would wait for all of them before the first MFMA. fa(i, s) / fb(j, s) give fragment addresses.
-template <class FA, class FB>
+// read from LDS while the first is multiplied. fa(i, s) / fb(j, s) give fragment addresses.
+//   SPLIT = false: each step's 12 reads have landed before the next step's are issued (the LDS
+//     counter tracks at most 15 reads; with 24 in flight the compiler would wait for all of
+//     them before the first MFMA).
+//   SPLIT = true: the first step's fragments are read B first, then A row by row, and each row
+//     of MFMAs waits only for its own fragments (the compiler's counted LDS waits), so the
+//     first MFMAs after the slab barrier start once five reads have landed. The second step's
+//     12 reads are issued after row kSplitRow of the first step, which keeps every wait within
+//     the counter's 15.
+constexpr int kSplitRow = 4;
+template <bool SPLIT, class FA, class FB>
 __device__ __forceinline__ void mfma_slab(f32x4 (&acc)[kTm][kTn], FA fa, FB fb) {
-  constexpr int KS = kGemmBK / 32;
-  bf16x8 a[2][kTm], b[2][kTn];
+  static_assert(kGemmBK == 64, "two 32-steps per slab");
+  static_assert((kTm - 1 - kSplitRow) + kTm + kTn <= 15, "waits stay within the LDS counter");
+  bf16x8 a0[kTm], b0[kTn], a1[kTm], b1[kTn];
+  auto row = [&](int i, const bf16x8(&a)[kTm], const bf16x8(&b)[kTn]) {
 #pragma unroll
-  for (int i = 0; i < kTm; ++i) a[0][i] = *(const bf16x8*)fa(i, 0);
+    for (int j = 0; j < kTn; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
+  };
+  // SPLIT reads B first (every row of MFMAs needs all of B); otherwise A first
+  auto read = [&](int s, bf16x8(&a)[kTm], bf16x8(&b)[kTn]) {
+    if constexpr (SPLIT) {
 #pragma unroll
-  for (int j = 0; j < kTn; ++j) b[0][j] = *(const bf16x8*)fb(j, 0);
+      for (int j = 0; j < kTn; ++j) b[j] = *(const bf16x8*)fb(j, s);
+    }
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    const int c = ks & 1;
+    for (int i = 0; i < kTm; ++i) a[i] = *(const bf16x8*)fa(i, s);
+    if constexpr (!SPLIT) {
+#pragma unroll
+      for (int j = 0; j < kTn; ++j) b[j] = *(const bf16x8*)fb(j, s);
+    }
+  };
+  read(0, a0, b0);
+  if constexpr (SPLIT) {
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < kSplitRow; ++i) {
+      row(i, a0, b0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    read(1, a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = kSplitRow; i < kTm; ++i) {
+      row(i, a0, b0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = 0; i < kTm; ++i) {
+      row(i, a1, b1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt at their maxima
     __builtin_amdgcn_sched_barrier(0);
-    if (ks + 1 < KS) {
-#pragma unroll
-      for (int i = 0; i < kTm; ++i) a[c ^ 1][i] = *(const bf16x8*)fa(i, ks + 1);
-#pragma unroll
-      for (int j = 0; j < kTn; ++j) b[c ^ 1][j] = *(const bf16x8*)fb(j, ks + 1);
-    }
+    read(1, a1, b1);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int i = 0; i < kTm; ++i)
+    for (int i = 0; i < kTm; ++i) row(i, a0, b0);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int j = 0; j < kTn; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[c][j], a[c][i], acc[i][j], 0, 0, 0);
+    for (int i = 0; i < kTm; ++i) row(i, a1, b1);
     __builtin_amdgcn_sched_barrier(0);
   }
 }
@@ -313,7 +350,7 @@ struct EpiRows {
   int y[kGemmTile];            // sampled id, or -1 when outside [0, N)
 };
 
-template <bool BETA, int EPI = kEpiStore>
+template <bool BETA, int EPI, bool SPLIT>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t tn,
                                           int64_t split, __bf16 (&lds)[2 * kSlab], EpiRows& er) {
   constexpr int BM = kGemmTile, BN = kGemmTile, BK = kGemmBK;
@@ -395,7 +432,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t tm, int64_t
     const __bf16* st = lds + (int)(kt & 1) * kSlab;
     const __bf16* la = st + (wm * kGemmWaveM + fr) * BK;
     const __bf16* lb = st + (BM + wn * kGemmWaveN + fr) * BK;
-    mfma_slab(acc, [&](int i, int s) { return la + i * 16 * BK + ((4 * s + fq) ^ sw) * 8; },
+    mfma_slab<SPLIT>(acc, [&](int i, int s) { return la + i * 16 * BK + ((4 * s + fq) ^ sw) * 8; },
               [&](int j, int s) { return lb + j * 16 * BK + ((4 * s + fq) ^ sw) * 8; });
   }
 
@@ -432,7 +469,11 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(const GemmArgs g) {
     if (u < 0) break;
     int64_t tm, tn, split;
     unit_tile<kGemmTile, kGemmTile>(g, u, tm, tn, split);
-    gemm_tile<BETA, EPI>(g, tm, tn, split, lds, er);
+    // The split fragment reads where the compiler keeps the K loop free of full vmcnt waits:
+    // in the other forms it placed a vmcnt(0) before the first step's A reads, which also
+    // waits for the next slab's loads.
+    constexpr bool kSplitReads = EPI == kEpiLse || (EPI == kEpiLseStore && QUEUED);
+    gemm_tile<BETA, EPI, kSplitReads>(g, tm, tn, split, lds, er);
     if (!QUEUED) break;
   }
 }
