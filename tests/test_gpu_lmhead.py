@@ -258,6 +258,22 @@ def test_lmhead_products_with_more_tiles_than_cus():
 
 
 @pytest.mark.parametrize("recompute", [False, True], ids=["chunked_logits", "recompute"])
+def test_lmhead_queued_products_ragged_hidden(recompute):
+    """H = 200 (three full 64-wide slabs and a masked one of 8) with a logits product of 314
+    tiles: the queued products (with the stored chunk and pairs, or pairs then G) end their
+    contraction on the masked slab, which is filled through registers. Against the oracle,
+    and a second call reproduces every output bit for bit."""
+    b = make_lmhead_batch(512, 40000, 200, device=DEV, seed=31, min_len=16, max_len=96)
+    out, _ = run_case("queued_ragged_hidden", b, chunk=512, recompute=recompute)
+    prm, _ = make_params(X.OP_CIS, dict(lam=b.lam, kappa=b.kappa), b.scale)
+    again = cis.lmhead_loss_bwd(b.hidden, b.weight, b.ids, b.logp_infer, b.adv, b.mask,
+                                params=prm, chunk=512, recompute=recompute)
+    torch.cuda.synchronize()
+    for k in ("logp_train", "w", "acted", "terms", "eps", "loss", "dhidden", "dweight"):
+        assert torch.equal(out[k], again[k]), k
+
+
+@pytest.mark.parametrize("recompute", [False, True], ids=["chunked_logits", "recompute"])
 def test_lmhead_largest_vocabulary(recompute):
     """V = 2^22, the largest vocabulary the LM-head calls accept: float32 logit rows of 16 MB
     through the streamed row path (or 65536 pairs per row folded by the combine), a logits
